@@ -1,0 +1,211 @@
+#!/usr/bin/env python3
+"""Benchmark of the link-stage attention hot path on one MI355X.
+
+One step = one pic_link_attn (or pic_link_decode) call over the whole batch
+of the workload: host chunk-id resolution and chunk-table upload, the
+attention kernel, and the split-K combine when used. The chunk store is
+filled (compile side, not timed) before the timed region, so every input is
+resident in HBM when timing starts.
+
+Default workload: the Llama-3-8B-shaped prefill link (H_q 32, H_kv 8, d 128,
+8 requests x 10 linked chunks of 512 tokens + 256 query tokens with causal own
+KV, bf16). Prints one JSON line.
+
+Algorithmic work counts visible (query, key) pairs only:
+  FLOPs = sum_r H_q (2 d_k + 2 d_v) P_r,  P_r = L_q L_d + sum_{i<L_q} (i + 1 + L_s - L_q)
+  bytes = Q + out + lse + own KV + each linked chunk's KV once.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_BF16_TFLOPS = 2500.0     # MI355X dense bf16 matrix peak
+PEAK_HBM_GBS = 8000.0         # MI355X HBM3E
+PEAK_FP32_VALU_TFLOPS = 157.3
+
+
+def algorithmic(cfg, wl):
+    from paper_2602_01519_amd import workloads as W
+    pairs = W.visible_pairs(cfg, wl.plan)
+    flops = pairs * cfg.n_q_heads * (2 * cfg.d_k + 2 * cfg.d_v)
+    esz = cfg.elem_bytes
+    tq = wl.q.shape[0]
+    ts = 0 if wl.k_self is None else wl.k_self.shape[0]
+    kv_tok = cfg.n_kv_heads * (cfg.d_k + (cfg.d_v if cfg.kind == W.GQA else 0)) * esz
+    chunk_bytes = sum(cfg.chunk_length(int(c)) for c in wl.used_chunks()) * kv_tok
+    nbytes = (tq * cfg.n_q_heads * (cfg.d_k + cfg.d_v) * esz + tq * cfg.n_q_heads * 4 +
+              ts * kv_tok + chunk_bytes)
+    return flops, nbytes
+
+
+def cpu_baseline(cfg, wl, dw, budget_s: float):
+    """Times the fp64 oracle on a bounded sample of whole requests (host cores),
+    and checks the GPU output of the sampled requests against it."""
+    import oracle
+    from paper_2602_01519_amd import workloads as W
+    p = wl.plan
+    flops_req = []
+    for r in range(p.batch):
+        sub = W.Plan(p.chunk_offsets[r:r + 2] - p.chunk_offsets[r], p.chunk_index[p.chunk_offsets[r]:p.chunk_offsets[r + 1]],
+                     p.q_offsets[r:r + 2] - p.q_offsets[r],
+                     None if p.self_offsets is None else p.self_offsets[r:r + 2] - p.self_offsets[r])
+        flops_req.append(W.visible_pairs(cfg, sub) * cfg.n_q_heads * (2 * cfg.d_k + 2 * cfg.d_v))
+    order = list(range(p.batch))
+    done, t_used, flops_done = [], 0.0, 0
+    out_gpu, _ = dw.results()
+    max_err = 0.0
+    for r in order:
+        if t_used > budget_s and done:
+            break
+        idx = p.chunk_index[p.chunk_offsets[r]:p.chunk_offsets[r + 1]]
+        links = [[dw.chunks[int(c)] if int(c) in dw.chunks else W.make_chunk(cfg, int(c)) for c in idx]]
+        qs = slice(p.q_offsets[r], p.q_offsets[r + 1])
+        so = None
+        ks = vs = None
+        if p.self_offsets is not None:
+            ss = slice(p.self_offsets[r], p.self_offsets[r + 1])
+            ks = wl.k_self[ss]
+            vs = None if wl.v_self is None else wl.v_self[ss]
+            so = np.array([0, ss.stop - ss.start], np.int32)
+        t0 = time.perf_counter()
+        ref, _ = oracle.link_attn(dtype=cfg.dtype, mla=cfg.kind == W.MLA, n_q_heads=cfg.n_q_heads,
+                                  d_v=cfg.d_v, links=links, q=wl.q[qs],
+                                  q_offsets=np.array([0, qs.stop - qs.start], np.int32), k_self=ks,
+                                  v_self=vs, self_offsets=so, tau=float(np.float32(cfg.scale)))
+        t_used += time.perf_counter() - t0
+        flops_done += flops_req[r]
+        done.append(r)
+        max_err = max(max_err, float(np.abs(out_gpu[qs] - ref).max()))
+    return {
+        "value": flops_done / t_used / 1e12,
+        "unit": "TFLOP/s",
+        "cores": oracle.num_threads(),
+        "kind": "oracle",
+        "sample": f"requests {done} of {p.batch} (all query rows and heads), fp64, {t_used:.1f} s",
+        "gpu_max_abs_err_on_sample": max_err,
+    }
+
+
+def main(argv=None):
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--config", default="llama_prefill",
+                    help="workload: tiny_f32, llama_prefill, long_rag, decode, mla")
+    ap.add_argument("--cpu-budget", type=float, default=15.0,
+                    help="seconds of oracle time for the CPU baseline (0 = skip)")
+    args = ap.parse_args(argv)
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported "
+              f"(the link path shards by request with no exchange, see the design notes)",
+              file=sys.stderr)
+        return 2
+
+    import torch
+    from paper_2602_01519_amd import pic, runner
+    from paper_2602_01519_amd import workloads as W
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        return 2
+    torch.cuda.set_device(0)
+    cfg = W.CONFIGS[args.config]
+    wl = W.make_workload(cfg)
+    keep = set(int(c) for c in wl.plan.chunk_index[wl.plan.chunk_offsets[0]:wl.plan.chunk_offsets[min(4, wl.plan.batch)]])
+    dw = runner.upload(wl, keep_host=keep)
+    stream = torch.cuda.current_stream()
+    for _ in range(args.warmup):
+        dw.run()
+    torch.cuda.synchronize()
+
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    pic.prof_begin()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    ev0.record(stream)
+    for _ in range(args.steps):
+        dw.run()
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    kern_ms, launches, kname = pic.prof_end()
+    step_ms = ev0.elapsed_time(ev1) / args.steps
+    kern_avg_ms = kern_ms / max(launches, 1)
+
+    flops, nbytes = algorithmic(cfg, wl)
+    tflops = flops / (step_ms * 1e-3) / 1e12
+    gbs = nbytes / (step_ms * 1e-3) / 1e9
+    if cfg.dtype == W.F32:
+        bound, peak, unit, achieved = "alu", PEAK_FP32_VALU_TFLOPS, "TFLOP/s", flops / (kern_avg_ms * 1e-3) / 1e12
+    elif cfg.decode:
+        bound, peak, unit, achieved = "hbm", PEAK_HBM_GBS, "GB/s", nbytes / (kern_avg_ms * 1e-3) / 1e9
+    else:
+        bound, peak, unit, achieved = "mfma", PEAK_BF16_TFLOPS, "TFLOP/s", flops / (kern_avg_ms * 1e-3) / 1e12
+
+    cpu = None
+    if args.cpu_budget > 0:
+        cpu = cpu_baseline(cfg, wl, dw, args.cpu_budget)
+    dw.close()
+
+    line = {
+        "metric": "link-attn TFLOP/s (algorithmic, visible pairs) at 1 GPU",
+        "value": round(tflops, 3),
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(step_ms, 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32" if cfg.dtype == W.F32 else "bf16",
+        "data": "synthetic (seeded N(0,1), shapes of the paper's Llama-3.1-8B / DeepSeek-V2-Lite backbones)",
+        "config": {
+            "workload": cfg.name,
+            "batch": cfg.batch,
+            "n_q_heads": cfg.n_q_heads,
+            "n_kv_heads": cfg.n_kv_heads,
+            "d_k": cfg.d_k,
+            "d_v": cfg.d_v,
+            "links_per_request": list(cfg.links),
+            "chunk_tokens": cfg.chunk_len,
+            "query_tokens": cfg.q_len,
+            "own_tokens": cfg.self_len,
+            "entry": "pic_link_decode" if cfg.decode else "pic_link_attn",
+        },
+        "us_per_request": round(step_ms * 1e3 / cfg.batch, 3),
+        "hbm_gbs_algorithmic": round(gbs, 1),
+        "hbm_frac": round(gbs / PEAK_HBM_GBS, 4),
+        "mfma_frac": round(tflops / PEAK_BF16_TFLOPS, 4) if cfg.dtype == W.BF16 else None,
+        "algorithmic_flops_per_step": flops,
+        "algorithmic_bytes_per_step": nbytes,
+        "wall_s_timed": round(wall, 4),
+        "roofline": {
+            "kernel": kname,
+            "bound": bound,
+            "achieved": round(achieved, 3),
+            "peak": peak,
+            "unit": unit,
+            "frac": round(achieved / peak, 4),
+            "traffic": None,
+            "kernel_avg_us": round(kern_avg_ms * 1e3, 3),
+            "launches": launches,
+        },
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(line), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

@@ -1,0 +1,173 @@
+/*
+ * pic.h -- link-stage attention over position-independent chunk caches, on
+ * one AMD Instinct MI355X (gfx950).
+ *
+ * The method (Comb, "You Need an Encoder for Native Position-Independent
+ * Caching"): each static context chunk is compiled once into key/value
+ * caches computed from position zero (Sec. 1, Fig. 1; Sec. 4.2 stores the
+ * cross-attention K and V). A request is a question plus zero or more
+ * contexts in any order (Sec. 3). In the link stage the request's chunk
+ * caches are looked up by id (Sec. 3, step 1), concatenated in request order
+ * along the document axis (Sec. 4.2), and the request's dynamic tokens
+ * attend over them -- without a mask (cross-attention, Sec. 4.2 Eq. 7-8) --
+ * and over their own KV under a causal mask (Sec. 4.1 Eq. 2-3), all under
+ * one softmax here. The PIC allocator owns a pool of GPU memory reserved
+ * when the system starts (Sec. 5.3).
+ *
+ * Math computed for request r, query row i (0 <= i < L_q), query head h:
+ *   keys  = [ K_{c_1} ; ... ; K_{c_n} ; K_own[0 .. i + L_s - L_q] ]
+ *   s_j   = softmax_scale * <q[i,h], keys_j[h / (H_q/H_kv)]>
+ *   out[i,h] = sum_j softmax(s)_j * values_j[h / (H_q/H_kv)]
+ *   lse[i,h] = log(sum_j exp(s_j))   (natural log; -inf and out = 0 if no key)
+ * The query rows are the last L_q of the L_s own tokens (bottom-right causal
+ * alignment): new tokens are appended to the query sequence (Sec. 4).
+ * MLA (absorbed latent form, Sec. 5.1 DeepSeek-V2-Lite backbone): one KV
+ * "head" whose rows are [latent | rope] (d_k wide); the value of a row is its
+ * first d_v entries, and the output is the latent (d_v wide) per head.
+ *
+ * Conventions for every call:
+ *   - Status codes are negative on error. All validation happens on the host
+ *     before any device work: an error launches nothing and writes nothing.
+ *     pic_last_error() gives a thread-local message about the last error.
+ *   - Device pointers are HIP device allocations on the current device;
+ *     "host" arrays are ordinary host memory, read before the call returns.
+ *   - `stream` is a hipStream_t (NULL = the null stream). All device work is
+ *     enqueued on it; calls return before it runs.
+ *   - Tensors are dense, row-major, with no padding, in the store's dtype
+ *     (fp32, or bf16 as raw 16-bit patterns) unless stated; lse is fp32.
+ *   - One host thread uses a store at a time. Outputs of calls that are in
+ *     flight on different streams must not alias.
+ */
+#ifndef PIC_H
+#define PIC_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  PIC_OK = 0,
+  PIC_ERR_INVALID = -1,      /* bad argument, shape or layout */
+  PIC_ERR_NOT_FOUND = -2,    /* a linked chunk id is not in the store */
+  PIC_ERR_EXISTS = -3,       /* put of an id already stored (chunks are immutable) */
+  PIC_ERR_OOM = -4,          /* the store's pool has no room */
+  PIC_ERR_HIP = -5,          /* a HIP runtime call failed */
+  PIC_ERR_UNSUPPORTED = -6   /* valid request this build has no kernel for */
+} pic_status;
+
+enum { PIC_F32 = 0, PIC_BF16 = 1 };     /* pic_store_desc.dtype */
+enum { PIC_GQA = 0, PIC_MLA = 1 };      /* pic_store_desc.kind  */
+
+/* Shape of one layer's chunk caches. d_k and d_v must be multiples of 8.
+ * GQA: n_kv_heads >= 1, separate K [.., d_k] and V [.., d_v] per head.
+ * MLA: n_kv_heads == 1, d_v <= d_k, the value is the first d_v of each key row.
+ * capacity_tokens: pool size in tokens. Each chunk occupies its length
+ * rounded up to a multiple of 64 tokens. */
+typedef struct pic_store_desc {
+  int32_t kind;
+  int32_t dtype;
+  int32_t n_kv_heads;
+  int32_t d_k;
+  int32_t d_v;
+  int32_t reserved;          /* must be 0 */
+  int64_t capacity_tokens;
+} pic_store_desc;
+
+typedef struct pic_store pic_store;
+
+/* Creates a chunk store on the current HIP device and reserves its pool
+ * (the PIC allocator's reservation, Sec. 5.3). *out receives the handle.
+ * Errors: INVALID (desc), UNSUPPORTED (shape), HIP (allocation failed). */
+pic_status pic_store_create(const pic_store_desc *desc, pic_store **out);
+
+/* Waits for the device, then frees the store and everything it owns.
+ * NULL is accepted and ignored. */
+pic_status pic_store_destroy(pic_store *store);
+
+/* Compile-stage entry (Sec. 3 steps 3-4): copies one chunk's caches into the
+ * pool and records chunk_id -> slot in the store's hash table.
+ *   k: device, token-major [n_tokens][n_kv_heads][d_k]
+ *   v: device, token-major [n_tokens][n_kv_heads][d_v] for GQA; NULL for MLA
+ * The copy (into the store's internal layout) is ordered on `stream`; the
+ * caller may reuse k and v once the stream has passed it.
+ * Errors: INVALID, EXISTS (id present), OOM (pool full), HIP. */
+pic_status pic_store_put(pic_store *store, uint64_t chunk_id, int64_t n_tokens, const void *k,
+                         const void *v, void *stream);
+
+/* Hash-table lookup (Sec. 3 step 1): *n_tokens_out = the chunk's length.
+ * Errors: INVALID, NOT_FOUND. */
+pic_status pic_store_lookup(const pic_store *store, uint64_t chunk_id, int64_t *n_tokens_out);
+
+/* Pool usage in (padded) tokens and the number of stored chunks. Any output
+ * pointer may be NULL. */
+pic_status pic_store_usage(const pic_store *store, int64_t *used_tokens,
+                           int64_t *capacity_tokens, int64_t *n_chunks);
+
+/* A batch of requests (Sec. 3: a question plus zero or more contexts).
+ * All arrays are host memory with batch+1 non-decreasing entries from 0.
+ *   chunk_offsets/chunk_ids: the links of request r, in request order, are
+ *     chunk_ids[chunk_offsets[r] .. chunk_offsets[r+1]-1]; an id may repeat.
+ *   q_offsets: the query tokens of request r are rows q_offsets[r].. of q.
+ *   self_offsets: own-KV tokens of request r (L_s >= L_q), or NULL for
+ *     cross-attention only (no own KV, every row sees only the documents). */
+typedef struct pic_link_req {
+  int32_t batch;
+  int32_t reserved;          /* must be 0 */
+  const int32_t *chunk_offsets;
+  const uint64_t *chunk_ids;
+  const int32_t *q_offsets;
+  const int32_t *self_offsets;
+} pic_link_req;
+
+/* Link-stage attention for prefill-shaped requests (Sec. 4.1-4.2).
+ *   q      device [Tq][n_q_heads][d_k], Tq = q_offsets[batch]
+ *   k_self device [Ts][n_kv_heads][d_k], Ts = self_offsets[batch] (NULL if none)
+ *   v_self device [Ts][n_kv_heads][d_v] (GQA), NULL for MLA
+ *   out    device [Tq][n_q_heads][d_v], store dtype
+ *   lse    device [Tq][n_q_heads] fp32 natural-log log-sum-exp, or NULL
+ * n_q_heads must be a multiple of n_kv_heads. softmax_scale (positive,
+ * finite) multiplies the dot products (Eq. 2 and 7 use 1/sqrt(d)). The chunk table of the call is
+ * copied to the device on `stream`; all host arrays are consumed on return.
+ * Errors: INVALID, NOT_FOUND, UNSUPPORTED, HIP. */
+pic_status pic_link_attn(pic_store *store, const pic_link_req *req, int32_t n_q_heads,
+                         const void *q, const void *k_self, const void *v_self,
+                         float softmax_scale, void *out, float *lse, void *stream);
+
+/* Link-stage attention for decode-shaped requests (few query tokens each):
+ * the same function as pic_link_attn (a generated token is treated like a
+ * query token, Sec. 4), computed by splitting each request's keys into
+ * num_splits ranges whose partial softmax states are merged exactly
+ * (log-sum-exp). num_splits = 0 lets the library choose; otherwise 1..256.
+ * Each request may have at most 16 query tokens.
+ * Errors: as pic_link_attn. */
+pic_status pic_link_decode(pic_store *store, const pic_link_req *req, int32_t n_q_heads,
+                           const void *q, const void *k_self, const void *v_self,
+                           float softmax_scale, int32_t num_splits, void *out, float *lse,
+                           void *stream);
+
+/* Test hook: materialises the concatenation (Sec. 4.2) of the listed chunks
+ * in the given order, reading the pool through the same address resolution
+ * the attention kernels use. k_out: device token-major [sum len][H_kv][d_k];
+ * v_out: device [sum len][H_kv][d_v] (GQA) or NULL (MLA). Bit-exact copies.
+ * Errors: INVALID, NOT_FOUND, HIP. */
+pic_status pic_debug_gather(pic_store *store, const uint64_t *ids, int32_t n, void *k_out,
+                            void *v_out, void *stream);
+
+/* Kernel timing for measurement. pic_prof_begin() clears and enables
+ * recording of HIP events around every launch of the main attention kernel;
+ * pic_prof_end() waits for them, disables recording and returns the summed
+ * kernel time in milliseconds, the launch count and the kernel's name
+ * (name_buf may be NULL). */
+pic_status pic_prof_begin(void);
+pic_status pic_prof_end(double *kernel_ms, int64_t *launches, char *name_buf, int32_t name_len);
+
+const char *pic_status_str(pic_status status);
+const char *pic_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* PIC_H */

@@ -1,0 +1,467 @@
+// Store layout transforms, the gather test hook, the generic vector-ALU link
+// attention and the split-K log-sum-exp combine. gfx950 only.
+#include "pic_internal.hpp"
+
+#include <cmath>
+
+namespace pic {
+namespace {
+
+__device__ __forceinline__ float to_f32(float x) { return x; }
+__device__ __forceinline__ float to_f32(uint16_t b) { return __uint_as_float((uint32_t)b << 16); }
+
+// fp32 -> bf16, round to nearest even (NaN stays NaN).
+__device__ __forceinline__ uint16_t bf16_rne(float f) {
+  uint32_t u = __float_as_uint(f);
+  if ((u & 0x7fffffffu) > 0x7f800000u) return 0x7fc0;
+  u += 0x7fffu + ((u >> 16) & 1u);
+  return (uint16_t)(u >> 16);
+}
+template <typename T> __device__ __forceinline__ T from_f32(float x);
+template <> __device__ __forceinline__ float from_f32<float>(float x) { return x; }
+template <> __device__ __forceinline__ uint16_t from_f32<uint16_t>(float x) { return bf16_rne(x); }
+
+// ---------------------------------------------------------------------------
+// Store layout transforms (the compile-side put; not on the link path).
+
+// src token-major [n][heads][width] -> dst [heads][lp][width], rows >= n zero.
+// width * esz is a multiple of 16, so every row is a whole number of uint4.
+__global__ void put_rows_kernel(const uint4 *__restrict__ src, uint4 *__restrict__ dst,
+                                int64_t n, int32_t lp, int32_t heads, int32_t vpr) {
+  const int64_t total = (int64_t)heads * lp * vpr;
+  for (int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; idx < total;
+       idx += (int64_t)gridDim.x * blockDim.x) {
+    const int64_t h = idx / ((int64_t)lp * vpr);
+    const int64_t rem = idx - h * lp * vpr;
+    const int64_t t = rem / vpr;
+    const int64_t c = rem - t * vpr;
+    uint4 v = make_uint4(0, 0, 0, 0);
+    if (t < n) v = src[(t * heads + h) * vpr + c];
+    dst[idx] = v;
+  }
+}
+
+// src token-major [n][heads][width] -> dst [heads][width][lp] (token axis
+// contiguous), columns >= n zero. 64x64 tiles through LDS so both the read
+// and the write are coalesced.
+template <typename E>
+__global__ void put_transposed_kernel(const E *__restrict__ src, E *__restrict__ dst, int64_t n,
+                                      int32_t lp, int32_t heads, int32_t width) {
+  __shared__ E tile[64][65];
+  const int64_t t0 = (int64_t)blockIdx.x * 64;
+  const int e0 = blockIdx.y * 64;
+  const int h = blockIdx.z;
+  for (int i = threadIdx.x; i < 64 * 64; i += blockDim.x) {
+    const int tl = i >> 6, el = i & 63;
+    const int64_t t = t0 + tl;
+    const int e = e0 + el;
+    E v = E(0);
+    if (t < n && e < width) v = src[(t * heads + h) * width + e];
+    tile[tl][el] = v;
+  }
+  __syncthreads();
+  for (int i = threadIdx.x; i < 64 * 64; i += blockDim.x) {
+    const int el = i >> 6, tl = i & 63;
+    const int64_t t = t0 + tl;
+    const int e = e0 + el;
+    if (e < width && t < lp) dst[((int64_t)h * width + e) * lp + t] = tile[tl][el];
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Address resolution shared by the gather hook and the attention kernels.
+
+// Link holding document token j of a request (links sorted by tok0).
+__device__ __forceinline__ int find_link(const LinkEntry *links, int n, int64_t j) {
+  int lo = 0, hi = n - 1;
+  while (lo < hi) {
+    const int mid = (lo + hi + 1) >> 1;
+    if (links[mid].tok0 <= j) lo = mid; else hi = mid - 1;
+  }
+  return lo;
+}
+
+// Element offset (from the pool base) of key row `row` of head `head` in a link.
+__device__ __forceinline__ int64_t key_row_off(const LinkEntry &e, int head, int row, int d_k) {
+  return e.k_off + ((int64_t)head * e.lp + row) * d_k;
+}
+// Element offset of value dim `dim` of token `row` (GQA, transposed V block).
+__device__ __forceinline__ int64_t value_off(const LinkEntry &e, int head, int dim, int row,
+                                             int d_v) {
+  return e.v_off + ((int64_t)head * d_v + dim) * e.lp + row;
+}
+
+template <typename E>
+__global__ void gather_kernel(const E *__restrict__ pool, const LinkEntry *__restrict__ links,
+                              int32_t n_links, int64_t total, int32_t heads, int32_t d_k,
+                              int32_t d_v, int32_t mla, E *__restrict__ k_out,
+                              E *__restrict__ v_out) {
+  const int64_t nk = total * heads * d_k;
+  const int64_t nv = mla ? 0 : total * heads * d_v;
+  for (int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; idx < nk + nv;
+       idx += (int64_t)gridDim.x * blockDim.x) {
+    if (idx < nk) {
+      const int64_t j = idx / ((int64_t)heads * d_k);
+      const int h = (int)((idx / d_k) % heads);
+      const int c = (int)(idx % d_k);
+      const LinkEntry e = links[find_link(links, n_links, j)];
+      k_out[idx] = pool[key_row_off(e, mla ? 0 : h, (int)(j - e.tok0), d_k) + c];
+    } else {
+      const int64_t x = idx - nk;
+      const int64_t j = x / ((int64_t)heads * d_v);
+      const int h = (int)((x / d_v) % heads);
+      const int c = (int)(x % d_v);
+      const LinkEntry e = links[find_link(links, n_links, j)];
+      v_out[x] = pool[value_off(e, h, c, (int)(j - e.tok0), d_v)];
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Generic link attention on the vector ALU.
+//
+// One workgroup = 4 waves = 16 rows of one (request, kv head); a row is a
+// (query token, query head of the group) pair. Keys are walked tile by tile:
+// the request's linked chunks in link order (no mask), then its own KV
+// (bottom-right causal). Per tile the K rows (and the value tile, transposed
+// so lanes index the value dim) are staged in LDS; lane = key for the scores,
+// lane = value dim for the P.V update. Online softmax in the log2 domain
+// (scale folded with log2 e into the staged queries).
+
+constexpr int kValuRows = 16;
+
+template <typename T, bool MLA>
+__global__ __launch_bounds__(256) void link_valu_kernel(LinkParams p) {
+  extern __shared__ float smem[];
+  const int d_k = p.d_k, d_v = p.d_v, group = p.group;
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+
+  const int g = blockIdx.x / p.nrb, rb = blockIdx.x % p.nrb;
+  const int split = blockIdx.y;
+  const int req_i = p.order[g / p.n_kv_heads];
+  const int kvh = g % p.n_kv_heads;
+  const ReqEntry R = p.reqs[req_i];
+  const int nrows = R.lq * group;
+  const int row0 = rb * kValuRows;
+  if (row0 >= nrows) return;
+  const int t_begin = (int)((int64_t)R.tiles * split / p.num_splits);
+  const int t_end = (int)((int64_t)R.tiles * (split + 1) / p.num_splits);
+
+  const T *__restrict__ pool = (const T *)p.pool;
+  const T *__restrict__ q = (const T *)p.q;
+  const T *__restrict__ k_self = (const T *)p.k_self;
+  const T *__restrict__ v_self = (const T *)p.v_self;
+
+  constexpr int EPW = 4 / sizeof(T);          // elements per 32-bit word
+  const int kwords = d_k / EPW;                // words per K row
+  const int kstride = kwords + 1;              // odd stride: conflict-free lane = key reads
+  const int vwords = kTile / EPW;              // words per value row (64 keys)
+  const int vstride = vwords + 1;
+  float *qs = smem;                                          // [16][d_k]
+  uint32_t *ks = (uint32_t *)(qs + kValuRows * d_k);         // [64][kstride]
+  uint32_t *vts = ks + kTile * kstride;                      // [d_v][vstride] (GQA)
+  float4 *pb = (float4 *)(vts + (MLA ? 0 : d_v * vstride));  // [4][64]
+  const T *ks_e = (const T *)ks;
+  T *vts_e = (T *)vts;
+
+  for (int x = threadIdx.x; x < kValuRows * d_k; x += blockDim.x) {
+    const int rl = x / d_k, c = x - rl * d_k;
+    const int row = row0 + rl;
+    float v = 0.f;
+    if (row < nrows) {
+      const int i = row / group, h = kvh * group + row % group;
+      v = to_f32(q[((int64_t)(R.q0 + i) * p.n_q_heads + h) * d_k + c]) * p.scale_log2;
+    }
+    qs[x] = v;
+  }
+
+  int lim[4];          // last visible own key per row (-1: none)
+  bool rvalid[4];
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+    const int row = row0 + wave * 4 + r;
+    rvalid[r] = row < nrows;
+    lim[r] = rvalid[r] ? row / group + R.ls - R.lq : -1;
+  }
+  float m[4], l[4], acc[4][8];
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+    m[r] = -INFINITY;
+    l[r] = 0.f;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) acc[r][j] = 0.f;
+  }
+  const int nvj = (d_v + 63) / 64;
+
+  int li = 0;
+  for (int t = t_begin; t < t_end; ++t) {
+    const bool own = t >= R.doc_tiles;
+    int nvalid, j0 = 0;
+    __syncthreads();
+    if (!own) {
+      while (p.links[R.link0 + li].tile0 + p.links[R.link0 + li].lp / kTile <= t) ++li;
+      const LinkEntry E = p.links[R.link0 + li];
+      const int tt = t - E.tile0;
+      nvalid = min(kTile, E.len - tt * kTile);
+      // 64 consecutive key rows (padding rows of the slot are zeros)
+      const uint32_t *src = (const uint32_t *)(pool + E.k_off +
+                                               ((int64_t)(MLA ? 0 : kvh) * E.lp + tt * kTile) * d_k);
+      for (int w = threadIdx.x; w < kTile * kwords; w += blockDim.x) {
+        const int r = w / kwords, c = w - r * kwords;
+        ks[r * kstride + c] = src[w];
+      }
+      if (!MLA) {
+        const T *vsrc = pool + E.v_off + (int64_t)kvh * d_v * E.lp + tt * kTile;
+        for (int w = threadIdx.x; w < d_v * vwords; w += blockDim.x) {
+          const int e = w / vwords, c = w - e * vwords;
+          vts[e * vstride + c] = ((const uint32_t *)(vsrc + (int64_t)e * E.lp))[c];
+        }
+      }
+    } else {
+      j0 = (t - R.doc_tiles) * kTile;
+      nvalid = min(kTile, R.ls - j0);
+      for (int w = threadIdx.x; w < kTile * kwords; w += blockDim.x) {
+        const int r = w / kwords, c = w - r * kwords;
+        uint32_t v = 0;
+        if (r < nvalid)
+          v = ((const uint32_t *)(k_self + ((int64_t)(R.s0 + j0 + r) * p.n_kv_heads + kvh) * d_k))[c];
+        ks[r * kstride + c] = v;
+      }
+      if (!MLA) {
+        const int vrow = vstride * EPW;
+        for (int x = threadIdx.x; x < kTile * d_v; x += blockDim.x) {
+          const int r = x / d_v, e = x - r * d_v;
+          T v = T(0);
+          if (r < nvalid) v = v_self[((int64_t)(R.s0 + j0 + r) * p.n_kv_heads + kvh) * d_v + e];
+          vts_e[e * vrow + r] = v;
+        }
+      }
+    }
+    __syncthreads();
+
+    // scores: lane = key
+    float s[4] = {0.f, 0.f, 0.f, 0.f};
+    const uint32_t *krow = ks + lane * kstride;
+    const float *qw = qs + (wave * 4) * d_k;
+    for (int w = 0; w < kwords; ++w) {
+      const uint32_t kw = krow[w];
+      if (EPW == 2) {
+        const float k0 = __uint_as_float(kw << 16), k1 = __uint_as_float(kw & 0xffff0000u);
+#pragma unroll
+        for (int r = 0; r < 4; ++r) s[r] += qw[r * d_k + 2 * w] * k0 + qw[r * d_k + 2 * w + 1] * k1;
+      } else {
+        const float k0 = __uint_as_float(kw);
+#pragma unroll
+        for (int r = 0; r < 4; ++r) s[r] += qw[r * d_k + w] * k0;
+      }
+    }
+    float pr[4], alpha[4];
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      bool vis = rvalid[r] && lane < nvalid && (!own || j0 + lane <= lim[r]);
+      float sv = vis ? s[r] : -INFINITY;
+      float mx = sv;
+#pragma unroll
+      for (int o = 32; o > 0; o >>= 1) mx = fmaxf(mx, __shfl_xor(mx, o));
+      const float mnew = fmaxf(m[r], mx);
+      float pv = 0.f;
+      alpha[r] = 1.f;
+      if (mnew != -INFINITY) {
+        pv = vis ? exp2f(sv - mnew) : 0.f;
+        alpha[r] = exp2f(m[r] - mnew);
+      }
+      float sum = pv;
+#pragma unroll
+      for (int o = 32; o > 0; o >>= 1) sum += __shfl_xor(sum, o);
+      l[r] = l[r] * alpha[r] + sum;
+      m[r] = mnew;
+      pr[r] = pv;
+    }
+    pb[wave * 64 + lane] = make_float4(pr[0], pr[1], pr[2], pr[3]);
+    __syncthreads();
+
+#pragma unroll
+    for (int r = 0; r < 4; ++r)
+#pragma unroll
+      for (int j = 0; j < 8; ++j) acc[r][j] *= alpha[r];
+    const int kmax = nvalid;
+    for (int k = 0; k < kmax; ++k) {
+      const float4 p4 = pb[wave * 64 + k];
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        if (j < nvj) {
+          const int e = lane + 64 * j;
+          if (e < d_v) {
+            float v;
+            if (MLA) v = to_f32(ks_e[k * kstride * EPW + e]);
+            else v = to_f32(vts_e[e * vstride * EPW + k]);
+            acc[0][j] += p4.x * v;
+            acc[1][j] += p4.y * v;
+            acc[2][j] += p4.z * v;
+            acc[3][j] += p4.w * v;
+          }
+        }
+      }
+    }
+  }
+
+  const int total_rows = p.total_q * p.n_q_heads;
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+    if (!rvalid[r]) continue;
+    const int row = row0 + wave * 4 + r;
+    const int i = row / group, h = kvh * group + row % group;
+    const int64_t orow = (int64_t)(R.q0 + i) * p.n_q_heads + h;
+    if (p.num_splits == 1) {
+      const float inv = l[r] > 0.f ? 1.f / l[r] : 0.f;
+      T *out = (T *)p.out + orow * d_v;
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        const int e = lane + 64 * j;
+        if (j < nvj && e < d_v) out[e] = from_f32<T>(acc[r][j] * inv);
+      }
+      if (p.lse && lane == 0)
+        p.lse[orow] = l[r] > 0.f ? (m[r] + log2f(l[r])) * 0.69314718055994531f : -INFINITY;
+    } else {
+      const int64_t prow = (int64_t)split * total_rows + orow;
+      float *po = p.part_o + prow * d_v;
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        const int e = lane + 64 * j;
+        if (j < nvj && e < d_v) po[e] = acc[r][j];
+      }
+      if (lane == 0) {
+        p.part_m[prow] = m[r];
+        p.part_l[prow] = l[r];
+      }
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Split-K combine: one wave per output row.
+//   M = max_s m_s,  w_s = 2^(m_s - M),  L = sum_s w_s l_s,
+//   out = sum_s w_s o_s / L,  lse = (M + log2 L) ln 2.
+template <typename T>
+__global__ __launch_bounds__(256) void combine_kernel(LinkParams p) {
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int64_t total_rows = (int64_t)p.total_q * p.n_q_heads;
+  const int64_t orow = (int64_t)blockIdx.x * 4 + wave;
+  if (orow >= total_rows) return;
+  const int S = p.num_splits;
+  float M = -INFINITY;
+  for (int s = lane; s < S; s += 64) M = fmaxf(M, p.part_m[s * total_rows + orow]);
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) M = fmaxf(M, __shfl_xor(M, o));
+  T *out = (T *)p.out + orow * p.d_v;
+  if (M == -INFINITY) {
+    for (int e = lane; e < p.d_v; e += 64) out[e] = from_f32<T>(0.f);
+    if (p.lse && lane == 0) p.lse[orow] = -INFINITY;
+    return;
+  }
+  float L = 0.f;
+  for (int s = lane; s < S; s += 64) {
+    const float ms = p.part_m[s * total_rows + orow];
+    if (ms != -INFINITY) L += exp2f(ms - M) * p.part_l[s * total_rows + orow];
+  }
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) L += __shfl_xor(L, o);
+  const float inv = 1.f / L;
+  for (int e = lane; e < p.d_v; e += 64) {
+    float a = 0.f;
+    for (int s = 0; s < S; ++s) {
+      const float ms = p.part_m[s * total_rows + orow];
+      if (ms != -INFINITY) a += exp2f(ms - M) * p.part_o[(s * total_rows + orow) * p.d_v + e];
+    }
+    out[e] = from_f32<T>(a * inv);
+  }
+  if (p.lse && lane == 0) p.lse[orow] = (M + log2f(L)) * 0.69314718055994531f;
+}
+
+size_t valu_lds_bytes(int esz, int mla, int d_k, int d_v) {
+  const int epw = 4 / esz;
+  const size_t kstride = d_k / epw + 1, vstride = kTile / epw + 1;
+  return sizeof(float) * kValuRows * d_k + 4 * kTile * kstride +
+         (mla ? 0 : 4 * d_v * vstride) + sizeof(float4) * 4 * 64;
+}
+
+template <typename T, bool MLA>
+hipError_t launch_valu_t(const LinkParams &p, hipStream_t st) {
+  const size_t lds = valu_lds_bytes(sizeof(T), MLA, p.d_k, p.d_v);
+  hipError_t e = hipFuncSetAttribute((const void *)link_valu_kernel<T, MLA>,
+                                     hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+  if (e != hipSuccess) return e;
+  dim3 grid(p.n_groups * p.nrb, p.num_splits);
+  hipLaunchKernelGGL((link_valu_kernel<T, MLA>), grid, dim3(256), lds, st, p);
+  return hipGetLastError();
+}
+
+}  // namespace
+
+int valu_rows_per_block() { return kValuRows; }
+
+size_t valu_lds_bytes_for(int esz, int mla, int d_k, int d_v) {
+  return valu_lds_bytes(esz, mla, d_k, d_v);
+}
+
+hipError_t launch_link_valu(const LinkParams &p, int dtype, int mla, hipStream_t st,
+                            const char **name) {
+  if (dtype == 0) {
+    *name = mla ? "link_valu_kernel<float,MLA>" : "link_valu_kernel<float,GQA>";
+    return mla ? launch_valu_t<float, true>(p, st) : launch_valu_t<float, false>(p, st);
+  }
+  *name = mla ? "link_valu_kernel<bf16,MLA>" : "link_valu_kernel<bf16,GQA>";
+  return mla ? launch_valu_t<uint16_t, true>(p, st) : launch_valu_t<uint16_t, false>(p, st);
+}
+
+hipError_t launch_combine(const LinkParams &p, int dtype, hipStream_t st) {
+  const int64_t rows = (int64_t)p.total_q * p.n_q_heads;
+  if (rows == 0) return hipSuccess;
+  dim3 grid((unsigned)((rows + 3) / 4));
+  if (dtype == 0)
+    hipLaunchKernelGGL(combine_kernel<float>, grid, dim3(256), 0, st, p);
+  else
+    hipLaunchKernelGGL(combine_kernel<uint16_t>, grid, dim3(256), 0, st, p);
+  return hipGetLastError();
+}
+
+hipError_t launch_put_rows(const void *src, void *dst, int64_t n_tokens, int32_t lp,
+                           int32_t heads, int32_t width, int32_t esz, hipStream_t st) {
+  const int32_t vpr = width * esz / 16;
+  const int64_t total = (int64_t)heads * lp * vpr;
+  const unsigned blocks = (unsigned)std::min<int64_t>((total + 255) / 256, 65536);
+  hipLaunchKernelGGL(put_rows_kernel, dim3(blocks), dim3(256), 0, st, (const uint4 *)src,
+                     (uint4 *)dst, n_tokens, lp, heads, vpr);
+  return hipGetLastError();
+}
+
+hipError_t launch_put_transposed(const void *src, void *dst, int64_t n_tokens, int32_t lp,
+                                 int32_t heads, int32_t width, int32_t esz, hipStream_t st) {
+  dim3 grid(lp / 64, (width + 63) / 64, heads);
+  if (esz == 2)
+    hipLaunchKernelGGL(put_transposed_kernel<uint16_t>, grid, dim3(256), 0, st,
+                       (const uint16_t *)src, (uint16_t *)dst, n_tokens, lp, heads, width);
+  else
+    hipLaunchKernelGGL(put_transposed_kernel<uint32_t>, grid, dim3(256), 0, st,
+                       (const uint32_t *)src, (uint32_t *)dst, n_tokens, lp, heads, width);
+  return hipGetLastError();
+}
+
+hipError_t launch_gather(const void *pool, const LinkEntry *links, int32_t n_links,
+                         int64_t total_tokens, int32_t heads, int32_t d_k, int32_t d_v,
+                         int32_t mla, int32_t esz, void *k_out, void *v_out, hipStream_t st) {
+  const int64_t n = total_tokens * heads * (d_k + (mla ? 0 : d_v));
+  if (n == 0) return hipSuccess;
+  const unsigned blocks = (unsigned)std::min<int64_t>((n + 255) / 256, 65536);
+  if (esz == 2)
+    hipLaunchKernelGGL(gather_kernel<uint16_t>, dim3(blocks), dim3(256), 0, st,
+                       (const uint16_t *)pool, links, n_links, total_tokens, heads, d_k, d_v, mla,
+                       (uint16_t *)k_out, (uint16_t *)v_out);
+  else
+    hipLaunchKernelGGL(gather_kernel<uint32_t>, dim3(blocks), dim3(256), 0, st,
+                       (const uint32_t *)pool, links, n_links, total_tokens, heads, d_k, d_v, mla,
+                       (uint32_t *)k_out, (uint32_t *)v_out);
+  return hipGetLastError();
+}
+
+}  // namespace pic

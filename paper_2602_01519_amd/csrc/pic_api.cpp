@@ -1,0 +1,597 @@
+// C ABI of the link-stage attention library: the chunk store (pool +
+// hash table + bump allocator), the per-call link planner and its staging of
+// the chunk table, kernel selection, and kernel timing.
+#include "../../include/pic.h"
+
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <mutex>
+#include <string>
+#include <unordered_map>
+#include <vector>
+
+#include "pic_internal.hpp"
+
+namespace pic {
+size_t valu_lds_bytes_for(int esz, int mla, int d_k, int d_v);
+}
+
+using namespace pic;
+
+namespace {
+
+thread_local std::string g_err;
+
+pic_status fail(pic_status st, const char *fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return st;
+}
+
+pic_status hip_fail(hipError_t e, const char *what) {
+  return fail(PIC_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+#define HIP_TRY(expr, what)                 \
+  do {                                      \
+    hipError_t e_ = (expr);                 \
+    if (e_ != hipSuccess) return hip_fail(e_, what); \
+  } while (0)
+
+// Restores the caller's current device on scope exit.
+struct DeviceGuard {
+  int prev = -1;
+  bool ok = true;
+  explicit DeviceGuard(int dev) {
+    if (hipGetDevice(&prev) != hipSuccess) { ok = false; return; }
+    if (prev != dev && hipSetDevice(dev) != hipSuccess) ok = false;
+  }
+  ~DeviceGuard() {
+    int cur;
+    if (prev >= 0 && hipGetDevice(&cur) == hipSuccess && cur != prev) (void)hipSetDevice(prev);
+  }
+};
+
+struct Slot {
+  int64_t off_tokens;   // first padded token of the slot in the pool
+  int64_t len;
+  int32_t lp;
+};
+
+// Pinned host table + device copy + completion event. The planner writes a
+// call's chunk/request tables into one slot, copies them to the device on
+// the call's stream, and records the event after the call's last kernel; a
+// slot is reused only after its event has completed.
+struct Stage {
+  void *host = nullptr;
+  void *dev = nullptr;
+  size_t cap = 0;
+  hipEvent_t done = nullptr;
+  bool pending = false;
+};
+
+constexpr int kRing = 8;
+
+struct ProfState {
+  std::mutex mu;
+  bool on = false;
+  std::vector<std::pair<hipEvent_t, hipEvent_t>> events;
+  std::vector<std::pair<hipEvent_t, hipEvent_t>> spare;
+  std::string name;
+};
+ProfState g_prof;
+
+inline int64_t round_up(int64_t x, int64_t m) { return (x + m - 1) / m * m; }
+
+}  // namespace
+
+struct pic_store {
+  pic_store_desc desc{};
+  int device = 0;
+  int esz = 2;
+  char *pool = nullptr;
+  int64_t capacity = 0;          // padded tokens
+  int64_t used = 0;
+  int64_t k_tok_elems = 0;       // K elements per padded token (all heads)
+  int64_t v_tok_elems = 0;       // V elements per padded token (GQA)
+  std::unordered_map<uint64_t, Slot> map;
+  Stage ring[kRing];
+  int next = 0;
+  void *work = nullptr;          // split partials
+  size_t work_cap = 0;
+};
+
+namespace {
+
+pic_status stage_acquire(pic_store *s, size_t bytes, Stage **out) {
+  Stage &st = s->ring[s->next];
+  s->next = (s->next + 1) % kRing;
+  if (st.pending) {
+    HIP_TRY(hipEventSynchronize(st.done), "hipEventSynchronize(stage)");
+    st.pending = false;
+  }
+  if (!st.done) HIP_TRY(hipEventCreateWithFlags(&st.done, hipEventDisableTiming), "hipEventCreate");
+  if (st.cap < bytes) {
+    if (st.host) (void)hipHostFree(st.host);
+    if (st.dev) (void)hipFree(st.dev);
+    st.host = st.dev = nullptr;
+    st.cap = 0;
+    size_t cap = std::max<size_t>(round_up((int64_t)bytes, 4096), 64 * 1024);
+    HIP_TRY(hipHostMalloc(&st.host, cap, hipHostMallocDefault), "hipHostMalloc(stage)");
+    HIP_TRY(hipMalloc(&st.dev, cap), "hipMalloc(stage)");
+    st.cap = cap;
+  }
+  *out = &st;
+  return PIC_OK;
+}
+
+pic_status ensure_work(pic_store *s, size_t bytes) {
+  if (s->work_cap >= bytes) return PIC_OK;
+  if (s->work) {
+    HIP_TRY(hipDeviceSynchronize(), "hipDeviceSynchronize(workspace)");
+    (void)hipFree(s->work);
+    s->work = nullptr;
+    s->work_cap = 0;
+  }
+  size_t cap = round_up((int64_t)bytes, 1 << 20);
+  HIP_TRY(hipMalloc(&s->work, cap), "hipMalloc(workspace)");
+  s->work_cap = cap;
+  return PIC_OK;
+}
+
+bool check_offsets(const int32_t *a, int32_t n) {
+  if (!a || a[0] != 0) return false;
+  for (int32_t i = 0; i < n; ++i)
+    if (a[i + 1] < a[i]) return false;
+  return true;
+}
+
+// Validated, resolved form of one link call.
+struct Plan {
+  std::vector<LinkEntry> links;
+  std::vector<ReqEntry> reqs;
+  std::vector<int32_t> order;
+  int32_t total_q = 0;
+  int32_t max_rows = 0;          // max over requests of lq * group
+  int32_t max_tiles = 0;
+  int64_t work_pairs = 0;
+};
+
+pic_status plan_call(pic_store *s, const pic_link_req *req, int32_t n_q_heads, const void *q,
+                     const void *k_self, const void *v_self, float scale, void *out,
+                     int32_t max_q_per_req, Plan &P) {
+  if (!s) return fail(PIC_ERR_INVALID, "store is NULL");
+  if (!req) return fail(PIC_ERR_INVALID, "req is NULL");
+  if (req->reserved != 0) return fail(PIC_ERR_INVALID, "req->reserved must be 0");
+  const pic_store_desc &d = s->desc;
+  const int32_t B = req->batch;
+  if (B < 0) return fail(PIC_ERR_INVALID, "batch < 0");
+  if (n_q_heads <= 0 || n_q_heads % d.n_kv_heads)
+    return fail(PIC_ERR_INVALID, "n_q_heads (%d) must be a positive multiple of n_kv_heads (%d)",
+                n_q_heads, d.n_kv_heads);
+  if (!std::isfinite(scale) || !(scale > 0.f))
+    return fail(PIC_ERR_INVALID, "softmax_scale must be positive and finite");
+  if (B == 0) return PIC_OK;
+  if (!check_offsets(req->chunk_offsets, B)) return fail(PIC_ERR_INVALID, "bad chunk_offsets");
+  if (!check_offsets(req->q_offsets, B)) return fail(PIC_ERR_INVALID, "bad q_offsets");
+  const bool self = req->self_offsets != nullptr;
+  if (self && !check_offsets(req->self_offsets, B)) return fail(PIC_ERR_INVALID, "bad self_offsets");
+  const int64_t n_links = req->chunk_offsets[B];
+  const int64_t tq = req->q_offsets[B];
+  const int64_t ts = self ? req->self_offsets[B] : 0;
+  if (n_links > 0 && !req->chunk_ids) return fail(PIC_ERR_INVALID, "chunk_ids is NULL");
+  if (tq > 0 && (!q || !out)) return fail(PIC_ERR_INVALID, "q/out is NULL");
+  if (tq * n_q_heads > INT32_MAX / 2) return fail(PIC_ERR_INVALID, "too many query rows");
+  if (self) {
+    if (ts > 0 && !k_self) return fail(PIC_ERR_INVALID, "k_self is NULL");
+    if (d.kind == PIC_GQA && ts > 0 && !v_self) return fail(PIC_ERR_INVALID, "v_self is NULL");
+    if (d.kind == PIC_MLA && v_self) return fail(PIC_ERR_INVALID, "v_self must be NULL for MLA");
+  } else if (k_self || v_self) {
+    return fail(PIC_ERR_INVALID, "k_self/v_self given without self_offsets");
+  }
+  const int group = n_q_heads / d.n_kv_heads;
+  P.links.resize(n_links);
+  P.reqs.resize(B);
+  std::vector<int64_t> weight(B);
+  for (int32_t r = 0; r < B; ++r) {
+    ReqEntry &R = P.reqs[r];
+    R.link0 = req->chunk_offsets[r];
+    R.nlinks = req->chunk_offsets[r + 1] - R.link0;
+    R.q0 = req->q_offsets[r];
+    R.lq = req->q_offsets[r + 1] - R.q0;
+    R.s0 = self ? req->self_offsets[r] : 0;
+    R.ls = self ? req->self_offsets[r + 1] - R.s0 : 0;
+    if (self && R.ls < R.lq)
+      return fail(PIC_ERR_INVALID, "request %d: %d query tokens but only %d own tokens", r, R.lq,
+                  R.ls);
+    if (R.lq > max_q_per_req)
+      return fail(PIC_ERR_INVALID, "request %d: %d query tokens exceeds %d", r, R.lq,
+                  max_q_per_req);
+    int64_t tiles = 0, toks = 0;
+    for (int32_t c = 0; c < R.nlinks; ++c) {
+      const uint64_t id = req->chunk_ids[R.link0 + c];
+      auto it = s->map.find(id);
+      if (it == s->map.end())
+        return fail(PIC_ERR_NOT_FOUND, "request %d link %d: chunk id 0x%llx not in the store", r,
+                    c, (unsigned long long)id);
+      const Slot &sl = it->second;
+      LinkEntry &E = P.links[R.link0 + c];
+      E.k_off = sl.off_tokens * (s->k_tok_elems + s->v_tok_elems);
+      E.v_off = d.kind == PIC_GQA ? E.k_off + (int64_t)sl.lp * s->k_tok_elems : E.k_off;
+      E.len = (int32_t)sl.len;
+      E.lp = sl.lp;
+      E.tile0 = (int32_t)tiles;
+      E.tok0 = (int32_t)toks;
+      tiles += sl.lp / kTile;
+      toks += sl.len;
+    }
+    if (toks + R.ls > INT32_MAX / 2) return fail(PIC_ERR_INVALID, "request %d too long", r);
+    R.doc_tiles = (int32_t)tiles;
+    R.tiles = (int32_t)(tiles + (R.ls + kTile - 1) / kTile);
+    P.max_rows = std::max(P.max_rows, R.lq * group);
+    P.max_tiles = std::max(P.max_tiles, R.tiles);
+    weight[r] = (int64_t)R.tiles * R.lq;
+    P.work_pairs += (int64_t)R.lq * (toks + R.ls);
+  }
+  P.order.resize(B);
+  for (int32_t r = 0; r < B; ++r) P.order[r] = r;
+  std::stable_sort(P.order.begin(), P.order.end(),
+                   [&](int32_t a, int32_t b) { return weight[a] > weight[b]; });
+  P.total_q = (int32_t)tq;
+  return PIC_OK;
+}
+
+// Copies the plan's tables into a staging slot and to the device.
+pic_status upload(pic_store *s, const Plan &P, hipStream_t st, Stage **stage, LinkParams &lp) {
+  const size_t nl = P.links.size(), nr = P.reqs.size();
+  const size_t off_r = round_up(sizeof(LinkEntry) * nl, 256);
+  const size_t off_o = off_r + round_up(sizeof(ReqEntry) * nr, 256);
+  const size_t bytes = off_o + round_up(sizeof(int32_t) * nr, 256);
+  pic_status rc = stage_acquire(s, bytes, stage);
+  if (rc != PIC_OK) return rc;
+  char *h = (char *)(*stage)->host;
+  if (nl) memcpy(h, P.links.data(), sizeof(LinkEntry) * nl);
+  memcpy(h + off_r, P.reqs.data(), sizeof(ReqEntry) * nr);
+  memcpy(h + off_o, P.order.data(), sizeof(int32_t) * nr);
+  HIP_TRY(hipMemcpyAsync((*stage)->dev, h, bytes, hipMemcpyHostToDevice, st), "hipMemcpyAsync(table)");
+  char *dv = (char *)(*stage)->dev;
+  lp.links = (const LinkEntry *)dv;
+  lp.reqs = (const ReqEntry *)(dv + off_r);
+  lp.order = (const int32_t *)(dv + off_o);
+  return PIC_OK;
+}
+
+void prof_start(hipStream_t st, std::pair<hipEvent_t, hipEvent_t> *ev) {
+  ev->first = ev->second = nullptr;
+  std::lock_guard<std::mutex> g(g_prof.mu);
+  if (!g_prof.on) return;
+  if (!g_prof.spare.empty()) {
+    *ev = g_prof.spare.back();
+    g_prof.spare.pop_back();
+  } else if (hipEventCreate(&ev->first) != hipSuccess || hipEventCreate(&ev->second) != hipSuccess) {
+    ev->first = ev->second = nullptr;
+    return;
+  }
+  (void)hipEventRecord(ev->first, st);
+}
+
+void prof_stop(hipStream_t st, std::pair<hipEvent_t, hipEvent_t> *ev, const char *name) {
+  if (!ev->first) return;
+  (void)hipEventRecord(ev->second, st);
+  std::lock_guard<std::mutex> g(g_prof.mu);
+  g_prof.events.push_back(*ev);
+  g_prof.name = name;
+}
+
+enum class Mode { Prefill, Decode };
+
+pic_status link_call(pic_store *s, const pic_link_req *req, int32_t n_q_heads, const void *q,
+                     const void *k_self, const void *v_self, float scale, int32_t num_splits,
+                     void *out, float *lse, void *stream, Mode mode) {
+  if (mode == Mode::Decode && (num_splits < 0 || num_splits > 256))
+    return fail(PIC_ERR_INVALID, "num_splits must be 0..256");
+  Plan P;
+  pic_status rc = plan_call(s, req, n_q_heads, q, k_self, v_self, scale, out,
+                            mode == Mode::Decode ? 16 : INT32_MAX, P);
+  if (rc != PIC_OK) return rc;
+  if (req->batch == 0 || P.total_q == 0) return PIC_OK;
+  const pic_store_desc &d = s->desc;
+  const bool mla = d.kind == PIC_MLA;
+  const hipStream_t st = (hipStream_t)stream;
+
+  LinkParams lp{};
+  lp.pool = s->pool;
+  lp.q = q;
+  lp.k_self = k_self;
+  lp.v_self = v_self;
+  lp.out = out;
+  lp.lse = lse;
+  lp.batch = req->batch;
+  lp.n_q_heads = n_q_heads;
+  lp.n_kv_heads = d.n_kv_heads;
+  lp.group = n_q_heads / d.n_kv_heads;
+  lp.d_k = d.d_k;
+  lp.d_v = d.d_v;
+  lp.total_q = P.total_q;
+  lp.scale_log2 = scale * 1.4426950408889634f;
+
+  // Kernel choice.
+  const bool mfma128 = d.dtype == PIC_BF16 && !mla && d.d_k == 128 && d.d_v == 128 &&
+                       mode == Mode::Prefill;
+  int rows_per_block = mfma128 ? mfma_d128_rows_per_block() : valu_rows_per_block();
+  if (!mfma128 && valu_lds_bytes_for(s->esz, mla, d.d_k, d.d_v) > 160 * 1024)
+    return fail(PIC_ERR_UNSUPPORTED, "head widths d_k=%d d_v=%d exceed the generic kernel's LDS",
+                d.d_k, d.d_v);
+  lp.nrb = std::max(1, (P.max_rows + rows_per_block - 1) / rows_per_block);
+  lp.n_groups = req->batch * d.n_kv_heads;
+  if (mfma128) lp.n_groups = (int32_t)round_up(lp.n_groups, 8);
+
+  int32_t splits = 1;
+  if (mode == Mode::Decode) {
+    if (num_splits > 0) {
+      splits = num_splits;
+    } else {
+      const int64_t blocks = (int64_t)req->batch * d.n_kv_heads * lp.nrb;
+      splits = (int32_t)std::max<int64_t>(1, std::min<int64_t>((2048 + blocks - 1) / blocks, 256));
+      splits = std::min(splits, std::max(1, P.max_tiles));
+    }
+  }
+  lp.num_splits = splits;
+  if (splits > 1) {
+    const size_t rows = (size_t)P.total_q * n_q_heads;
+    const size_t bytes = rows * splits * (d.d_v + 2) * sizeof(float) + 1024;
+    rc = ensure_work(s, bytes);
+    if (rc != PIC_OK) return rc;
+    lp.part_o = (float *)s->work;
+    lp.part_m = lp.part_o + rows * splits * d.d_v;
+    lp.part_l = lp.part_m + rows * splits;
+  }
+
+  DeviceGuard dg(s->device);
+  if (!dg.ok) return fail(PIC_ERR_HIP, "cannot select the store's device");
+  Stage *stage = nullptr;
+  rc = upload(s, P, st, &stage, lp);
+  if (rc != PIC_OK) return rc;
+
+  std::pair<hipEvent_t, hipEvent_t> ev;
+  const char *name = "";
+  prof_start(st, &ev);
+  hipError_t e;
+  if (mfma128)
+    e = launch_link_mfma_d128(lp, st, &name);
+  else
+    e = launch_link_valu(lp, d.dtype, mla, st, &name);
+  prof_stop(st, &ev, name);
+  if (e != hipSuccess) return hip_fail(e, name);
+  if (splits > 1) {
+    e = launch_combine(lp, d.dtype, st);
+    if (e != hipSuccess) return hip_fail(e, "combine_kernel");
+  }
+  HIP_TRY(hipEventRecord(stage->done, st), "hipEventRecord(stage)");
+  stage->pending = true;
+  return PIC_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+pic_status pic_store_create(const pic_store_desc *desc, pic_store **out) {
+  if (!desc || !out) return fail(PIC_ERR_INVALID, "desc/out is NULL");
+  *out = nullptr;
+  const pic_store_desc &d = *desc;
+  if (d.kind != PIC_GQA && d.kind != PIC_MLA) return fail(PIC_ERR_INVALID, "unknown kind %d", d.kind);
+  if (d.dtype != PIC_F32 && d.dtype != PIC_BF16) return fail(PIC_ERR_INVALID, "unknown dtype %d", d.dtype);
+  if (d.reserved != 0) return fail(PIC_ERR_INVALID, "desc->reserved must be 0");
+  if (d.n_kv_heads <= 0 || d.d_k <= 0 || d.d_v <= 0 || d.capacity_tokens <= 0)
+    return fail(PIC_ERR_INVALID, "n_kv_heads, d_k, d_v and capacity_tokens must be positive");
+  if (d.kind == PIC_MLA && (d.n_kv_heads != 1 || d.d_v > d.d_k))
+    return fail(PIC_ERR_INVALID, "MLA needs n_kv_heads == 1 and d_v <= d_k");
+  if (d.d_k % 8 || d.d_v % 8) return fail(PIC_ERR_UNSUPPORTED, "d_k and d_v must be multiples of 8");
+  if (d.d_k > 1024 || d.d_v > 1024 || d.n_kv_heads > 256)
+    return fail(PIC_ERR_UNSUPPORTED, "head count or width too large");
+  pic_store *s = new (std::nothrow) pic_store();
+  if (!s) return fail(PIC_ERR_OOM, "host allocation failed");
+  s->desc = d;
+  s->esz = d.dtype == PIC_F32 ? 4 : 2;
+  s->capacity = round_up(d.capacity_tokens, kTile);
+  s->k_tok_elems = (int64_t)d.n_kv_heads * d.d_k;
+  s->v_tok_elems = d.kind == PIC_GQA ? (int64_t)d.n_kv_heads * d.d_v : 0;
+  hipError_t e = hipGetDevice(&s->device);
+  if (e == hipSuccess) {
+    const size_t bytes = (size_t)s->capacity * (s->k_tok_elems + s->v_tok_elems) * s->esz;
+    e = hipMalloc((void **)&s->pool, bytes);
+  }
+  if (e != hipSuccess) {
+    delete s;
+    return hip_fail(e, "hipMalloc(pool)");
+  }
+  *out = s;
+  return PIC_OK;
+}
+
+pic_status pic_store_destroy(pic_store *s) {
+  if (!s) return PIC_OK;
+  DeviceGuard dg(s->device);
+  (void)hipDeviceSynchronize();
+  for (Stage &st : s->ring) {
+    if (st.host) (void)hipHostFree(st.host);
+    if (st.dev) (void)hipFree(st.dev);
+    if (st.done) (void)hipEventDestroy(st.done);
+  }
+  if (s->work) (void)hipFree(s->work);
+  if (s->pool) (void)hipFree(s->pool);
+  delete s;
+  return PIC_OK;
+}
+
+pic_status pic_store_put(pic_store *s, uint64_t chunk_id, int64_t n_tokens, const void *k,
+                         const void *v, void *stream) {
+  if (!s) return fail(PIC_ERR_INVALID, "store is NULL");
+  if (n_tokens <= 0 || n_tokens > INT32_MAX / 4) return fail(PIC_ERR_INVALID, "n_tokens out of range");
+  if (!k) return fail(PIC_ERR_INVALID, "k is NULL");
+  const bool gqa = s->desc.kind == PIC_GQA;
+  if (gqa && !v) return fail(PIC_ERR_INVALID, "v is NULL");
+  if (!gqa && v) return fail(PIC_ERR_INVALID, "v must be NULL for MLA");
+  if (s->map.count(chunk_id)) return fail(PIC_ERR_EXISTS, "chunk id 0x%llx already stored",
+                                          (unsigned long long)chunk_id);
+  const int64_t lp = round_up(n_tokens, kTile);
+  if (s->used + lp > s->capacity)
+    return fail(PIC_ERR_OOM, "pool full: %lld of %lld tokens used, chunk needs %lld",
+                (long long)s->used, (long long)s->capacity, (long long)lp);
+  DeviceGuard dg(s->device);
+  if (!dg.ok) return fail(PIC_ERR_HIP, "cannot select the store's device");
+  for (const void *ptr : {k, v}) {
+    if (!ptr) continue;
+    hipPointerAttribute_t attr;
+    if (hipPointerGetAttributes(&attr, ptr) != hipSuccess ||
+        (attr.type != hipMemoryTypeDevice && attr.type != hipMemoryTypeManaged)) {
+      (void)hipGetLastError();
+      return fail(PIC_ERR_INVALID, "k and v must be device memory");
+    }
+  }
+  const hipStream_t st = (hipStream_t)stream;
+  const pic_store_desc &d = s->desc;
+  char *kdst = s->pool + (size_t)s->used * (s->k_tok_elems + s->v_tok_elems) * s->esz;
+  hipError_t e = launch_put_rows(k, kdst, n_tokens, (int32_t)lp, d.n_kv_heads, d.d_k, s->esz, st);
+  if (e != hipSuccess) return hip_fail(e, "put_rows_kernel");
+  if (gqa) {
+    char *vdst = kdst + (size_t)lp * s->k_tok_elems * s->esz;
+    e = launch_put_transposed(v, vdst, n_tokens, (int32_t)lp, d.n_kv_heads, d.d_v, s->esz, st);
+    if (e != hipSuccess) return hip_fail(e, "put_transposed_kernel");
+  }
+  // A slot is its K block followed by its V block; slot offsets count padded
+  // tokens of (K + V) elements.
+  Slot sl{s->used, n_tokens, (int32_t)lp};
+  s->used += lp;
+  s->map.emplace(chunk_id, sl);
+  return PIC_OK;
+}
+
+pic_status pic_store_lookup(const pic_store *s, uint64_t chunk_id, int64_t *n_tokens_out) {
+  if (!s || !n_tokens_out) return fail(PIC_ERR_INVALID, "store/n_tokens_out is NULL");
+  auto it = s->map.find(chunk_id);
+  if (it == s->map.end()) return fail(PIC_ERR_NOT_FOUND, "chunk id 0x%llx not in the store",
+                                      (unsigned long long)chunk_id);
+  *n_tokens_out = it->second.len;
+  return PIC_OK;
+}
+
+pic_status pic_store_usage(const pic_store *s, int64_t *used, int64_t *cap, int64_t *n) {
+  if (!s) return fail(PIC_ERR_INVALID, "store is NULL");
+  if (used) *used = s->used;
+  if (cap) *cap = s->capacity;
+  if (n) *n = (int64_t)s->map.size();
+  return PIC_OK;
+}
+
+pic_status pic_link_attn(pic_store *s, const pic_link_req *req, int32_t n_q_heads, const void *q,
+                         const void *k_self, const void *v_self, float softmax_scale, void *out,
+                         float *lse, void *stream) {
+  return link_call(s, req, n_q_heads, q, k_self, v_self, softmax_scale, 0, out, lse, stream,
+                   Mode::Prefill);
+}
+
+pic_status pic_link_decode(pic_store *s, const pic_link_req *req, int32_t n_q_heads,
+                           const void *q, const void *k_self, const void *v_self,
+                           float softmax_scale, int32_t num_splits, void *out, float *lse,
+                           void *stream) {
+  return link_call(s, req, n_q_heads, q, k_self, v_self, softmax_scale, num_splits, out, lse,
+                   stream, Mode::Decode);
+}
+
+pic_status pic_debug_gather(pic_store *s, const uint64_t *ids, int32_t n, void *k_out,
+                            void *v_out, void *stream) {
+  if (!s) return fail(PIC_ERR_INVALID, "store is NULL");
+  if (n < 0 || (n > 0 && !ids)) return fail(PIC_ERR_INVALID, "bad id list");
+  const bool gqa = s->desc.kind == PIC_GQA;
+  std::vector<LinkEntry> links(n);
+  int64_t toks = 0;
+  for (int32_t i = 0; i < n; ++i) {
+    auto it = s->map.find(ids[i]);
+    if (it == s->map.end()) return fail(PIC_ERR_NOT_FOUND, "chunk id 0x%llx not in the store",
+                                        (unsigned long long)ids[i]);
+    const Slot &sl = it->second;
+    LinkEntry &E = links[i];
+    E.k_off = sl.off_tokens * s->k_tok_elems + sl.off_tokens * s->v_tok_elems;
+    E.v_off = E.k_off + (int64_t)sl.lp * s->k_tok_elems;
+    E.len = (int32_t)sl.len;
+    E.lp = sl.lp;
+    E.tile0 = 0;
+    E.tok0 = (int32_t)toks;
+    toks += sl.len;
+  }
+  if (toks == 0) return PIC_OK;
+  if (!k_out || (gqa && !v_out)) return fail(PIC_ERR_INVALID, "k_out/v_out is NULL");
+  if (!gqa && v_out) return fail(PIC_ERR_INVALID, "v_out must be NULL for MLA");
+  DeviceGuard dg(s->device);
+  if (!dg.ok) return fail(PIC_ERR_HIP, "cannot select the store's device");
+  const hipStream_t st = (hipStream_t)stream;
+  Stage *stage = nullptr;
+  pic_status rc = stage_acquire(s, sizeof(LinkEntry) * n, &stage);
+  if (rc != PIC_OK) return rc;
+  memcpy(stage->host, links.data(), sizeof(LinkEntry) * n);
+  HIP_TRY(hipMemcpyAsync(stage->dev, stage->host, sizeof(LinkEntry) * n, hipMemcpyHostToDevice, st),
+          "hipMemcpyAsync(gather table)");
+  const pic_store_desc &d = s->desc;
+  hipError_t e = launch_gather(s->pool, (const LinkEntry *)stage->dev, n, toks, d.n_kv_heads,
+                               d.d_k, d.d_v, !gqa, s->esz, k_out, v_out, st);
+  if (e != hipSuccess) return hip_fail(e, "gather_kernel");
+  HIP_TRY(hipEventRecord(stage->done, st), "hipEventRecord(stage)");
+  stage->pending = true;
+  return PIC_OK;
+}
+
+pic_status pic_prof_begin(void) {
+  std::lock_guard<std::mutex> g(g_prof.mu);
+  for (auto &ev : g_prof.events) g_prof.spare.push_back(ev);
+  g_prof.events.clear();
+  g_prof.on = true;
+  return PIC_OK;
+}
+
+pic_status pic_prof_end(double *kernel_ms, int64_t *launches, char *name_buf, int32_t name_len) {
+  std::lock_guard<std::mutex> g(g_prof.mu);
+  g_prof.on = false;
+  double total = 0.0;
+  for (auto &ev : g_prof.events) {
+    HIP_TRY(hipEventSynchronize(ev.second), "hipEventSynchronize(prof)");
+    float ms = 0.f;
+    HIP_TRY(hipEventElapsedTime(&ms, ev.first, ev.second), "hipEventElapsedTime");
+    total += ms;
+  }
+  if (kernel_ms) *kernel_ms = total;
+  if (launches) *launches = (int64_t)g_prof.events.size();
+  if (name_buf && name_len > 0) {
+    snprintf(name_buf, (size_t)name_len, "%s", g_prof.name.c_str());
+  }
+  for (auto &ev : g_prof.events) g_prof.spare.push_back(ev);
+  g_prof.events.clear();
+  return PIC_OK;
+}
+
+const char *pic_status_str(pic_status st) {
+  switch (st) {
+    case PIC_OK: return "PIC_OK";
+    case PIC_ERR_INVALID: return "PIC_ERR_INVALID";
+    case PIC_ERR_NOT_FOUND: return "PIC_ERR_NOT_FOUND";
+    case PIC_ERR_EXISTS: return "PIC_ERR_EXISTS";
+    case PIC_ERR_OOM: return "PIC_ERR_OOM";
+    case PIC_ERR_HIP: return "PIC_ERR_HIP";
+    case PIC_ERR_UNSUPPORTED: return "PIC_ERR_UNSUPPORTED";
+  }
+  return "PIC_ERR_?";
+}
+
+const char *pic_last_error(void) { return g_err.c_str(); }
+
+}  // extern "C"

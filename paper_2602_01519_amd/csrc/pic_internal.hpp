@@ -1,0 +1,90 @@
+// Internal declarations shared by the host planner and the HIP kernels.
+// Not part of the C ABI (include/pic.h is).
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+
+namespace pic {
+
+// Keys per attention tile. Every chunk slot in the pool is padded to a
+// multiple of it (zero rows), so a tile never straddles two chunks and the
+// pool's rows stay 16-byte aligned.
+constexpr int kTile = 64;
+
+// Pool layout of one chunk slot with padded length lp (elements of the
+// store's dtype, offsets relative to the pool base):
+//   GQA  K block  [n_kv_heads][lp][d_k]    at k_off  (head-major, token rows)
+//        V block  [n_kv_heads][d_v][lp]    at v_off  (transposed: the value
+//                                          dim is the row, tokens contiguous)
+//   MLA  K block  [lp][d_k]                at k_off  (value = first d_v entries
+//        of each row; v_off == k_off)
+// The transposed V lets a matrix-core operand read 8 consecutive keys of one
+// value column with a single 16-byte load.
+
+struct LinkEntry {        // one link of one request, in link order
+  int64_t k_off;
+  int64_t v_off;
+  int32_t len;            // tokens
+  int32_t lp;             // padded tokens (multiple of kTile)
+  int32_t tile0;          // index of the link's first tile within the request
+  int32_t tok0;           // index of the link's first token within the request
+};
+
+struct ReqEntry {
+  int32_t link0, nlinks;  // links[link0 .. link0+nlinks)
+  int32_t q0, lq;         // query rows q0 .. q0+lq of q / out
+  int32_t s0, ls;         // own rows s0 .. s0+ls of k_self / v_self (ls = 0: none)
+  int32_t doc_tiles;      // tiles over the linked documents
+  int32_t tiles;          // doc_tiles + ceil(ls / kTile)
+};
+
+struct LinkParams {
+  const void *pool;
+  const LinkEntry *links;
+  const ReqEntry *reqs;
+  const int32_t *order;   // requests, heaviest first
+  const void *q;
+  const void *k_self;
+  const void *v_self;
+  void *out;
+  float *lse;
+  float *part_o;          // split partials: [split][Tq*H_q][d_v] unnormalised
+  float *part_m;          // [split][Tq*H_q] running max (log2 domain)
+  float *part_l;          // [split][Tq*H_q] running sum
+  int32_t batch;
+  int32_t n_q_heads;
+  int32_t n_kv_heads;
+  int32_t group;          // n_q_heads / n_kv_heads
+  int32_t d_k;
+  int32_t d_v;
+  int32_t total_q;        // Tq
+  int32_t num_splits;     // 1: write out/lse directly; >1: write partials
+  int32_t nrb;            // row blocks per (request, kv head)
+  int32_t n_groups;       // batch * n_kv_heads, padded as the kernel requires
+  float scale_log2;       // softmax_scale * log2(e)
+};
+
+// Launchers (each returns the launch status).
+hipError_t launch_put_rows(const void *src, void *dst, int64_t n_tokens, int32_t lp,
+                           int32_t heads, int32_t width, int32_t esz, hipStream_t st);
+hipError_t launch_put_transposed(const void *src, void *dst, int64_t n_tokens, int32_t lp,
+                                 int32_t heads, int32_t width, int32_t esz, hipStream_t st);
+hipError_t launch_gather(const void *pool, const LinkEntry *links, int32_t n_links,
+                         int64_t total_tokens, int32_t heads, int32_t d_k, int32_t d_v,
+                         int32_t mla, int32_t esz, void *k_out, void *v_out, hipStream_t st);
+
+// Generic vector-ALU link attention: any d_k <= 576, d_v <= 512, fp32 or bf16.
+hipError_t launch_link_valu(const LinkParams &p, int dtype, int mla, hipStream_t st,
+                            const char **name);
+int valu_rows_per_block();
+
+// bf16 GQA link attention on MFMA, d_k = d_v = 128 (prefill-shaped).
+hipError_t launch_link_mfma_d128(const LinkParams &p, hipStream_t st, const char **name);
+int mfma_d128_rows_per_block();
+
+// Log-sum-exp merge of split partials into out / lse.
+hipError_t launch_combine(const LinkParams &p, int dtype, hipStream_t st);
+
+}  // namespace pic

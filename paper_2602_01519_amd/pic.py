@@ -1,0 +1,208 @@
+"""Python binding of the link-attention C ABI (include/pic.h), by ctypes.
+
+Argument marshalling only: every step of the path runs in the HIP library.
+Tensors are passed as raw device pointers (torch tensors are accepted and
+their ``data_ptr()`` is taken); host arrays are numpy arrays. Streams are
+``hipStream_t`` handles as integers (``torch.cuda.current_stream().cuda_stream``)
+or None for the null stream. Every non-OK status raises PicError.
+
+The library must have been built (paper_2602_01519_amd/build.py); importing
+a function of this module without it raises PicError -- there is no fallback.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import re
+from typing import Optional
+
+import numpy as np
+
+_LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libpic.so")
+_HEADER = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "include", "pic.h")
+_lib = None
+
+OK, ERR_INVALID, ERR_NOT_FOUND, ERR_EXISTS, ERR_OOM, ERR_HIP, ERR_UNSUPPORTED = 0, -1, -2, -3, -4, -5, -6
+F32, BF16 = 0, 1
+GQA, MLA = 0, 1
+
+
+class PicError(RuntimeError):
+    def __init__(self, status: int, message: str):
+        super().__init__(f"{status_name(status)}: {message}")
+        self.status = status
+
+
+_NAMES = {0: "PIC_OK", -1: "PIC_ERR_INVALID", -2: "PIC_ERR_NOT_FOUND", -3: "PIC_ERR_EXISTS",
+          -4: "PIC_ERR_OOM", -5: "PIC_ERR_HIP", -6: "PIC_ERR_UNSUPPORTED"}
+
+
+def status_name(st: int) -> str:
+    return _NAMES.get(st, f"status {st}")
+
+
+class StoreDesc(ctypes.Structure):
+    _fields_ = [("kind", ctypes.c_int32), ("dtype", ctypes.c_int32), ("n_kv_heads", ctypes.c_int32),
+                ("d_k", ctypes.c_int32), ("d_v", ctypes.c_int32), ("reserved", ctypes.c_int32),
+                ("capacity_tokens", ctypes.c_int64)]
+
+
+class LinkReq(ctypes.Structure):
+    _fields_ = [("batch", ctypes.c_int32), ("reserved", ctypes.c_int32),
+                ("chunk_offsets", ctypes.c_void_p), ("chunk_ids", ctypes.c_void_p),
+                ("q_offsets", ctypes.c_void_p), ("self_offsets", ctypes.c_void_p)]
+
+
+def lib_path() -> str:
+    return _LIB_PATH
+
+
+def lib():
+    """The loaded libpic.so; raises PicError if it has not been built."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_LIB_PATH):
+            raise PicError(ERR_UNSUPPORTED, f"{_LIB_PATH} is not built; run paper_2602_01519_amd/build.py")
+        L = ctypes.CDLL(_LIB_PATH)
+        vp, i32, i64, u64, f32 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_uint64, ctypes.c_float
+        sig = {
+            "pic_store_create": [vp, vp],
+            "pic_store_destroy": [vp],
+            "pic_store_put": [vp, u64, i64, vp, vp, vp],
+            "pic_store_lookup": [vp, u64, vp],
+            "pic_store_usage": [vp, vp, vp, vp],
+            "pic_link_attn": [vp, vp, i32, vp, vp, vp, f32, vp, vp, vp],
+            "pic_link_decode": [vp, vp, i32, vp, vp, vp, f32, i32, vp, vp, vp],
+            "pic_debug_gather": [vp, vp, i32, vp, vp, vp],
+            "pic_prof_begin": [],
+            "pic_prof_end": [vp, vp, vp, i32],
+        }
+        for name, args in sig.items():
+            fn = getattr(L, name)
+            fn.argtypes = args
+            fn.restype = ctypes.c_int
+        L.pic_status_str.argtypes = [ctypes.c_int]
+        L.pic_status_str.restype = ctypes.c_char_p
+        L.pic_last_error.argtypes = []
+        L.pic_last_error.restype = ctypes.c_char_p
+        _lib = L
+    return _lib
+
+
+def header_functions() -> list:
+    """Names of the functions include/pic.h declares."""
+    text = open(_HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(pic_[a-z_]+)\s*\(", text)))
+
+
+def last_error() -> str:
+    return lib().pic_last_error().decode()
+
+
+def _check(st: int):
+    if st != OK:
+        raise PicError(st, last_error())
+
+
+def _ptr(x):
+    if x is None:
+        return None
+    if isinstance(x, int):
+        return x
+    if isinstance(x, np.ndarray):
+        return x.ctypes.data
+    return x.data_ptr()          # torch tensor
+
+
+def _host_i32(a):
+    return None if a is None else np.ascontiguousarray(a, dtype=np.int32)
+
+
+class Store:
+    """A chunk store (pool + hash table) on the current HIP device."""
+
+    def __init__(self, kind: int, dtype: int, n_kv_heads: int, d_k: int, d_v: int, capacity_tokens: int):
+        self.desc = StoreDesc(kind, dtype, n_kv_heads, d_k, d_v, 0, capacity_tokens)
+        h = ctypes.c_void_p()
+        _check(lib().pic_store_create(ctypes.byref(self.desc), ctypes.byref(h)))
+        self.handle = h
+
+    def close(self):
+        if self.handle:
+            _check(lib().pic_store_destroy(self.handle))
+            self.handle = None
+
+    def __enter__(self):
+        return self
+
+    def __exit__(self, *exc):
+        self.close()
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def put(self, chunk_id: int, n_tokens: int, k, v, stream: Optional[int] = None):
+        _check(lib().pic_store_put(self.handle, int(chunk_id), int(n_tokens), _ptr(k), _ptr(v), stream))
+
+    def lookup(self, chunk_id: int) -> int:
+        n = ctypes.c_int64()
+        _check(lib().pic_store_lookup(self.handle, int(chunk_id), ctypes.byref(n)))
+        return n.value
+
+    def usage(self):
+        u, c, n = ctypes.c_int64(), ctypes.c_int64(), ctypes.c_int64()
+        _check(lib().pic_store_usage(self.handle, ctypes.byref(u), ctypes.byref(c), ctypes.byref(n)))
+        return u.value, c.value, n.value
+
+
+def _req(chunk_offsets, chunk_ids, q_offsets, self_offsets, keep: list):
+    co = _host_i32(chunk_offsets)
+    ids = np.ascontiguousarray(chunk_ids, dtype=np.uint64)
+    qo = _host_i32(q_offsets)
+    so = _host_i32(self_offsets)
+    keep += [co, ids, qo, so]
+    return LinkReq(len(qo) - 1, 0, co.ctypes.data, ids.ctypes.data if ids.size else None,
+                   qo.ctypes.data, None if so is None else so.ctypes.data)
+
+
+def link_attn(store: Store, chunk_offsets, chunk_ids, q_offsets, self_offsets, n_q_heads: int, q,
+              k_self, v_self, softmax_scale: float, out, lse=None, stream: Optional[int] = None):
+    """pic_link_attn: prefill-shaped link attention."""
+    keep: list = []
+    req = _req(chunk_offsets, chunk_ids, q_offsets, self_offsets, keep)
+    _check(lib().pic_link_attn(store.handle, ctypes.byref(req), int(n_q_heads), _ptr(q), _ptr(k_self),
+                               _ptr(v_self), float(softmax_scale), _ptr(out), _ptr(lse), stream))
+
+
+def link_decode(store: Store, chunk_offsets, chunk_ids, q_offsets, self_offsets, n_q_heads: int, q,
+                k_self, v_self, softmax_scale: float, out, lse=None, num_splits: int = 0,
+                stream: Optional[int] = None):
+    """pic_link_decode: decode-shaped link attention with split-K."""
+    keep: list = []
+    req = _req(chunk_offsets, chunk_ids, q_offsets, self_offsets, keep)
+    _check(lib().pic_link_decode(store.handle, ctypes.byref(req), int(n_q_heads), _ptr(q), _ptr(k_self),
+                                 _ptr(v_self), float(softmax_scale), int(num_splits), _ptr(out),
+                                 _ptr(lse), stream))
+
+
+def debug_gather(store: Store, ids, k_out, v_out, stream: Optional[int] = None):
+    """pic_debug_gather: materialise the concatenation of the listed chunks."""
+    ids = np.ascontiguousarray(ids, dtype=np.uint64)
+    _check(lib().pic_debug_gather(store.handle, ids.ctypes.data if ids.size else None, len(ids),
+                                  _ptr(k_out), _ptr(v_out), stream))
+
+
+def prof_begin():
+    _check(lib().pic_prof_begin())
+
+
+def prof_end():
+    """(summed kernel milliseconds, launches, kernel name) since prof_begin()."""
+    ms, n = ctypes.c_double(), ctypes.c_int64()
+    name = ctypes.create_string_buffer(128)
+    _check(lib().pic_prof_end(ctypes.byref(ms), ctypes.byref(n), name, 128))
+    return ms.value, n.value, name.value.decode()

@@ -1,0 +1,306 @@
+"""GPU parity: the HIP path through the C ABI against the fp64 oracle.
+
+Tolerances (from the stated accuracy bar): bf16 inputs max-abs <= 2e-2 and
+mean-abs <= 2e-3 over the compared outputs; fp32 inputs max-abs and mean-abs
+<= 1e-4. The log-sum-exp is compared to 2e-3 (bf16) / 1e-4 (fp32) absolute.
+The gather hook must be bit-exact.
+"""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2602_01519_amd import pic, runner
+from paper_2602_01519_amd import workloads as W
+
+pytestmark = pytest.mark.gpu
+
+TOL = {W.F32: (1e-4, 1e-4, 1e-4), W.BF16: (2e-2, 2e-3, 2e-3)}
+
+
+def compare(cfg, out, lse, ref, ref_lse, sel=None, label=""):
+    if sel is not None:
+        rows = sel.reshape(out.shape[0], out.shape[1]).astype(bool)
+        out, ref, lse, ref_lse = out[rows], ref[rows], lse[rows], ref_lse[rows]
+    max_tol, mean_tol, lse_tol = TOL[cfg.dtype]
+    assert np.all(np.isfinite(out)), f"{label}: non-finite output"
+    err = np.abs(out - ref)
+    print(f"{label}: max_abs={err.max() if err.size else 0:.3e} mean_abs={err.mean() if err.size else 0:.3e} "
+          f"rel_l2={np.linalg.norm(err) / max(np.linalg.norm(ref), 1e-30):.3e}", flush=True)
+    if err.size:
+        assert err.max() <= max_tol, f"{label}: max abs err {err.max()}"
+        assert err.mean() <= mean_tol, f"{label}: mean abs err {err.mean()}"
+    fin = np.isfinite(ref_lse)
+    assert np.array_equal(fin, np.isfinite(lse)), f"{label}: lse finiteness differs"
+    assert np.all(np.isneginf(lse[~fin]))
+    if fin.any():
+        assert np.abs(lse[fin] - ref_lse[fin]).max() <= lse_tol, f"{label}: lse err"
+
+
+def run_and_check(cfg, decode=None, num_splits=0, requests=None):
+    wl = W.make_workload(cfg)
+    keep = None
+    sel = None
+    if requests is not None:
+        p = wl.plan
+        keep = set()
+        for r in requests:
+            keep |= set(int(c) for c in p.chunk_index[p.chunk_offsets[r]:p.chunk_offsets[r + 1]])
+        sel = np.zeros((wl.q.shape[0], cfg.n_q_heads), np.uint8)
+        for r in requests:
+            sel[p.q_offsets[r]:p.q_offsets[r + 1]] = 1
+        sel = sel.reshape(-1)
+    print(f"case {cfg.name}: decode={decode} splits={num_splits} requests={requests}", flush=True)
+    dw = runner.upload(wl, keep_host=keep)
+    try:
+        dw.run(decode=decode, num_splits=num_splits)
+        torch.cuda.synchronize()
+        out, lse = dw.results()
+        chunks = dict(dw.chunks)
+        if requests is not None:       # the oracle only needs the sampled requests' chunks
+            for c in range(cfg.store_chunks):
+                chunks.setdefault(c, None)
+            links = oracle.workload_links(wl, chunks)
+            links = [l if r in requests else [] for r, l in enumerate(links)]
+            ref, ref_lse = oracle.link_attn(
+                dtype=cfg.dtype, mla=cfg.kind == W.MLA, n_q_heads=cfg.n_q_heads, d_v=cfg.d_v,
+                links=links, q=wl.q, q_offsets=wl.plan.q_offsets, k_self=wl.k_self, v_self=wl.v_self,
+                self_offsets=wl.plan.self_offsets, tau=float(np.float32(cfg.scale)), row_select=sel)
+        else:
+            ref, ref_lse = oracle.run_workload(wl, chunks)
+        compare(cfg, out, lse, ref, ref_lse, sel, cfg.name)
+    finally:
+        dw.close()
+    return out, lse
+
+
+# ---------------------------------------------------------------------------
+# gather: bit-exact
+
+
+@pytest.mark.parametrize("dtype,kind,dk,dv", [(W.BF16, W.GQA, 128, 128), (W.F32, W.GQA, 64, 32),
+                                              (W.BF16, W.MLA, 576, 512)])
+def test_gather_is_bit_exact(dtype, kind, dk, dv):
+    cfg = W.small_config("gather", dtype=dtype, kind=kind, d_k=dk, d_v=dv,
+                         chunk_lens=(70, 64, 1, 130, 3), n_kv_heads=2)
+    store = pic.Store(kind, dtype, cfg.n_kv_heads, dk, dv, 4096)
+    host = {}
+    for i in range(cfg.store_chunks):
+        k, v = W.make_chunk(cfg, i)
+        store.put(1000 + i, k.shape[0], runner.to_device(k, "cuda"), runner.to_device(v, "cuda"))
+        host[i] = (k, v)
+    order = [3, 0, 4, 3, 1, 2, 0]
+    total = sum(host[i][0].shape[0] for i in order)
+    et = torch.int16 if dtype == W.BF16 else torch.float32
+    canary = 77
+    k_out = torch.full((total + 5, cfg.n_kv_heads, dk), canary, dtype=et, device="cuda")
+    v_out = None if kind == W.MLA else torch.full((total + 5, cfg.n_kv_heads, dv), canary, dtype=et,
+                                                  device="cuda")
+    pic.debug_gather(store, [1000 + i for i in order], k_out, v_out)
+    torch.cuda.synchronize()
+    kk = k_out.cpu().numpy()
+    want_k = np.concatenate([host[i][0] for i in order])
+    assert kk[:total].tobytes() == want_k.tobytes()
+    assert np.all(kk[total:] == canary)
+    if v_out is not None:
+        vv = v_out.cpu().numpy()
+        assert vv[:total].tobytes() == np.concatenate([host[i][1] for i in order]).tobytes()
+        assert np.all(vv[total:] == canary)
+    assert store.lookup(1002) == 1
+    used, cap, n = store.usage()
+    assert n == 5 and used == 128 + 64 + 64 + 192 + 64      # padded to 64-token multiples
+    store.close()
+
+
+# ---------------------------------------------------------------------------
+# small ragged workloads: every output row against the oracle
+
+SMALL = {
+    # MFMA path: d = 128 bf16 GQA; ragged chunks, several 128-row blocks, own tiles
+    "mfma_gqa4": W.small_config("mfma_gqa4", d_k=128, chunk_lens=(70, 64, 1, 130, 200), batch=3,
+                                links=(0, 4), q_len=(37, 5, 130), self_len=(41, 5, 130)),
+    "mfma_cross_only": W.small_config("mfma_cross_only", d_k=128, chunk_lens=(70, 64, 1, 130),
+                                      batch=2, links=(1, 3), q_len=(40, 3), self_len=None),
+    "mfma_mha": W.small_config("mfma_mha", d_k=128, n_q_heads=4, n_kv_heads=4,
+                               chunk_lens=(64, 129), batch=2, links=(1, 2), q_len=(70, 1),
+                               self_len=(70, 66)),
+    "mfma_mqa": W.small_config("mfma_mqa", d_k=128, n_q_heads=8, n_kv_heads=1,
+                               chunk_lens=(100, 28), batch=1, links=(2, 2), q_len=50, self_len=50),
+    "mfma_no_chunks": W.small_config("mfma_no_chunks", d_k=128, chunk_lens=(64,), batch=2,
+                                     links=(0, 0), q_len=(65, 7), self_len=(65, 20)),
+    "valu_bf16_d64": W.small_config("valu_bf16_d64", d_k=64, chunk_lens=(70, 64, 1, 130),
+                                    batch=2, links=(1, 3), q_len=(37, 5), self_len=(41, 5)),
+    "valu_f32_d64": W.small_config("valu_f32_d64", dtype=W.F32, d_k=64, chunk_lens=(70, 64, 1, 130),
+                                   batch=2, links=(1, 3), q_len=(37, 5), self_len=(41, 5)),
+    "valu_f32_dv32": W.small_config("valu_f32_dv32", dtype=W.F32, d_k=64, d_v=32,
+                                    chunk_lens=(9, 64, 77), batch=2, links=(1, 3), q_len=(3, 12),
+                                    self_len=(3, 20)),
+    "valu_mla": W.small_config("valu_mla", kind=W.MLA, n_q_heads=16, d_k=576, d_v=512,
+                               chunk_lens=(70, 64, 1, 130), batch=2, links=(1, 3), q_len=(9, 4),
+                               self_len=(9, 6), q_std=1.0, scale=1 / math.sqrt(192)),
+    "valu_mla_f32": W.small_config("valu_mla_f32", dtype=W.F32, kind=W.MLA, n_q_heads=4, d_k=64,
+                                   d_v=32, chunk_lens=(70, 1, 65), batch=2, links=(1, 3),
+                                   q_len=(9, 4), self_len=(9, 6)),
+}
+
+
+@pytest.mark.parametrize("name", sorted(SMALL))
+def test_small_parity(name):
+    run_and_check(SMALL[name])
+
+
+DECODE = W.small_config("decode_small", d_k=128, n_q_heads=32, n_kv_heads=8,
+                        chunk_lens=(1024, 700, 64, 1, 300, 512), batch=5, links=(0, 4), q_len=1,
+                        self_len=(128, 1, 65, 3, 200), decode=True)
+
+
+@pytest.mark.parametrize("splits", [1, 2, 7, 0])
+def test_decode_splits(splits):
+    run_and_check(DECODE, decode=True, num_splits=splits)
+
+
+def test_decode_f32_and_multi_token():
+    cfg = W.small_config("decode_f32", dtype=W.F32, d_k=64, chunk_lens=(200, 64, 9), batch=3,
+                         links=(1, 3), q_len=(1, 4, 16), self_len=(5, 4, 40), decode=True)
+    run_and_check(cfg, decode=True, num_splits=3)
+
+
+def test_prefill_and_decode_agree_on_single_token_requests():
+    cfg = DECODE
+    a, la = run_and_check(cfg, decode=False)
+    b, lb = run_and_check(cfg, decode=True, num_splits=5)
+    assert np.abs(a - b).max() <= 2e-2
+    assert np.abs(la - lb).max() <= 2e-3
+
+
+# ---------------------------------------------------------------------------
+# the five benchmark workloads at their full sizes (sampled requests where the
+# oracle would take minutes)
+
+
+def test_config_tiny_f32():
+    run_and_check(W.CONFIGS["tiny_f32"])
+
+
+def test_config_llama_prefill():
+    run_and_check(W.CONFIGS["llama_prefill"], requests=[0, 5])
+
+
+def test_config_long_rag():
+    cfg = W.CONFIGS["long_rag"]
+    p = W.make_plan(cfg)
+    n = np.diff(p.chunk_offsets)
+    run_and_check(cfg, requests=[int(np.argmax(n)), int(np.argmin(n))])
+
+
+def test_config_decode():
+    run_and_check(W.CONFIGS["decode"], requests=[0, 17, 63])
+
+
+def test_config_mla():
+    run_and_check(W.CONFIGS["mla"], requests=[3])
+
+
+# ---------------------------------------------------------------------------
+# invariants on the GPU
+
+
+def test_chunk_order_permutation_on_gpu():
+    cfg = SMALL["mfma_gqa4"]
+    wl = W.make_workload(cfg)
+    dw = runner.upload(wl)
+    try:
+        dw.run()
+        torch.cuda.synchronize()
+        a, la = dw.results()
+        p = wl.plan
+        ids = wl.link_ids().copy()
+        for r in range(p.batch):
+            s, e = p.chunk_offsets[r], p.chunk_offsets[r + 1]
+            ids[s:e] = ids[s:e][::-1]
+        stream = torch.cuda.current_stream().cuda_stream
+        pic.link_attn(dw.store, p.chunk_offsets, ids, p.q_offsets, p.self_offsets, cfg.n_q_heads, dw.q,
+                      dw.k_self, dw.v_self, float(np.float32(cfg.scale)), dw.out, dw.lse, stream=stream)
+        torch.cuda.synchronize()
+        b, lb = dw.results()
+        assert np.abs(a - b).max() <= 2e-2 and np.abs(a - b).mean() <= 2e-3
+        assert np.abs(la - lb).max() <= 1e-3
+    finally:
+        dw.close()
+
+
+# ---------------------------------------------------------------------------
+# error paths: nothing is launched, outputs stay untouched
+
+
+def _canary_case():
+    cfg = W.small_config("err", d_k=128, chunk_lens=(64, 32), batch=1, links=(2, 2), q_len=4,
+                         self_len=4)
+    wl = W.make_workload(cfg)
+    dw = runner.upload(wl)
+    dw.out.fill_(1234)
+    dw.lse.fill_(5.0)
+    torch.cuda.synchronize()
+    return cfg, wl, dw
+
+
+def _untouched(dw):
+    torch.cuda.synchronize()
+    return bool(torch.all(dw.out == 1234)) and bool(torch.all(dw.lse == 5.0))
+
+
+def test_unknown_chunk_id_is_not_found_and_launches_nothing():
+    cfg, wl, dw = _canary_case()
+    p = wl.plan
+    ids = wl.link_ids().copy()
+    ids[1] = 0xDEADBEEF
+    with pytest.raises(pic.PicError) as e:
+        pic.link_attn(dw.store, p.chunk_offsets, ids, p.q_offsets, p.self_offsets, cfg.n_q_heads,
+                      dw.q, dw.k_self, dw.v_self, 1.0, dw.out, dw.lse)
+    assert e.value.status == pic.ERR_NOT_FOUND
+    assert _untouched(dw)
+    dw.close()
+
+
+def test_invalid_calls_launch_nothing():
+    cfg, wl, dw = _canary_case()
+    p = wl.plan
+    ids = wl.link_ids()
+    call = lambda **kw: pic.link_attn(
+        dw.store, kw.get("co", p.chunk_offsets), ids, kw.get("qo", p.q_offsets), kw.get("so", p.self_offsets),
+        kw.get("hq", cfg.n_q_heads), dw.q, dw.k_self, dw.v_self, kw.get("scale", 1.0), dw.out, dw.lse)
+    for kw in [dict(hq=7), dict(scale=0.0), dict(scale=float("nan")), dict(qo=[0, 5]),
+               dict(co=[1, 2]), dict(so=[0, 3])]:
+        with pytest.raises(pic.PicError) as e:
+            call(**kw)
+        assert e.value.status == pic.ERR_INVALID, kw
+    with pytest.raises(pic.PicError) as e:      # more than 16 query tokens for decode
+        q17 = np.array([0, 17], np.int32)
+        pic.link_decode(dw.store, p.chunk_offsets, ids, q17, np.array([0, 17], np.int32), cfg.n_q_heads,
+                        dw.q, dw.k_self, dw.v_self, 1.0, dw.out, dw.lse)
+    assert e.value.status == pic.ERR_INVALID
+    assert _untouched(dw)
+    dw.close()
+
+
+def test_store_put_errors():
+    store = pic.Store(W.GQA, W.BF16, 2, 64, 64, 128)
+    k = torch.zeros((64, 2, 64), dtype=torch.int16, device="cuda")
+    store.put(1, 64, k, k)
+    with pytest.raises(pic.PicError) as e:
+        store.put(1, 64, k, k)
+    assert e.value.status == pic.ERR_EXISTS
+    store.put(2, 10, k, k)                       # padded to 64: pool now full
+    with pytest.raises(pic.PicError) as e:
+        store.put(3, 1, k, k)
+    assert e.value.status == pic.ERR_OOM
+    host = np.zeros((64, 2, 64), np.int16)
+    with pytest.raises(pic.PicError) as e:
+        store.put(4, 64, host, host)
+    assert e.value.status in (pic.ERR_INVALID, pic.ERR_OOM)
+    with pytest.raises(pic.PicError) as e:
+        store.lookup(99)
+    assert e.value.status == pic.ERR_NOT_FOUND
+    store.close()
