@@ -81,21 +81,22 @@ __device__ __forceinline__ int find_link(const LinkEntry *links, int n, int64_t 
   return lo;
 }
 
-// Element offset (from the pool base) of key row `row` of head `head` in a link.
-__device__ __forceinline__ int64_t key_row_off(const LinkEntry &e, int head, int row, int d_k) {
-  return e.k_off + ((int64_t)head * e.lp + row) * d_k;
+// Key row `row` of head `head` in a slot (GQA head-major K; MLA has one head).
+template <typename E>
+__device__ __forceinline__ const E *key_row(const LinkEntry &e, int head, int row, int d_k) {
+  return (const E *)e.k + ((int64_t)head * e.lp + row) * d_k;
 }
-// Element offset of value dim `dim` of token `row` (GQA, transposed V block).
-__device__ __forceinline__ int64_t value_off(const LinkEntry &e, int head, int dim, int row,
+// Value dim `dim` of token `row` of head `head` (GQA transposed V block).
+template <typename E>
+__device__ __forceinline__ const E *value_at(const LinkEntry &e, int head, int dim, int row,
                                              int d_v) {
-  return e.v_off + ((int64_t)head * d_v + dim) * e.lp + row;
+  return (const E *)e.v + ((int64_t)head * d_v + dim) * e.lp + row;
 }
 
 template <typename E>
-__global__ void gather_kernel(const E *__restrict__ pool, const LinkEntry *__restrict__ links,
-                              int32_t n_links, int64_t total, int32_t heads, int32_t d_k,
-                              int32_t d_v, int32_t mla, E *__restrict__ k_out,
-                              E *__restrict__ v_out) {
+__global__ void gather_kernel(const LinkEntry *__restrict__ links, int32_t n_links, int64_t total,
+                              int32_t heads, int32_t d_k, int32_t d_v, int32_t mla,
+                              E *__restrict__ k_out, E *__restrict__ v_out) {
   const int64_t nk = total * heads * d_k;
   const int64_t nv = mla ? 0 : total * heads * d_v;
   for (int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; idx < nk + nv;
@@ -105,15 +106,71 @@ __global__ void gather_kernel(const E *__restrict__ pool, const LinkEntry *__res
       const int h = (int)((idx / d_k) % heads);
       const int c = (int)(idx % d_k);
       const LinkEntry e = links[find_link(links, n_links, j)];
-      k_out[idx] = pool[key_row_off(e, mla ? 0 : h, (int)(j - e.tok0), d_k) + c];
+      k_out[idx] = key_row<E>(e, mla ? 0 : h, (int)(j - e.tok0), d_k)[c];
     } else {
       const int64_t x = idx - nk;
       const int64_t j = x / ((int64_t)heads * d_v);
       const int h = (int)((x / d_v) % heads);
       const int c = (int)(x % d_v);
       const LinkEntry e = links[find_link(links, n_links, j)];
-      v_out[x] = pool[value_off(e, h, c, (int)(j - e.tok0), d_v)];
+      v_out[x] = *value_at<E>(e, h, c, (int)(j - e.tok0), d_v);
     }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Own KV of a request laid out like a chunk slot (at its last link): K rows
+// head-major, V transposed, zero padding up to lp. One launch per call,
+// blockIdx.z = request.
+
+__global__ void prep_own_rows_kernel(const ReqEntry *__restrict__ reqs,
+                                     const LinkEntry *__restrict__ links,
+                                     const uint4 *__restrict__ src, int32_t heads, int32_t vpr) {
+  const ReqEntry R = reqs[blockIdx.z];
+  if (R.ls == 0) return;
+  const LinkEntry E = links[R.link0 + R.nlinks - 1];
+  uint4 *dst = (uint4 *)E.k;
+  const int64_t total = (int64_t)heads * E.lp * vpr;
+  for (int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; idx < total;
+       idx += (int64_t)gridDim.x * blockDim.x) {
+    const int64_t h = idx / ((int64_t)E.lp * vpr);
+    const int64_t rem = idx - h * E.lp * vpr;
+    const int64_t t = rem / vpr;
+    const int64_t c = rem - t * vpr;
+    uint4 v = make_uint4(0, 0, 0, 0);
+    if (t < R.ls) v = src[((R.s0 + t) * heads + h) * vpr + c];
+    dst[idx] = v;
+  }
+}
+
+template <typename E>
+__global__ void prep_own_transposed_kernel(const ReqEntry *__restrict__ reqs,
+                                           const LinkEntry *__restrict__ links,
+                                           const E *__restrict__ src, int32_t heads,
+                                           int32_t width) {
+  __shared__ E tile[64][65];
+  const ReqEntry R = reqs[blockIdx.z];
+  if (R.ls == 0) return;
+  const LinkEntry L = links[R.link0 + R.nlinks - 1];
+  const int64_t t0 = (int64_t)blockIdx.x * 64;
+  if (t0 >= L.lp) return;
+  const int eblocks = (width + 63) / 64;
+  const int h = blockIdx.y / eblocks;
+  const int e0 = (blockIdx.y % eblocks) * 64;
+  E *dst = (E *)L.v;
+  for (int i = threadIdx.x; i < 64 * 64; i += blockDim.x) {
+    const int tl = i >> 6, el = i & 63;
+    const int64_t t = t0 + tl;
+    const int e = e0 + el;
+    E v = E(0);
+    if (t < R.ls && e < width) v = src[((R.s0 + t) * heads + h) * width + e];
+    tile[tl][el] = v;
+  }
+  __syncthreads();
+  for (int i = threadIdx.x; i < 64 * 64; i += blockDim.x) {
+    const int el = i >> 6, tl = i & 63;
+    const int e = e0 + el;
+    if (e < width) dst[((int64_t)h * width + e) * L.lp + t0 + tl] = tile[tl][el];
   }
 }
 
@@ -147,10 +204,7 @@ __global__ __launch_bounds__(256) void link_valu_kernel(LinkParams p) {
   const int t_begin = (int)((int64_t)R.tiles * split / p.num_splits);
   const int t_end = (int)((int64_t)R.tiles * (split + 1) / p.num_splits);
 
-  const T *__restrict__ pool = (const T *)p.pool;
   const T *__restrict__ q = (const T *)p.q;
-  const T *__restrict__ k_self = (const T *)p.k_self;
-  const T *__restrict__ v_self = (const T *)p.v_self;
 
   constexpr int EPW = 4 / sizeof(T);          // elements per 32-bit word
   const int kwords = d_k / EPW;                // words per K row
@@ -162,7 +216,7 @@ __global__ __launch_bounds__(256) void link_valu_kernel(LinkParams p) {
   uint32_t *vts = ks + kTile * kstride;                      // [d_v][vstride] (GQA)
   float4 *pb = (float4 *)(vts + (MLA ? 0 : d_v * vstride));  // [4][64]
   const T *ks_e = (const T *)ks;
-  T *vts_e = (T *)vts;
+  const T *vts_e = (const T *)vts;
 
   for (int x = threadIdx.x; x < kValuRows * d_k; x += blockDim.x) {
     const int rl = x / d_k, c = x - rl * d_k;
@@ -196,45 +250,23 @@ __global__ __launch_bounds__(256) void link_valu_kernel(LinkParams p) {
   int li = 0;
   for (int t = t_begin; t < t_end; ++t) {
     const bool own = t >= R.doc_tiles;
-    int nvalid, j0 = 0;
     __syncthreads();
-    if (!own) {
-      while (p.links[R.link0 + li].tile0 + p.links[R.link0 + li].lp / kTile <= t) ++li;
-      const LinkEntry E = p.links[R.link0 + li];
-      const int tt = t - E.tile0;
-      nvalid = min(kTile, E.len - tt * kTile);
-      // 64 consecutive key rows (padding rows of the slot are zeros)
-      const uint32_t *src = (const uint32_t *)(pool + E.k_off +
-                                               ((int64_t)(MLA ? 0 : kvh) * E.lp + tt * kTile) * d_k);
-      for (int w = threadIdx.x; w < kTile * kwords; w += blockDim.x) {
-        const int r = w / kwords, c = w - r * kwords;
-        ks[r * kstride + c] = src[w];
-      }
-      if (!MLA) {
-        const T *vsrc = pool + E.v_off + (int64_t)kvh * d_v * E.lp + tt * kTile;
-        for (int w = threadIdx.x; w < d_v * vwords; w += blockDim.x) {
-          const int e = w / vwords, c = w - e * vwords;
-          vts[e * vstride + c] = ((const uint32_t *)(vsrc + (int64_t)e * E.lp))[c];
-        }
-      }
-    } else {
-      j0 = (t - R.doc_tiles) * kTile;
-      nvalid = min(kTile, R.ls - j0);
-      for (int w = threadIdx.x; w < kTile * kwords; w += blockDim.x) {
-        const int r = w / kwords, c = w - r * kwords;
-        uint32_t v = 0;
-        if (r < nvalid)
-          v = ((const uint32_t *)(k_self + ((int64_t)(R.s0 + j0 + r) * p.n_kv_heads + kvh) * d_k))[c];
-        ks[r * kstride + c] = v;
-      }
-      if (!MLA) {
-        const int vrow = vstride * EPW;
-        for (int x = threadIdx.x; x < kTile * d_v; x += blockDim.x) {
-          const int r = x / d_v, e = x - r * d_v;
-          T v = T(0);
-          if (r < nvalid) v = v_self[((int64_t)(R.s0 + j0 + r) * p.n_kv_heads + kvh) * d_v + e];
-          vts_e[e * vrow + r] = v;
-        }
+    while (p.links[R.link0 + li].tile0 + p.links[R.link0 + li].lp / kTile <= t) ++li;
+    const LinkEntry E = p.links[R.link0 + li];
+    const int tt = t - E.tile0;
+    const int nvalid = min(kTile, E.len - tt * kTile);
+    const int j0 = tt * kTile;          // key index within the link (own: within the own KV)
+    // 64 consecutive key rows (the slot's padding rows are zeros)
+    const uint32_t *src = (const uint32_t *)key_row<T>(E, MLA ? 0 : kvh, tt * kTile, d_k);
+    for (int w = threadIdx.x; w < kTile * kwords; w += blockDim.x) {
+      const int r = w / kwords, c = w - r * kwords;
+      ks[r * kstride + c] = src[w];
+    }
+    if (!MLA) {
+      const T *vsrc = value_at<T>(E, kvh, 0, tt * kTile, d_v);
+      for (int w = threadIdx.x; w < d_v * vwords; w += blockDim.x) {
+        const int e = w / vwords, c = w - e * vwords;
+        vts[e * vstride + c] = ((const uint32_t *)(vsrc + (int64_t)e * E.lp))[c];
       }
     }
     __syncthreads();
@@ -447,20 +479,38 @@ hipError_t launch_put_transposed(const void *src, void *dst, int64_t n_tokens, i
   return hipGetLastError();
 }
 
-hipError_t launch_gather(const void *pool, const LinkEntry *links, int32_t n_links,
-                         int64_t total_tokens, int32_t heads, int32_t d_k, int32_t d_v,
-                         int32_t mla, int32_t esz, void *k_out, void *v_out, hipStream_t st) {
+hipError_t launch_gather(const LinkEntry *links, int32_t n_links, int64_t total_tokens,
+                         int32_t heads, int32_t d_k, int32_t d_v, int32_t mla, int32_t esz,
+                         void *k_out, void *v_out, hipStream_t st) {
   const int64_t n = total_tokens * heads * (d_k + (mla ? 0 : d_v));
   if (n == 0) return hipSuccess;
   const unsigned blocks = (unsigned)std::min<int64_t>((n + 255) / 256, 65536);
   if (esz == 2)
-    hipLaunchKernelGGL(gather_kernel<uint16_t>, dim3(blocks), dim3(256), 0, st,
-                       (const uint16_t *)pool, links, n_links, total_tokens, heads, d_k, d_v, mla,
-                       (uint16_t *)k_out, (uint16_t *)v_out);
+    hipLaunchKernelGGL(gather_kernel<uint16_t>, dim3(blocks), dim3(256), 0, st, links, n_links,
+                       total_tokens, heads, d_k, d_v, mla, (uint16_t *)k_out, (uint16_t *)v_out);
   else
-    hipLaunchKernelGGL(gather_kernel<uint32_t>, dim3(blocks), dim3(256), 0, st,
-                       (const uint32_t *)pool, links, n_links, total_tokens, heads, d_k, d_v, mla,
-                       (uint32_t *)k_out, (uint32_t *)v_out);
+    hipLaunchKernelGGL(gather_kernel<uint32_t>, dim3(blocks), dim3(256), 0, st, links, n_links,
+                       total_tokens, heads, d_k, d_v, mla, (uint32_t *)k_out, (uint32_t *)v_out);
+  return hipGetLastError();
+}
+
+hipError_t launch_prep_own(const LinkParams &p, int32_t mla, int32_t esz, int32_t max_own_lp,
+                           hipStream_t st) {
+  if (max_own_lp == 0 || p.batch == 0) return hipSuccess;
+  const int32_t vpr = p.d_k * esz / 16;
+  const int64_t per_req = (int64_t)p.n_kv_heads * max_own_lp * vpr;
+  const unsigned bx = (unsigned)std::min<int64_t>((per_req + 255) / 256, 4096);
+  hipLaunchKernelGGL(prep_own_rows_kernel, dim3(bx, 1, p.batch), dim3(256), 0, st, p.reqs, p.links,
+                     (const uint4 *)p.k_self, p.n_kv_heads, vpr);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess || mla) return e;
+  dim3 grid(max_own_lp / 64, p.n_kv_heads * ((p.d_v + 63) / 64), p.batch);
+  if (esz == 2)
+    hipLaunchKernelGGL(prep_own_transposed_kernel<uint16_t>, grid, dim3(256), 0, st, p.reqs, p.links,
+                       (const uint16_t *)p.v_self, p.n_kv_heads, p.d_v);
+  else
+    hipLaunchKernelGGL(prep_own_transposed_kernel<uint32_t>, grid, dim3(256), 0, st, p.reqs, p.links,
+                       (const uint32_t *)p.v_self, p.n_kv_heads, p.d_v);
   return hipGetLastError();
 }
 

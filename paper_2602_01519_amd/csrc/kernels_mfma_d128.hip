@@ -52,111 +52,78 @@ __device__ __forceinline__ int key_of_m(int m) {
   return (a >> 1) * 16 + gg * 8 + (a & 1) * 4 + c;
 }
 
-__device__ __forceinline__ bf16x8 as_bf16x8(uint4 u) {
-  return __builtin_bit_cast(bf16x8, u);
-}
+__device__ __forceinline__ bf16x8 as_bf16x8(uint4 u) { return __builtin_bit_cast(bf16x8, u); }
 
-// One tile's worth of global loads, held in registers between the load and
-// the LDS store so the loads overlap the previous tile's math.
-struct TileRegs {
-  uint4 k[4];
-  uint4 v[4];
-};
+typedef __attribute__((address_space(3))) void *lds_ptr;
 
-struct TileSrc {
-  bool own;
-  int nvalid;     // valid keys in the tile
-  int j0;         // own-key index of the tile's first key (own tiles)
-  const uint16_t *kbase;   // doc: first K row of the tile; own: k_self row 0 of the request
-  const uint16_t *vbase;   // doc: V^T row 0 at the tile's first key; own: v_self row 0
-  int64_t vstride;         // doc: elements between V^T rows (= lp); own: unused
-};
-
-__device__ __forceinline__ TileSrc resolve_tile(const LinkParams &p, const ReqEntry &R, int kvh,
-                                                int t, int &li) {
-  TileSrc s;
-  const uint16_t *pool = (const uint16_t *)p.pool;
-  if (t < R.doc_tiles) {
-    while (p.links[R.link0 + li].tile0 + p.links[R.link0 + li].lp / kTile <= t) ++li;
-    const LinkEntry E = p.links[R.link0 + li];
-    const int tt = t - E.tile0;
-    s.own = false;
-    s.nvalid = min(kTile, E.len - tt * kTile);
-    s.j0 = 0;
-    s.kbase = pool + E.k_off + ((int64_t)kvh * E.lp + tt * kTile) * kD;
-    s.vbase = pool + E.v_off + (int64_t)kvh * kD * E.lp + tt * kTile;
-    s.vstride = E.lp;
-  } else {
-    s.own = true;
-    s.j0 = (t - R.doc_tiles) * kTile;
-    s.nvalid = min(kTile, R.ls - s.j0);
-    s.kbase = (const uint16_t *)p.k_self + ((int64_t)R.s0 * p.n_kv_heads + kvh) * kD;
-    s.vbase = (const uint16_t *)p.v_self + ((int64_t)R.s0 * p.n_kv_heads + kvh) * kD;
-    s.vstride = 0;
-  }
-  return s;
-}
-
-__device__ __forceinline__ void load_tile(const TileSrc &s, int n_kv_heads, TileRegs &r) {
-  const int tid = threadIdx.x;
-  if (!s.own) {
-#pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      const int idx = tid + 256 * u;          // 1024 chunks: key = idx/16, c = idx%16
-      r.k[u] = ((const uint4 *)s.kbase)[idx];
-      const int e = idx >> 3, c = idx & 7;    // 1024 chunks: dv = idx/8, keys c*8..
-      r.v[u] = *(const uint4 *)(s.vbase + (int64_t)e * s.vstride + c * 8);
-    }
-  } else {
-    const int64_t rs = (int64_t)n_kv_heads * kD;   // elements between own rows
-#pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      const int idx = tid + 256 * u;
-      const int key = idx >> 4, c = idx & 15;
-      uint4 kv = make_uint4(0, 0, 0, 0), vv = make_uint4(0, 0, 0, 0);
-      if (key < s.nvalid) {
-        kv = *(const uint4 *)(s.kbase + (int64_t)(s.j0 + key) * rs + c * 8);
-        vv = *(const uint4 *)(s.vbase + (int64_t)(s.j0 + key) * rs + c * 8);
-      }
-      r.k[u] = kv;
-      r.v[u] = vv;       // 8 value dims (c*8 ..) of one key
-    }
-  }
-}
-
-__device__ __forceinline__ void store_tile(const TileSrc &s, const TileRegs &r, Smem &sm, int buf) {
-  const int tid = threadIdx.x;
+// Starts the copy of key tile tt of link E (kv head kvh) into LDS buffers
+// kdst / vdst with direct global->LDS loads: lane i of a load lands at slot
+// base + i, so each lane fetches the global chunk that belongs at that slot
+// of the swizzled layout. 4 K loads + 4 V loads per lane, 16 bytes each.
+__device__ __forceinline__ void issue_tile(const LinkEntry &E, int kvh, int tt, uint4 *kdst,
+                                           uint4 *vdst, int wave, int lane) {
+  const uint16_t *kb = (const uint16_t *)E.k + ((int64_t)kvh * E.lp + tt * kTile) * kD;
+  const uint16_t *vb = (const uint16_t *)E.v + (int64_t)kvh * kD * E.lp + tt * kTile;
 #pragma unroll
   for (int u = 0; u < 4; ++u) {
-    const int idx = tid + 256 * u;
-    sm.k[buf][k_slot(idx >> 4, idx & 15)] = r.k[u];
-  }
-  if (!s.own) {
-#pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      const int idx = tid + 256 * u;
-      sm.vt[buf][v_slot(idx >> 3, idx & 7)] = r.v[u];
-    }
-  } else {
-    // token-major own values: scatter the 8 dims of one key into V^T
-    uint16_t *vt16 = (uint16_t *)sm.vt[buf];
-#pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      const int idx = tid + 256 * u;
-      const int key = idx >> 4, c = idx & 15;
-      const uint16_t *vals = (const uint16_t *)&r.v[u];
-#pragma unroll
-      for (int x = 0; x < 8; ++x) {
-        const int dv = c * 8 + x;
-        vt16[v_slot(dv, key >> 3) * 8 + (key & 7)] = vals[x];
-      }
-    }
+    const int base = (u * kWaves + wave) * 64;
+    const int s = base + lane;
+    const int key = s >> 4, kc = (s & 15) ^ (key & 15);
+    __builtin_amdgcn_global_load_lds(kb + key * kD + kc * 8, (lds_ptr)(kdst + base), 16, 0, 0);
+    const int dv = s >> 3, vc = (s & 7) ^ (dv & 7);
+    __builtin_amdgcn_global_load_lds(vb + (int64_t)dv * E.lp + vc * 8, (lds_ptr)(vdst + base), 16,
+                                     0, 0);
   }
 }
 
-__global__ __launch_bounds__(256, 1) void link_mfma_d128_kernel(LinkParams p) {
+// Sum / max of a value over lanes i and i ^ 32 (the two key halves of a row).
+__device__ __forceinline__ float half_swap_max(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false,
+                                                  false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ __forceinline__ float half_swap_sum(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false,
+                                                  false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+
+// The request's link table is read through a window of kWin entries staged
+// in LDS, so walking tiles costs LDS reads instead of dependent global loads.
+constexpr int kWin = 32;
+
+struct LinkCursor {
+  int li = 0;       // current link (index within the request)
+  int wb = 0;       // first link held in the window
+};
+
+__device__ __forceinline__ void load_window(const LinkParams &p, const ReqEntry &R, LinkEntry *win,
+                                            int wb) {
+  const int n = min(kWin, R.nlinks - wb);
+  for (int i = threadIdx.x; i < n; i += blockDim.x) win[i] = p.links[R.link0 + wb + i];
+}
+
+// Moves the cursor to the link holding tile t (t only grows) and returns it.
+// Uniform across the workgroup: it may reload the window between barriers.
+__device__ __forceinline__ LinkEntry advance(const LinkParams &p, const ReqEntry &R,
+                                             LinkEntry *win, LinkCursor &cur, int t) {
+  for (;;) {
+    if (cur.li - cur.wb >= kWin) {
+      __syncthreads();
+      cur.wb += kWin;
+      load_window(p, R, win, cur.wb);
+      __syncthreads();
+    }
+    const LinkEntry e = win[cur.li - cur.wb];
+    if (t < e.tile0 + e.lp / kTile) return e;
+    ++cur.li;
+  }
+}
+
+__global__ __launch_bounds__(256, 2) void link_mfma_d128_kernel(LinkParams p) {
   __shared__ Smem sm;
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int n = lane & 31, g = lane >> 5;
 
   // XCD-aware work mapping: consecutive blocks go round-robin to the 8 XCDs;
@@ -186,6 +153,20 @@ __global__ __launch_bounds__(256, 1) void link_mfma_d128_kernel(LinkParams p) {
   const int lim = rvalid ? qi + R.ls - R.lq : -1;     // last visible own key
   const int64_t orow = (int64_t)(R.q0 + qi) * p.n_q_heads + qh;
 
+  __shared__ LinkEntry win[kWin];
+  LinkCursor cur;
+  load_window(p, R, win, 0);
+  __syncthreads();
+  // masking facts of the tile being computed: valid keys, own-KV key offset
+  int nvalid_cur = kTile, j0_cur = 0;
+  if (t_begin < t_end) {
+    const LinkEntry E = advance(p, R, win, cur, t_begin);
+    const int tt = t_begin - E.tile0;
+    issue_tile(E, kvh, tt, sm.k[0], sm.vt[0], wave, lane);
+    nvalid_cur = min(kTile, E.len - tt * kTile);
+    j0_cur = tt * kTile;
+  }
+
   // Q fragments: d = step*16 + g*8 + (0..7)
   bf16x8 qf[8];
   {
@@ -205,61 +186,62 @@ __global__ __launch_bounds__(256, 1) void link_mfma_d128_kernel(LinkParams p) {
     for (int x = 0; x < 16; ++x) o[d][x] = 0.f;
   float m_used = -INFINITY, lsum = 0.f;
   const float c = p.scale_log2;
+  const int krow0 = key_of_m(n);      // key row feeding this lane's M index, block 0
+  typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+  const bf16x2 ones = {(__bf16)1.0f, (__bf16)1.0f};
 
-  int li = 0;
-  TileRegs regs;
-  TileSrc cur = resolve_tile(p, R, kvh, t_begin < t_end ? t_begin : 0, li);
-  if (t_begin < t_end) {
-    load_tile(cur, p.n_kv_heads, regs);
-    store_tile(cur, regs, sm, 0);
-  }
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
   __syncthreads();
 
-  const int krow0 = key_of_m(n);      // key row feeding this lane's M index, block 0
   for (int t = t_begin; t < t_end; ++t) {
     const int buf = (t - t_begin) & 1;
-    TileSrc nxt;
-    const bool more = t + 1 < t_end;
-    if (more) {
-      nxt = resolve_tile(p, R, kvh, t + 1, li);
-      load_tile(nxt, p.n_kv_heads, regs);
+    const int nvalid = nvalid_cur, j0 = j0_cur;
+    const bool own = t >= R.doc_tiles;
+    if (t + 1 < t_end) {
+      const LinkEntry E = advance(p, R, win, cur, t + 1);
+      const int tt = t + 1 - E.tile0;
+      issue_tile(E, kvh, tt, sm.k[buf ^ 1], sm.vt[buf ^ 1], wave, lane);
+      nvalid_cur = min(kTile, E.len - tt * kTile);
+      j0_cur = tt * kTile;
     }
 
     // ---- S^T = K Q^T : two 32-key blocks
-    f32x16 s[2];
+    const uint4 *kt = sm.k[buf];
+    bf16x8 ka[8], kb[8];
 #pragma unroll
-    for (int b = 0; b < 2; ++b) {
+    for (int st = 0; st < 8; ++st) {
+      ka[st] = as_bf16x8(kt[k_slot(krow0, st * 2 + g)]);
+      kb[st] = as_bf16x8(kt[k_slot(32 + krow0, st * 2 + g)]);
+    }
+    f32x16 s0, s1;
 #pragma unroll
-      for (int x = 0; x < 16; ++x) s[b][x] = 0.f;
-      const int krow = b * 32 + krow0;
+    for (int x = 0; x < 16; ++x) { s0[x] = 0.f; s1[x] = 0.f; }
 #pragma unroll
-      for (int st = 0; st < 8; ++st) {
-        const bf16x8 kf = as_bf16x8(sm.k[buf][k_slot(krow, st * 2 + g)]);
-        s[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[st], s[b], 0, 0, 0);
-      }
+    for (int st = 0; st < 8; ++st) {
+      s0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka[st], qf[st], s0, 0, 0, 0);
+      s1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kb[st], qf[st], s1, 0, 0, 0);
     }
 
     // ---- masking (only on ragged or own tiles)
-    // s[b][x] is the score of key b*32 + (x>>3)*16 + g*8 + (x&7) for this row
-    if (cur.own || cur.nvalid < kTile) {
-      const int kl = cur.own ? lim - cur.j0 : kTile;     // visible iff key <= kl
-      const int kv = cur.nvalid;
+    // s_b[x] is the score of key b*32 + (x>>3)*16 + g*8 + (x&7) for this row
+    if (own || nvalid < kTile) {
+      const int kl = own ? lim - j0 : kTile;     // visible iff key <= kl
 #pragma unroll
-      for (int b = 0; b < 2; ++b)
-#pragma unroll
-        for (int x = 0; x < 16; ++x) {
-          const int key = b * 32 + (x >> 3) * 16 + g * 8 + (x & 7);
-          if (key >= kv || key > kl) s[b][x] = -INFINITY;
-        }
+      for (int x = 0; x < 16; ++x) {
+        const int key = (x >> 3) * 16 + g * 8 + (x & 7);
+        if (key >= nvalid || key > kl) s0[x] = -INFINITY;
+        if (key + 32 >= nvalid || key + 32 > kl) s1[x] = -INFINITY;
+      }
     }
 
     // ---- online softmax (log2 domain, lazy rescale)
     float tmax = -INFINITY;
 #pragma unroll
-    for (int b = 0; b < 2; ++b)
-#pragma unroll
-      for (int x = 0; x < 16; x += 2) tmax = fmaxf(fmaxf(tmax, s[b][x]), s[b][x + 1]);
-    tmax = fmaxf(tmax, __shfl_xor(tmax, 32));
+    for (int x = 0; x < 16; x += 2) {
+      tmax = fmaxf(fmaxf(tmax, s0[x]), s0[x + 1]);
+      tmax = fmaxf(fmaxf(tmax, s1[x]), s1[x + 1]);
+    }
+    tmax = half_swap_max(tmax);
     const float mnew = fmaxf(m_used, tmax * c);
     if (__any(mnew > m_used + kLazy)) {
       const float alpha = mnew == m_used ? 1.f : __builtin_amdgcn_exp2f(m_used - mnew);
@@ -273,35 +255,39 @@ __global__ __launch_bounds__(256, 1) void link_mfma_d128_kernel(LinkParams p) {
     const float neg_m = m_used == -INFINITY ? 0.f : -m_used;
     bf16x8 pf[4];
 #pragma unroll
-    for (int b = 0; b < 2; ++b)
+    for (int x = 0; x < 8; ++x) {
+      pf[0][x] = (__bf16)__builtin_amdgcn_exp2f(__builtin_fmaf(s0[x], c, neg_m));
+      pf[1][x] = (__bf16)__builtin_amdgcn_exp2f(__builtin_fmaf(s0[8 + x], c, neg_m));
+      pf[2][x] = (__bf16)__builtin_amdgcn_exp2f(__builtin_fmaf(s1[x], c, neg_m));
+      pf[3][x] = (__bf16)__builtin_amdgcn_exp2f(__builtin_fmaf(s1[8 + x], c, neg_m));
+    }
+    // row sum of the rounded probabilities (the values the PV product uses)
 #pragma unroll
-      for (int h2 = 0; h2 < 2; ++h2)
+    for (int ks = 0; ks < 4; ++ks)
 #pragma unroll
-        for (int x = 0; x < 8; ++x) {
-          const float pv = __builtin_amdgcn_exp2f(__builtin_fmaf(s[b][h2 * 8 + x], c, neg_m));
-          lsum += pv;
-          pf[b * 2 + h2][x] = (__bf16)pv;
-        }
+      for (int x = 0; x < 8; x += 2) {
+        const bf16x2 pp = {pf[ks][x], pf[ks][x + 1]};
+        lsum = __builtin_amdgcn_fdot2_f32_bf16(pp, ones, lsum, false);
+      }
 
     // ---- O^T += V^T P^T : 4 value blocks x 4 key steps
+    const uint4 *vt = sm.vt[buf];
 #pragma unroll
     for (int ks = 0; ks < 4; ++ks) {
+      bf16x8 vf[4];
 #pragma unroll
-      for (int d = 0; d < 4; ++d) {
-        const bf16x8 vf = as_bf16x8(sm.vt[buf][v_slot(d * 32 + n, ks * 2 + g)]);
-        o[d] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf[ks], o[d], 0, 0, 0);
-      }
+      for (int d = 0; d < 4; ++d) vf[d] = as_bf16x8(vt[v_slot(d * 32 + n, ks * 2 + g)]);
+#pragma unroll
+      for (int d = 0; d < 4; ++d)
+        o[d] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[d], pf[ks], o[d], 0, 0, 0);
     }
 
-    if (more) {
-      store_tile(nxt, regs, sm, buf ^ 1);
-      cur = nxt;
-    }
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     __syncthreads();
   }
 
   // ---- epilogue: O^T[dv][row] with dv = d*32 + (x>>2)*8 + g*4 + (x&3)
-  const float ltot = lsum + __shfl_xor(lsum, 32);
+  const float ltot = half_swap_sum(lsum);
   if (!rvalid) return;
   const int total_rows = p.total_q * p.n_q_heads;
   if (p.num_splits == 1) {

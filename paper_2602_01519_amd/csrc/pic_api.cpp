@@ -157,13 +157,15 @@ bool check_offsets(const int32_t *a, int32_t n) {
 
 // Validated, resolved form of one link call.
 struct Plan {
-  std::vector<LinkEntry> links;
+  std::vector<LinkEntry> links;  // per request: its document links, then its own KV
   std::vector<ReqEntry> reqs;
   std::vector<int32_t> order;
+  std::vector<std::pair<int32_t, int64_t>> own;   // (link index, workspace byte offset)
+  int64_t own_bytes = 0;
+  int32_t max_own_lp = 0;
   int32_t total_q = 0;
   int32_t max_rows = 0;          // max over requests of lq * group
   int32_t max_tiles = 0;
-  int64_t work_pairs = 0;
 };
 
 pic_status plan_call(pic_store *s, const pic_link_req *req, int32_t n_q_heads, const void *q,
@@ -199,13 +201,15 @@ pic_status plan_call(pic_store *s, const pic_link_req *req, int32_t n_q_heads, c
     return fail(PIC_ERR_INVALID, "k_self/v_self given without self_offsets");
   }
   const int group = n_q_heads / d.n_kv_heads;
-  P.links.resize(n_links);
+  const int64_t slot_tok_bytes = (s->k_tok_elems + s->v_tok_elems) * s->esz;
+  P.links.clear();
+  P.links.reserve(n_links + B);
   P.reqs.resize(B);
   std::vector<int64_t> weight(B);
   for (int32_t r = 0; r < B; ++r) {
     ReqEntry &R = P.reqs[r];
-    R.link0 = req->chunk_offsets[r];
-    R.nlinks = req->chunk_offsets[r + 1] - R.link0;
+    const int32_t c0 = req->chunk_offsets[r], nc = req->chunk_offsets[r + 1] - c0;
+    R.link0 = (int32_t)P.links.size();
     R.q0 = req->q_offsets[r];
     R.lq = req->q_offsets[r + 1] - R.q0;
     R.s0 = self ? req->self_offsets[r] : 0;
@@ -217,30 +221,43 @@ pic_status plan_call(pic_store *s, const pic_link_req *req, int32_t n_q_heads, c
       return fail(PIC_ERR_INVALID, "request %d: %d query tokens exceeds %d", r, R.lq,
                   max_q_per_req);
     int64_t tiles = 0, toks = 0;
-    for (int32_t c = 0; c < R.nlinks; ++c) {
-      const uint64_t id = req->chunk_ids[R.link0 + c];
+    for (int32_t c = 0; c < nc; ++c) {
+      const uint64_t id = req->chunk_ids[c0 + c];
       auto it = s->map.find(id);
       if (it == s->map.end())
         return fail(PIC_ERR_NOT_FOUND, "request %d link %d: chunk id 0x%llx not in the store", r,
                     c, (unsigned long long)id);
       const Slot &sl = it->second;
-      LinkEntry &E = P.links[R.link0 + c];
-      E.k_off = sl.off_tokens * (s->k_tok_elems + s->v_tok_elems);
-      E.v_off = d.kind == PIC_GQA ? E.k_off + (int64_t)sl.lp * s->k_tok_elems : E.k_off;
+      LinkEntry E;
+      E.k = s->pool + sl.off_tokens * slot_tok_bytes;
+      E.v = d.kind == PIC_GQA ? (const char *)E.k + (int64_t)sl.lp * s->k_tok_elems * s->esz : E.k;
       E.len = (int32_t)sl.len;
       E.lp = sl.lp;
       E.tile0 = (int32_t)tiles;
       E.tok0 = (int32_t)toks;
+      P.links.push_back(E);
       tiles += sl.lp / kTile;
       toks += sl.len;
     }
     if (toks + R.ls > INT32_MAX / 2) return fail(PIC_ERR_INVALID, "request %d too long", r);
     R.doc_tiles = (int32_t)tiles;
-    R.tiles = (int32_t)(tiles + (R.ls + kTile - 1) / kTile);
+    if (R.ls > 0) {             // own KV: a slot in the call's workspace, filled on the device
+      LinkEntry E{};
+      E.len = R.ls;
+      E.lp = (int32_t)round_up(R.ls, kTile);
+      E.tile0 = (int32_t)tiles;
+      E.tok0 = (int32_t)toks;
+      P.own.emplace_back((int32_t)P.links.size(), P.own_bytes);
+      P.own_bytes += round_up((int64_t)E.lp * slot_tok_bytes, 256);
+      P.max_own_lp = std::max(P.max_own_lp, E.lp);
+      P.links.push_back(E);
+      tiles += E.lp / kTile;
+    }
+    R.nlinks = (int32_t)P.links.size() - R.link0;
+    R.tiles = (int32_t)tiles;
     P.max_rows = std::max(P.max_rows, R.lq * group);
     P.max_tiles = std::max(P.max_tiles, R.tiles);
     weight[r] = (int64_t)R.tiles * R.lq;
-    P.work_pairs += (int64_t)R.lq * (toks + R.ls);
   }
   P.order.resize(B);
   for (int32_t r = 0; r < B; ++r) P.order[r] = r;
@@ -309,7 +326,6 @@ pic_status link_call(pic_store *s, const pic_link_req *req, int32_t n_q_heads, c
   const hipStream_t st = (hipStream_t)stream;
 
   LinkParams lp{};
-  lp.pool = s->pool;
   lp.q = q;
   lp.k_self = k_self;
   lp.v_self = v_self;
@@ -346,12 +362,21 @@ pic_status link_call(pic_store *s, const pic_link_req *req, int32_t n_q_heads, c
     }
   }
   lp.num_splits = splits;
-  if (splits > 1) {
-    const size_t rows = (size_t)P.total_q * n_q_heads;
-    const size_t bytes = rows * splits * (d.d_v + 2) * sizeof(float) + 1024;
-    rc = ensure_work(s, bytes);
+  // Workspace: [own KV slots][split partials].
+  const size_t rows = (size_t)P.total_q * n_q_heads;
+  const size_t part_off = round_up(P.own_bytes, 256);
+  const size_t part_bytes = splits > 1 ? rows * splits * (d.d_v + 2) * sizeof(float) : 0;
+  if (part_off + part_bytes > 0) {
+    rc = ensure_work(s, part_off + part_bytes);
     if (rc != PIC_OK) return rc;
-    lp.part_o = (float *)s->work;
+  }
+  for (auto &o : P.own) {
+    LinkEntry &E = P.links[o.first];
+    E.k = (char *)s->work + o.second;
+    E.v = mla ? E.k : (const char *)E.k + (int64_t)E.lp * s->k_tok_elems * s->esz;
+  }
+  if (splits > 1) {
+    lp.part_o = (float *)((char *)s->work + part_off);
     lp.part_m = lp.part_o + rows * splits * d.d_v;
     lp.part_l = lp.part_m + rows * splits;
   }
@@ -362,6 +387,10 @@ pic_status link_call(pic_store *s, const pic_link_req *req, int32_t n_q_heads, c
   rc = upload(s, P, st, &stage, lp);
   if (rc != PIC_OK) return rc;
 
+  if (P.max_own_lp > 0) {
+    hipError_t e = launch_prep_own(lp, mla, s->esz, P.max_own_lp, st);
+    if (e != hipSuccess) return hip_fail(e, "prep_own kernels");
+  }
   std::pair<hipEvent_t, hipEvent_t> ev;
   const char *name = "";
   prof_start(st, &ev);
@@ -522,8 +551,8 @@ pic_status pic_debug_gather(pic_store *s, const uint64_t *ids, int32_t n, void *
                                         (unsigned long long)ids[i]);
     const Slot &sl = it->second;
     LinkEntry &E = links[i];
-    E.k_off = sl.off_tokens * s->k_tok_elems + sl.off_tokens * s->v_tok_elems;
-    E.v_off = E.k_off + (int64_t)sl.lp * s->k_tok_elems;
+    E.k = s->pool + sl.off_tokens * (s->k_tok_elems + s->v_tok_elems) * s->esz;
+    E.v = gqa ? (const char *)E.k + (int64_t)sl.lp * s->k_tok_elems * s->esz : E.k;
     E.len = (int32_t)sl.len;
     E.lp = sl.lp;
     E.tile0 = 0;
@@ -543,7 +572,7 @@ pic_status pic_debug_gather(pic_store *s, const uint64_t *ids, int32_t n, void *
   HIP_TRY(hipMemcpyAsync(stage->dev, stage->host, sizeof(LinkEntry) * n, hipMemcpyHostToDevice, st),
           "hipMemcpyAsync(gather table)");
   const pic_store_desc &d = s->desc;
-  hipError_t e = launch_gather(s->pool, (const LinkEntry *)stage->dev, n, toks, d.n_kv_heads,
+  hipError_t e = launch_gather((const LinkEntry *)stage->dev, n, toks, d.n_kv_heads,
                                d.d_k, d.d_v, !gqa, s->esz, k_out, v_out, st);
   if (e != hipSuccess) return hip_fail(e, "gather_kernel");
   HIP_TRY(hipEventRecord(stage->done, st), "hipEventRecord(stage)");

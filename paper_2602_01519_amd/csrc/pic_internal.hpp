@@ -13,19 +13,20 @@ namespace pic {
 // pool's rows stay 16-byte aligned.
 constexpr int kTile = 64;
 
-// Pool layout of one chunk slot with padded length lp (elements of the
-// store's dtype, offsets relative to the pool base):
-//   GQA  K block  [n_kv_heads][lp][d_k]    at k_off  (head-major, token rows)
-//        V block  [n_kv_heads][d_v][lp]    at v_off  (transposed: the value
-//                                          dim is the row, tokens contiguous)
-//   MLA  K block  [lp][d_k]                at k_off  (value = first d_v entries
-//        of each row; v_off == k_off)
+// Layout of one chunk slot with padded length lp (elements of the store's
+// dtype):
+//   GQA  K block  [n_kv_heads][lp][d_k]    (head-major, token rows)
+//        V block  [n_kv_heads][d_v][lp]    (transposed: the value dim is the
+//                                          row, tokens contiguous)
+//   MLA  K block  [lp][d_k]                (value = first d_v of each row)
 // The transposed V lets a matrix-core operand read 8 consecutive keys of one
-// value column with a single 16-byte load.
+// value column with a single 16-byte load. A request's own KV is laid out
+// the same way (in the call's workspace) before the attention kernel runs,
+// so every key tile of a request -- document or own -- is read alike.
 
 struct LinkEntry {        // one link of one request, in link order
-  int64_t k_off;
-  int64_t v_off;
+  const void *k;          // K block of the slot
+  const void *v;          // GQA: V block; MLA: same as k
   int32_t len;            // tokens
   int32_t lp;             // padded tokens (multiple of kTile)
   int32_t tile0;          // index of the link's first tile within the request
@@ -33,15 +34,14 @@ struct LinkEntry {        // one link of one request, in link order
 };
 
 struct ReqEntry {
-  int32_t link0, nlinks;  // links[link0 .. link0+nlinks)
+  int32_t link0, nlinks;  // links[link0 .. link0+nlinks); the own KV, if any, is the last
   int32_t q0, lq;         // query rows q0 .. q0+lq of q / out
   int32_t s0, ls;         // own rows s0 .. s0+ls of k_self / v_self (ls = 0: none)
-  int32_t doc_tiles;      // tiles over the linked documents
+  int32_t doc_tiles;      // tiles over the linked documents (own tiles follow)
   int32_t tiles;          // doc_tiles + ceil(ls / kTile)
 };
 
 struct LinkParams {
-  const void *pool;
   const LinkEntry *links;
   const ReqEntry *reqs;
   const int32_t *order;   // requests, heaviest first
@@ -71,9 +71,14 @@ hipError_t launch_put_rows(const void *src, void *dst, int64_t n_tokens, int32_t
                            int32_t heads, int32_t width, int32_t esz, hipStream_t st);
 hipError_t launch_put_transposed(const void *src, void *dst, int64_t n_tokens, int32_t lp,
                                  int32_t heads, int32_t width, int32_t esz, hipStream_t st);
-hipError_t launch_gather(const void *pool, const LinkEntry *links, int32_t n_links,
-                         int64_t total_tokens, int32_t heads, int32_t d_k, int32_t d_v,
-                         int32_t mla, int32_t esz, void *k_out, void *v_out, hipStream_t st);
+hipError_t launch_gather(const LinkEntry *links, int32_t n_links, int64_t total_tokens,
+                         int32_t heads, int32_t d_k, int32_t d_v, int32_t mla, int32_t esz,
+                         void *k_out, void *v_out, hipStream_t st);
+
+// Lays each request's own KV (token-major k_self / v_self) out like a chunk
+// slot at its own link (the request's last link), zero-padded to lp.
+hipError_t launch_prep_own(const LinkParams &p, int32_t mla, int32_t esz, int32_t max_own_lp,
+                           hipStream_t st);
 
 // Generic vector-ALU link attention: any d_k <= 576, d_v <= 512, fp32 or bf16.
 hipError_t launch_link_valu(const LinkParams &p, int dtype, int mla, hipStream_t st,

@@ -226,7 +226,7 @@ def test_chunk_order_permutation_on_gpu():
         torch.cuda.synchronize()
         b, lb = dw.results()
         assert np.abs(a - b).max() <= 2e-2 and np.abs(a - b).mean() <= 2e-3
-        assert np.abs(la - lb).max() <= 1e-3
+        assert np.abs(la - lb).max() <= 2e-3     # the log-sum-exp tolerance of the oracle checks
     finally:
         dw.close()
 
