@@ -11,40 +11,64 @@
 //   S^T[64 keys][32 rows] = K . Q^T        16 x v_mfma_f32_32x32x16_bf16
 //   online softmax on S^T (each lane holds one row's 32 scores)
 //   O^T[128][32 rows]    += V^T . P^T      16 x v_mfma_f32_32x32x16_bf16
-// K and V^T tiles are staged in LDS, double-buffered, with 16-byte chunks
-// XOR-swizzled so the fragment reads are bank-conflict free. The store keeps
-// V transposed per chunk, so a V^T tile is 128 rows of 128 contiguous bytes.
-// The M index of the QK^T product is permuted (key row pi(m) feeds M index m)
-// so that the scores a lane receives for a 16-key PV step are 8 consecutive
-// keys: P^T then feeds the PV product straight from registers, and the V^T
-// fragment for those keys is one 16-byte LDS read.
+// K and V^T tiles are copied global -> LDS by the load-to-LDS path
+// (global_load_lds_dwordx4, no register staging), double-buffered in four
+// distinct LDS arrays; the tile loop is unrolled by two so every access names
+// its buffer statically, which lets the compiler see that a tile's reads and
+// the next tile's copy never alias (no wait on the copy before the reads).
+// The store keeps V transposed per chunk, so a V^T tile is 128 rows of 128
+// contiguous bytes. The M index of the QK^T product is permuted (key row
+// pi(m) feeds M index m) so that the scores a lane receives for a 16-key PV
+// step are 8 consecutive keys: P^T feeds the PV product straight from
+// registers and the V^T fragment for those keys is one 16-byte LDS read.
 //
 // Softmax: log2 domain (scale * log2 e applied by FMA), row max through one
 // cross-half lane swap, and a lazy rescale: the running max used for the
-// exponentials is only moved when a row's max grows by more than 8 (p stays
-// <= 2^8), which skips the accumulator rescale on almost every tile. The row
-// sums are kept per lane half and added once at the end.
+// exponentials only moves when a row's max grows by more than 8 (p stays
+// <= 2^8), which skips the accumulator rescale on almost every tile. Row
+// sums are kept per lane half (bf16 dot products of the rounded
+// probabilities, i.e. the weights the PV product uses) and added at the end.
 #include "pic_internal.hpp"
 
 namespace pic {
 namespace {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef __attribute__((address_space(3))) void *lds_ptr;
 
 constexpr int kD = 128;
 constexpr int kWaves = 4;
 constexpr int kRowsPerWave = 32;
 constexpr int kRows = kWaves * kRowsPerWave;
 constexpr float kLazy = 8.0f;
+constexpr int kWin = 32;     // link-table entries staged in LDS
+#ifndef PIC_QK_AHEAD
+#define PIC_QK_AHEAD 5
+#endif
+#ifndef PIC_PV_AHEAD
+#define PIC_PV_AHEAD 8
+#endif
+constexpr int kQkAhead = PIC_QK_AHEAD;   // K-fragment read lead, in QK steps
+constexpr int kPvAhead = PIC_PV_AHEAD;   // V-fragment read lead, in PV MFMAs
 
-struct Smem {
-  uint4 k[2][kTile * 16];   // [buf][key][16 chunks of 8 d], chunk c at c ^ (key & 15)
-  uint4 vt[2][kD * 8];      // [buf][dv][8 chunks of 8 keys], chunk c at c ^ (dv & 7)
-};
-
-__device__ __forceinline__ int k_slot(int key, int c) { return key * 16 + (c ^ (key & 15)); }
-__device__ __forceinline__ int v_slot(int dv, int c) { return dv * 8 + (c ^ (dv & 7)); }
+// LDS tiles, 16-byte chunks XOR-swizzled within each row. The swizzles keep
+// every fragment read conflict-free whether a 16-byte-per-lane read is served
+// 8 or 16 lanes at a time: the 8 (16) lanes of a group read 8 (16) distinct
+// chunk positions of the bank row.
+//   K   [key][16 chunks of 8 d]:   chunk c at c ^ hk(key), hk swaps bits 2 and 3
+//       of key & 15 (a lane group reads keys {0-3, 8-11} or {4-7, 12-15}).
+//   V^T [dv][8 chunks of 8 keys]:  chunk c at c ^ hv(dv & 31) with
+//       hv(x) = (x ^ (x >> 3)) & 7 (two 128-byte rows share a 256-byte bank
+//       row; depending on dv & 31 only, the 4 value blocks of a lane share
+//       one address register).
+__device__ __forceinline__ int hk(int key) {
+  return (key & 3) | ((key & 8) >> 1) | ((key & 4) << 1);
+}
+__device__ __forceinline__ int hv(int x) { return (x ^ (x >> 3)) & 7; }
+__device__ __forceinline__ int k_slot(int key, int c) { return key * 16 + (c ^ hk(key & 15)); }
+__device__ __forceinline__ int v_slot(int dv, int c) { return dv * 8 + (c ^ hv(dv & 31)); }
 
 // Key row that feeds M index m of the QK^T product (see the file comment).
 __device__ __forceinline__ int key_of_m(int m) {
@@ -54,29 +78,15 @@ __device__ __forceinline__ int key_of_m(int m) {
 
 __device__ __forceinline__ bf16x8 as_bf16x8(uint4 u) { return __builtin_bit_cast(bf16x8, u); }
 
-typedef __attribute__((address_space(3))) void *lds_ptr;
-
-// Starts the copy of key tile tt of link E (kv head kvh) into LDS buffers
-// kdst / vdst with direct global->LDS loads: lane i of a load lands at slot
-// base + i, so each lane fetches the global chunk that belongs at that slot
-// of the swizzled layout. 4 K loads + 4 V loads per lane, 16 bytes each.
-__device__ __forceinline__ void issue_tile(const LinkEntry &E, int kvh, int tt, uint4 *kdst,
-                                           uint4 *vdst, int wave, int lane) {
-  const uint16_t *kb = (const uint16_t *)E.k + ((int64_t)kvh * E.lp + tt * kTile) * kD;
-  const uint16_t *vb = (const uint16_t *)E.v + (int64_t)kvh * kD * E.lp + tt * kTile;
-#pragma unroll
-  for (int u = 0; u < 4; ++u) {
-    const int base = (u * kWaves + wave) * 64;
-    const int s = base + lane;
-    const int key = s >> 4, kc = (s & 15) ^ (key & 15);
-    __builtin_amdgcn_global_load_lds(kb + key * kD + kc * 8, (lds_ptr)(kdst + base), 16, 0, 0);
-    const int dv = s >> 3, vc = (s & 7) ^ (dv & 7);
-    __builtin_amdgcn_global_load_lds(vb + (int64_t)dv * E.lp + vc * 8, (lds_ptr)(vdst + base), 16,
-                                     0, 0);
-  }
+__device__ __forceinline__ int uni(int x) { return __builtin_amdgcn_readfirstlane(x); }
+__device__ __forceinline__ const char *uni(const void *p) {
+  const uint64_t u = (uint64_t)p;
+  const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)u);
+  const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(u >> 32));
+  return (const char *)(((uint64_t)hi << 32) | lo);
 }
 
-// Sum / max of a value over lanes i and i ^ 32 (the two key halves of a row).
+// Max / sum of a value over lanes i and i ^ 32 (the two key halves of a row).
 __device__ __forceinline__ float half_swap_max(float x) {
   const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false,
                                                   false);
@@ -88,43 +98,188 @@ __device__ __forceinline__ float half_swap_sum(float x) {
   return __uint_as_float(r[0]) + __uint_as_float(r[1]);
 }
 
-// The request's link table is read through a window of kWin entries staged
-// in LDS, so walking tiles costs LDS reads instead of dependent global loads.
-constexpr int kWin = 32;
-
-struct LinkCursor {
-  int li = 0;       // current link (index within the request)
-  int wb = 0;       // first link held in the window
+// A key tile: workgroup-uniform facts.
+struct TileRef {
+  const char *k;     // first K row of the tile (kv head applied), bytes
+  const char *v;     // V^T row 0 at the tile's first key (kv head applied)
+  int lp;            // V^T row stride in elements
+  int nvalid;        // valid keys in the tile
+  int j0;            // key index of the tile's first key within its link
+  int own;           // the tile belongs to the request's own KV (causal mask)
 };
 
-__device__ __forceinline__ void load_window(const LinkParams &p, const ReqEntry &R, LinkEntry *win,
-                                            int wb) {
-  const int n = min(kWin, R.nlinks - wb);
-  for (int i = threadIdx.x; i < n; i += blockDim.x) win[i] = p.links[R.link0 + wb + i];
+struct Ctx {
+  const LinkParams *p;
+  ReqEntry R;
+  int kvh, wave, lane, n, g;
+  LinkEntry *win;    // link-table window in LDS
+  int li, wb;        // cursor: current link, first link held in the window
+  uint32_t koff[4];  // byte offsets of this lane's 4 K chunks within a tile
+  uint32_t vrow[4], vcol[4];   // row / byte column of its 4 V^T chunks
+};
+
+__device__ __forceinline__ void load_window(Ctx &c) {
+  const int n = min(kWin, c.R.nlinks - c.wb);
+  for (int i = threadIdx.x; i < n; i += blockDim.x) c.win[i] = c.p->links[c.R.link0 + c.wb + i];
 }
 
-// Moves the cursor to the link holding tile t (t only grows) and returns it.
-// Uniform across the workgroup: it may reload the window between barriers.
-__device__ __forceinline__ LinkEntry advance(const LinkParams &p, const ReqEntry &R,
-                                             LinkEntry *win, LinkCursor &cur, int t) {
+// Tile t of the request (t only grows across calls). Workgroup-uniform: it
+// may reload the link window between two barriers.
+__device__ __forceinline__ TileRef tile_ref(Ctx &c, int t) {
   for (;;) {
-    if (cur.li - cur.wb >= kWin) {
+    if (c.li - c.wb >= kWin) {
       __syncthreads();
-      cur.wb += kWin;
-      load_window(p, R, win, cur.wb);
+      c.wb += kWin;
+      load_window(c);
       __syncthreads();
     }
-    const LinkEntry e = win[cur.li - cur.wb];
-    if (t < e.tile0 + e.lp / kTile) return e;
-    ++cur.li;
+    const LinkEntry &e = c.win[c.li - c.wb];
+    const int tile0 = uni(e.tile0), lp = uni(e.lp);
+    if (t < tile0 + lp / kTile) {
+      const int tt = t - tile0;
+      TileRef r;
+      r.lp = lp;
+      r.nvalid = min(kTile, uni(e.len) - tt * kTile);
+      r.j0 = tt * kTile;
+      r.own = t >= c.R.doc_tiles;
+      r.k = uni(e.k) + ((int64_t)c.kvh * lp + tt * kTile) * kD * 2;
+      r.v = uni(e.v) + ((int64_t)c.kvh * kD * lp + tt * kTile) * 2;
+      return r;
+    }
+    ++c.li;
+  }
+}
+
+// Copies of a tile into LDS: lane i of a load-to-LDS lands at slot base + i,
+// so each lane fetches the global chunk that belongs at that slot of the
+// swizzled layout (uniform base address + per-lane 32-bit offset).
+__device__ __forceinline__ void issue_k(const Ctx &c, const TileRef &r, uint4 *kdst) {
+#pragma unroll
+  for (int u = 0; u < 4; ++u)
+    __builtin_amdgcn_global_load_lds(r.k + c.koff[u], (lds_ptr)(kdst + (u * kWaves + c.wave) * 64),
+                                     16, 0, 0);
+}
+__device__ __forceinline__ void issue_v(const Ctx &c, const TileRef &r, uint4 *vdst) {
+#pragma unroll
+  for (int u = 0; u < 4; ++u)
+    __builtin_amdgcn_global_load_lds(r.v + (c.vrow[u] * (uint32_t)r.lp * 2u + c.vcol[u]),
+                                     (lds_ptr)(vdst + (u * kWaves + c.wave) * 64), 16, 0, 0);
+}
+
+struct Acc {
+  f32x16 o[4];
+  float m_used, lsum;
+};
+
+// Masks keys past the tile's valid end and, in own tiles, keys after the
+// row's causal limit. s0[x] / s1[x] hold key (x>>3)*16 + g*8 + (x&7) (+32).
+__device__ __forceinline__ void mask_tile(const Ctx &c, f32x16 &s0, f32x16 &s1, int nvalid,
+                                          int j0, int own, int lim) {
+  if (own || nvalid < kTile) {
+    // visible iff key <= kl; compared as (key - g*8) against kl - g*8 so the
+    // left side is a compile-time constant per element
+    const int kl = (own ? min(lim - j0, nvalid - 1) : nvalid - 1) - c.g * 8;
+#pragma unroll
+    for (int x = 0; x < 16; ++x) {
+      const int key = (x >> 3) * 16 + (x & 7);
+      if (key > kl) s0[x] = -INFINITY;
+      if (key + 32 > kl) s1[x] = -INFINITY;
+    }
+  }
+}
+
+// One tile: S = K Q^T from kt, mask, online softmax (log2 domain, lazy
+// rescale), O += V^T P^T from vt. In both matrix sections the LDS fragment
+// reads are issued a few MFMAs ahead of their use (scheduling groups), so an
+// MFMA does not wait on the read issued right before it.
+__device__ __forceinline__ void compute_tile(const Ctx &c, const uint4 *kt, const uint4 *vt,
+                                             const bf16x8 (&qf)[8], Acc &a, int nvalid, int j0,
+                                             int own, int lim, float sc) {
+  const int krow0 = key_of_m(c.n);
+  f32x16 s0, s1;
+#pragma unroll
+  for (int x = 0; x < 16; ++x) {
+    s0[x] = 0.f;
+    s1[x] = 0.f;
+  }
+#pragma unroll
+  for (int st = 0; st < 8; ++st) {
+    const bf16x8 ka = as_bf16x8(kt[k_slot(krow0, st * 2 + c.g)]);
+    const bf16x8 kb = as_bf16x8(kt[k_slot(32 + krow0, st * 2 + c.g)]);
+    s0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka, qf[st], s0, 0, 0, 0);
+    s1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kb, qf[st], s1, 0, 0, 0);
+  }
+  // K reads run kQkAhead steps (2 reads per step) ahead of the MFMAs
+  __builtin_amdgcn_sched_group_barrier(0x100, 2 * kQkAhead, 0);
+#pragma unroll
+  for (int st = 0; st < 8; ++st) {
+    __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
+    if (st + kQkAhead < 8) __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+  }
+  mask_tile(c, s0, s1, nvalid, j0, own, lim);
+
+  float tmax = -INFINITY;
+#pragma unroll
+  for (int x = 0; x < 16; x += 2) {
+    tmax = fmaxf(fmaxf(tmax, s0[x]), s0[x + 1]);
+    tmax = fmaxf(fmaxf(tmax, s1[x]), s1[x + 1]);
+  }
+  tmax = half_swap_max(tmax);
+  const float mnew = fmaxf(a.m_used, tmax * sc);
+  if (__any(mnew > a.m_used + kLazy)) {
+    const float alpha = mnew == a.m_used ? 1.f : __builtin_amdgcn_exp2f(a.m_used - mnew);
+    a.m_used = mnew;
+    a.lsum *= alpha;
+#pragma unroll
+    for (int d = 0; d < 4; ++d)
+#pragma unroll
+      for (int x = 0; x < 16; ++x) a.o[d][x] *= alpha;
+  }
+  const float neg_m = a.m_used == -INFINITY ? 0.f : -a.m_used;
+  bf16x8 pf[4];
+#pragma unroll
+  for (int x = 0; x < 8; ++x) {
+    pf[0][x] = (__bf16)__builtin_amdgcn_exp2f(__builtin_fmaf(s0[x], sc, neg_m));
+    pf[1][x] = (__bf16)__builtin_amdgcn_exp2f(__builtin_fmaf(s0[8 + x], sc, neg_m));
+    pf[2][x] = (__bf16)__builtin_amdgcn_exp2f(__builtin_fmaf(s1[x], sc, neg_m));
+    pf[3][x] = (__bf16)__builtin_amdgcn_exp2f(__builtin_fmaf(s1[8 + x], sc, neg_m));
+  }
+  const bf16x2 ones = {(__bf16)1.0f, (__bf16)1.0f};
+#pragma unroll
+  for (int ks = 0; ks < 4; ++ks)
+#pragma unroll
+    for (int x = 0; x < 8; x += 2) {
+      const bf16x2 pp = {pf[ks][x], pf[ks][x + 1]};
+      a.lsum = __builtin_amdgcn_fdot2_f32_bf16(pp, ones, a.lsum, false);
+    }
+
+#pragma unroll
+  for (int ks = 0; ks < 4; ++ks)
+#pragma unroll
+    for (int d = 0; d < 4; ++d) {
+      const bf16x8 vf = as_bf16x8(vt[v_slot(d * 32 + c.n, ks * 2 + c.g)]);
+      a.o[d] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf[ks], a.o[d], 0, 0, 0);
+    }
+  // V reads run kPvAhead MFMAs ahead
+  __builtin_amdgcn_sched_group_barrier(0x100, kPvAhead, 0);
+#pragma unroll
+  for (int i = 0; i < 16; ++i) {
+    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+    if (i + kPvAhead < 16) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
   }
 }
 
 __global__ __launch_bounds__(256, 2) void link_mfma_d128_kernel(LinkParams p) {
-  __shared__ Smem sm;
-  const int lane = threadIdx.x & 63;
-  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  const int n = lane & 31, g = lane >> 5;
+  __shared__ uint4 sk0[kTile * 16], sk1[kTile * 16];
+  __shared__ uint4 sv0[kD * 8], sv1[kD * 8];
+  __shared__ LinkEntry win[kWin];
+
+  Ctx c;
+  c.p = &p;
+  c.lane = threadIdx.x & 63;
+  c.wave = uni(threadIdx.x >> 6);
+  c.n = c.lane & 31;
+  c.g = c.lane >> 5;
 
   // XCD-aware work mapping: consecutive blocks go round-robin to the 8 XCDs;
   // all row blocks of one (request, kv head) land on the same XCD (same L2)
@@ -136,8 +291,9 @@ __global__ __launch_bounds__(256, 2) void link_mfma_d128_kernel(LinkParams p) {
   const int split = blockIdx.y;
   if (grp >= p.batch * p.n_kv_heads) return;
   const int req_i = p.order[grp / p.n_kv_heads];
-  const int kvh = grp % p.n_kv_heads;
-  const ReqEntry R = p.reqs[req_i];
+  c.kvh = grp % p.n_kv_heads;
+  c.R = p.reqs[req_i];
+  const ReqEntry &R = c.R;
   const int group = p.group;
   const int nrows = R.lq * group;
   const int row0 = rb * kRows;
@@ -146,25 +302,36 @@ __global__ __launch_bounds__(256, 2) void link_mfma_d128_kernel(LinkParams p) {
   const int t_end = (int)((int64_t)R.tiles * (split + 1) / p.num_splits);
 
   // This lane's row.
-  const int row = row0 + wave * kRowsPerWave + n;
+  const int row = row0 + c.wave * kRowsPerWave + c.n;
   const bool rvalid = row < nrows;
   const int qi = rvalid ? row / group : 0;
-  const int qh = kvh * group + (rvalid ? row % group : 0);
+  const int qh = c.kvh * group + (rvalid ? row % group : 0);
   const int lim = rvalid ? qi + R.ls - R.lq : -1;     // last visible own key
   const int64_t orow = (int64_t)(R.q0 + qi) * p.n_q_heads + qh;
 
-  __shared__ LinkEntry win[kWin];
-  LinkCursor cur;
-  load_window(p, R, win, 0);
+  // Per-lane load-to-LDS offsets (see issue_k / issue_v).
+#pragma unroll
+  for (int u = 0; u < 4; ++u) {
+    const int s = (u * kWaves + c.wave) * 64 + c.lane;
+    const int key = s >> 4, kc = (s & 15) ^ hk(key & 15);
+    c.koff[u] = (uint32_t)((key * kD + kc * 8) * 2);
+    const int dv = s >> 3;
+    c.vrow[u] = (uint32_t)dv;
+    c.vcol[u] = (uint32_t)(((s & 7) ^ hv(dv & 31)) * 16);
+  }
+
+  c.win = win;
+  c.li = 0;
+  c.wb = 0;
+  load_window(c);
   __syncthreads();
-  // masking facts of the tile being computed: valid keys, own-KV key offset
-  int nvalid_cur = kTile, j0_cur = 0;
+
+  // masking facts of the tile held in each buffer pair
+  TileRef ref0{}, ref1{};
   if (t_begin < t_end) {
-    const LinkEntry E = advance(p, R, win, cur, t_begin);
-    const int tt = t_begin - E.tile0;
-    issue_tile(E, kvh, tt, sm.k[0], sm.vt[0], wave, lane);
-    nvalid_cur = min(kTile, E.len - tt * kTile);
-    j0_cur = tt * kTile;
+    ref0 = tile_ref(c, t_begin);
+    issue_k(c, ref0, sk0);
+    issue_v(c, ref0, sv0);
   }
 
   // Q fragments: d = step*16 + g*8 + (0..7)
@@ -174,120 +341,48 @@ __global__ __launch_bounds__(256, 2) void link_mfma_d128_kernel(LinkParams p) {
 #pragma unroll
     for (int s = 0; s < 8; ++s) {
       uint4 v = make_uint4(0, 0, 0, 0);
-      if (rvalid) v = qrow[s * 2 + g];
+      if (rvalid) v = qrow[s * 2 + c.g];
       qf[s] = as_bf16x8(v);
     }
   }
 
-  f32x16 o[4];
+  Acc a;
 #pragma unroll
   for (int d = 0; d < 4; ++d)
 #pragma unroll
-    for (int x = 0; x < 16; ++x) o[d][x] = 0.f;
-  float m_used = -INFINITY, lsum = 0.f;
-  const float c = p.scale_log2;
-  const int krow0 = key_of_m(n);      // key row feeding this lane's M index, block 0
-  typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
-  const bf16x2 ones = {(__bf16)1.0f, (__bf16)1.0f};
+    for (int x = 0; x < 16; ++x) a.o[d][x] = 0.f;
+  a.m_used = -INFINITY;
+  a.lsum = 0.f;
+  const float sc = p.scale_log2;
 
   asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
   __syncthreads();
 
-  for (int t = t_begin; t < t_end; ++t) {
-    const int buf = (t - t_begin) & 1;
-    const int nvalid = nvalid_cur, j0 = j0_cur;
-    const bool own = t >= R.doc_tiles;
+  // Unrolled by two so every access names its buffers statically.
+  for (int t = t_begin; t < t_end; t += 2) {
+    // tile t in buffers 0; copy tile t+1 into buffers 1
     if (t + 1 < t_end) {
-      const LinkEntry E = advance(p, R, win, cur, t + 1);
-      const int tt = t + 1 - E.tile0;
-      issue_tile(E, kvh, tt, sm.k[buf ^ 1], sm.vt[buf ^ 1], wave, lane);
-      nvalid_cur = min(kTile, E.len - tt * kTile);
-      j0_cur = tt * kTile;
+      ref1 = tile_ref(c, t + 1);
+      issue_k(c, ref1, sk1);
+      issue_v(c, ref1, sv1);
     }
-
-    // ---- S^T = K Q^T : two 32-key blocks
-    const uint4 *kt = sm.k[buf];
-    bf16x8 ka[8], kb[8];
-#pragma unroll
-    for (int st = 0; st < 8; ++st) {
-      ka[st] = as_bf16x8(kt[k_slot(krow0, st * 2 + g)]);
-      kb[st] = as_bf16x8(kt[k_slot(32 + krow0, st * 2 + g)]);
+    compute_tile(c, sk0, sv0, qf, a, ref0.nvalid, ref0.j0, ref0.own, lim, sc);
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    __syncthreads();
+    if (t + 1 >= t_end) break;
+    // tile t+1 in buffers 1; copy tile t+2 into buffers 0
+    if (t + 2 < t_end) {
+      ref0 = tile_ref(c, t + 2);
+      issue_k(c, ref0, sk0);
+      issue_v(c, ref0, sv0);
     }
-    f32x16 s0, s1;
-#pragma unroll
-    for (int x = 0; x < 16; ++x) { s0[x] = 0.f; s1[x] = 0.f; }
-#pragma unroll
-    for (int st = 0; st < 8; ++st) {
-      s0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka[st], qf[st], s0, 0, 0, 0);
-      s1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kb[st], qf[st], s1, 0, 0, 0);
-    }
-
-    // ---- masking (only on ragged or own tiles)
-    // s_b[x] is the score of key b*32 + (x>>3)*16 + g*8 + (x&7) for this row
-    if (own || nvalid < kTile) {
-      const int kl = own ? lim - j0 : kTile;     // visible iff key <= kl
-#pragma unroll
-      for (int x = 0; x < 16; ++x) {
-        const int key = (x >> 3) * 16 + g * 8 + (x & 7);
-        if (key >= nvalid || key > kl) s0[x] = -INFINITY;
-        if (key + 32 >= nvalid || key + 32 > kl) s1[x] = -INFINITY;
-      }
-    }
-
-    // ---- online softmax (log2 domain, lazy rescale)
-    float tmax = -INFINITY;
-#pragma unroll
-    for (int x = 0; x < 16; x += 2) {
-      tmax = fmaxf(fmaxf(tmax, s0[x]), s0[x + 1]);
-      tmax = fmaxf(fmaxf(tmax, s1[x]), s1[x + 1]);
-    }
-    tmax = half_swap_max(tmax);
-    const float mnew = fmaxf(m_used, tmax * c);
-    if (__any(mnew > m_used + kLazy)) {
-      const float alpha = mnew == m_used ? 1.f : __builtin_amdgcn_exp2f(m_used - mnew);
-      m_used = mnew;
-      lsum *= alpha;
-#pragma unroll
-      for (int d = 0; d < 4; ++d)
-#pragma unroll
-        for (int x = 0; x < 16; ++x) o[d][x] *= alpha;
-    }
-    const float neg_m = m_used == -INFINITY ? 0.f : -m_used;
-    bf16x8 pf[4];
-#pragma unroll
-    for (int x = 0; x < 8; ++x) {
-      pf[0][x] = (__bf16)__builtin_amdgcn_exp2f(__builtin_fmaf(s0[x], c, neg_m));
-      pf[1][x] = (__bf16)__builtin_amdgcn_exp2f(__builtin_fmaf(s0[8 + x], c, neg_m));
-      pf[2][x] = (__bf16)__builtin_amdgcn_exp2f(__builtin_fmaf(s1[x], c, neg_m));
-      pf[3][x] = (__bf16)__builtin_amdgcn_exp2f(__builtin_fmaf(s1[8 + x], c, neg_m));
-    }
-    // row sum of the rounded probabilities (the values the PV product uses)
-#pragma unroll
-    for (int ks = 0; ks < 4; ++ks)
-#pragma unroll
-      for (int x = 0; x < 8; x += 2) {
-        const bf16x2 pp = {pf[ks][x], pf[ks][x + 1]};
-        lsum = __builtin_amdgcn_fdot2_f32_bf16(pp, ones, lsum, false);
-      }
-
-    // ---- O^T += V^T P^T : 4 value blocks x 4 key steps
-    const uint4 *vt = sm.vt[buf];
-#pragma unroll
-    for (int ks = 0; ks < 4; ++ks) {
-      bf16x8 vf[4];
-#pragma unroll
-      for (int d = 0; d < 4; ++d) vf[d] = as_bf16x8(vt[v_slot(d * 32 + n, ks * 2 + g)]);
-#pragma unroll
-      for (int d = 0; d < 4; ++d)
-        o[d] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[d], pf[ks], o[d], 0, 0, 0);
-    }
-
+    compute_tile(c, sk1, sv1, qf, a, ref1.nvalid, ref1.j0, ref1.own, lim, sc);
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     __syncthreads();
   }
 
   // ---- epilogue: O^T[dv][row] with dv = d*32 + (x>>2)*8 + g*4 + (x&3)
-  const float ltot = half_swap_sum(lsum);
+  const float ltot = half_swap_sum(a.lsum);
   if (!rvalid) return;
   const int total_rows = p.total_q * p.n_q_heads;
   if (p.num_splits == 1) {
@@ -297,14 +392,14 @@ __global__ __launch_bounds__(256, 2) void link_mfma_d128_kernel(LinkParams p) {
     for (int d = 0; d < 4; ++d)
 #pragma unroll
       for (int jj = 0; jj < 4; ++jj) {
-        const int dv = d * 32 + jj * 8 + g * 4;
+        const int dv = d * 32 + jj * 8 + c.g * 4;
         __bf16 v4[4];
 #pragma unroll
-        for (int x = 0; x < 4; ++x) v4[x] = (__bf16)(o[d][jj * 4 + x] * inv);
+        for (int x = 0; x < 4; ++x) v4[x] = (__bf16)(a.o[d][jj * 4 + x] * inv);
         *(uint2 *)(out + dv) = __builtin_bit_cast(uint2, v4);
       }
-    if (p.lse && g == 0)
-      p.lse[orow] = ltot > 0.f ? (m_used + log2f(ltot)) * 0.69314718055994531f : -INFINITY;
+    if (p.lse && c.g == 0)
+      p.lse[orow] = ltot > 0.f ? (a.m_used + log2f(ltot)) * 0.69314718055994531f : -INFINITY;
   } else {
     const int64_t prow = (int64_t)split * total_rows + orow;
     float *po = p.part_o + prow * kD;
@@ -312,12 +407,12 @@ __global__ __launch_bounds__(256, 2) void link_mfma_d128_kernel(LinkParams p) {
     for (int d = 0; d < 4; ++d)
 #pragma unroll
       for (int jj = 0; jj < 4; ++jj) {
-        const int dv = d * 32 + jj * 8 + g * 4;
-        *(float4 *)(po + dv) =
-            make_float4(o[d][jj * 4], o[d][jj * 4 + 1], o[d][jj * 4 + 2], o[d][jj * 4 + 3]);
+        const int dv = d * 32 + jj * 8 + c.g * 4;
+        *(float4 *)(po + dv) = make_float4(a.o[d][jj * 4], a.o[d][jj * 4 + 1],
+                                           a.o[d][jj * 4 + 2], a.o[d][jj * 4 + 3]);
       }
-    if (g == 0) {
-      p.part_m[prow] = ltot > 0.f ? m_used : -INFINITY;
+    if (c.g == 0) {
+      p.part_m[prow] = ltot > 0.f ? a.m_used : -INFINITY;
       p.part_l[prow] = ltot;
     }
   }
