@@ -20,6 +20,7 @@ SOURCES = [
     "pic_api.cpp",
     "kernels_generic.hip",
     "kernels_mfma_d128.hip",
+    "kernels_decode_d128.hip",
 ]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")

@@ -341,21 +341,31 @@ pic_status link_call(pic_store *s, const pic_link_req *req, int32_t n_q_heads, c
   lp.scale_log2 = scale * 1.4426950408889634f;
 
   // Kernel choice.
-  const bool mfma128 = d.dtype == PIC_BF16 && !mla && d.d_k == 128 && d.d_v == 128 &&
-                       mode == Mode::Prefill;
-  int rows_per_block = mfma128 ? mfma_d128_rows_per_block() : valu_rows_per_block();
-  if (!mfma128 && valu_lds_bytes_for(s->esz, mla, d.d_k, d.d_v) > 160 * 1024)
+  //   bf16 GQA d=128: decode-shaped calls with at most 16 rows per (request,
+  //   kv head) stream keys with the decode kernel; everything else runs the
+  //   matrix-core flash kernel (split when decoding).
+  //   Other shapes / fp32 / MLA: the generic vector-ALU kernel.
+  enum class K { Valu, Mfma128, Decode128 } kern = K::Valu;
+  const bool bf16_128 = d.dtype == PIC_BF16 && !mla && d.d_k == 128 && d.d_v == 128;
+  if (bf16_128)
+    kern = mode == Mode::Decode && P.max_rows <= decode_d128_max_rows() ? K::Decode128 : K::Mfma128;
+  if (kern == K::Valu && valu_lds_bytes_for(s->esz, mla, d.d_k, d.d_v) > 160 * 1024)
     return fail(PIC_ERR_UNSUPPORTED, "head widths d_k=%d d_v=%d exceed the generic kernel's LDS",
                 d.d_k, d.d_v);
+  const int rows_per_block = kern == K::Mfma128 ? mfma_d128_rows_per_block()
+                             : kern == K::Valu  ? valu_rows_per_block()
+                                                : decode_d128_max_rows();
   lp.nrb = std::max(1, (P.max_rows + rows_per_block - 1) / rows_per_block);
   lp.n_groups = req->batch * d.n_kv_heads;
-  if (mfma128) lp.n_groups = (int32_t)round_up(lp.n_groups, 8);
+  if (kern == K::Mfma128) lp.n_groups = (int32_t)round_up(lp.n_groups, 8);
 
   int32_t splits = 1;
   if (mode == Mode::Decode) {
     if (num_splits > 0) {
       splits = num_splits;
     } else {
+      // about 2048 work items (one wave each for the decode kernel, a
+      // workgroup each otherwise), never more splits than tiles
       const int64_t blocks = (int64_t)req->batch * d.n_kv_heads * lp.nrb;
       splits = (int32_t)std::max<int64_t>(1, std::min<int64_t>((2048 + blocks - 1) / blocks, 256));
       splits = std::min(splits, std::max(1, P.max_tiles));
@@ -395,7 +405,9 @@ pic_status link_call(pic_store *s, const pic_link_req *req, int32_t n_q_heads, c
   const char *name = "";
   prof_start(st, &ev);
   hipError_t e;
-  if (mfma128)
+  if (kern == K::Decode128)
+    e = launch_link_decode_d128(lp, st, &name);
+  else if (kern == K::Mfma128)
     e = launch_link_mfma_d128(lp, st, &name);
   else
     e = launch_link_valu(lp, d.dtype, mla, st, &name);

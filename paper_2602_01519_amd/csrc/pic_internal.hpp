@@ -89,6 +89,11 @@ int valu_rows_per_block();
 hipError_t launch_link_mfma_d128(const LinkParams &p, hipStream_t st, const char **name);
 int mfma_d128_rows_per_block();
 
+// bf16 GQA decode-shaped link attention, d_k = d_v = 128, at most
+// decode_d128_max_rows() rows per (request, kv head); one wave per split.
+hipError_t launch_link_decode_d128(const LinkParams &p, hipStream_t st, const char **name);
+int decode_d128_max_rows();
+
 // Log-sum-exp merge of split partials into out / lse.
 hipError_t launch_combine(const LinkParams &p, int dtype, hipStream_t st);
 

@@ -161,6 +161,16 @@ def test_decode_splits(splits):
     run_and_check(DECODE, decode=True, num_splits=splits)
 
 
+@pytest.mark.parametrize("q_len,splits", [((4, 1, 2), 3), ((4, 1, 2), 1), ((5, 2, 16), 4)])
+def test_decode_multi_token_bf16(q_len, splits):
+    """Up to 16 rows per (request, kv head) use the streaming decode kernel;
+    more rows fall back to the split matrix-core kernel."""
+    cfg = W.small_config("decode_multi", d_k=128, n_q_heads=8, n_kv_heads=2,
+                         chunk_lens=(300, 64, 9, 1024), batch=3, links=(1, 3), q_len=q_len,
+                         self_len=(40, 3, 70), decode=True)
+    run_and_check(cfg, decode=True, num_splits=splits)
+
+
 def test_decode_f32_and_multi_token():
     cfg = W.small_config("decode_f32", dtype=W.F32, d_k=64, chunk_lens=(200, 64, 9), batch=3,
                          links=(1, 3), q_len=(1, 4, 16), self_len=(5, 4, 40), decode=True)
