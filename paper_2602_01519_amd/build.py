@@ -21,6 +21,7 @@ SOURCES = [
     "kernels_generic.hip",
     "kernels_mfma_d128.hip",
     "kernels_decode_d128.hip",
+    "kernels_mla.hip",
 ]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")

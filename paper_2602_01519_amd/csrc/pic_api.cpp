@@ -345,16 +345,20 @@ pic_status link_call(pic_store *s, const pic_link_req *req, int32_t n_q_heads, c
   //   kv head) stream keys with the decode kernel; everything else runs the
   //   matrix-core flash kernel (split when decoding).
   //   Other shapes / fp32 / MLA: the generic vector-ALU kernel.
-  enum class K { Valu, Mfma128, Decode128 } kern = K::Valu;
+  //   bf16 MLA with 576-wide latent rows and 512-wide values: the MLA
+  //   matrix-core kernel (split when decoding).
+  enum class K { Valu, Mfma128, Decode128, Mla } kern = K::Valu;
   const bool bf16_128 = d.dtype == PIC_BF16 && !mla && d.d_k == 128 && d.d_v == 128;
   if (bf16_128)
     kern = mode == Mode::Decode && P.max_rows <= decode_d128_max_rows() ? K::Decode128 : K::Mfma128;
+  if (d.dtype == PIC_BF16 && mla && d.d_k == 576 && d.d_v == 512) kern = K::Mla;
   if (kern == K::Valu && valu_lds_bytes_for(s->esz, mla, d.d_k, d.d_v) > 160 * 1024)
     return fail(PIC_ERR_UNSUPPORTED, "head widths d_k=%d d_v=%d exceed the generic kernel's LDS",
                 d.d_k, d.d_v);
-  const int rows_per_block = kern == K::Mfma128 ? mfma_d128_rows_per_block()
-                             : kern == K::Valu  ? valu_rows_per_block()
-                                                : decode_d128_max_rows();
+  const int rows_per_block = kern == K::Mfma128   ? mfma_d128_rows_per_block()
+                             : kern == K::Valu    ? valu_rows_per_block()
+                             : kern == K::Mla     ? mla_rows_per_block()
+                                                  : decode_d128_max_rows();
   lp.nrb = std::max(1, (P.max_rows + rows_per_block - 1) / rows_per_block);
   lp.n_groups = req->batch * d.n_kv_heads;
   if (kern == K::Mfma128) lp.n_groups = (int32_t)round_up(lp.n_groups, 8);
@@ -407,6 +411,8 @@ pic_status link_call(pic_store *s, const pic_link_req *req, int32_t n_q_heads, c
   hipError_t e;
   if (kern == K::Decode128)
     e = launch_link_decode_d128(lp, st, &name);
+  else if (kern == K::Mla)
+    e = launch_link_mla(lp, st, &name);
   else if (kern == K::Mfma128)
     e = launch_link_mfma_d128(lp, st, &name);
   else

@@ -94,6 +94,11 @@ int mfma_d128_rows_per_block();
 hipError_t launch_link_decode_d128(const LinkParams &p, hipStream_t st, const char **name);
 int decode_d128_max_rows();
 
+// bf16 MLA (absorbed) link attention: one 576-wide latent kv head, values
+// are the first 512 entries of each latent row.
+hipError_t launch_link_mla(const LinkParams &p, hipStream_t st, const char **name);
+int mla_rows_per_block();
+
 // Log-sum-exp merge of split partials into out / lse.
 hipError_t launch_combine(const LinkParams &p, int dtype, hipStream_t st);
 

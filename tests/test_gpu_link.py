@@ -137,9 +137,18 @@ SMALL = {
     "valu_f32_dv32": W.small_config("valu_f32_dv32", dtype=W.F32, d_k=64, d_v=32,
                                     chunk_lens=(9, 64, 77), batch=2, links=(1, 3), q_len=(3, 12),
                                     self_len=(3, 20)),
-    "valu_mla": W.small_config("valu_mla", kind=W.MLA, n_q_heads=16, d_k=576, d_v=512,
+    "valu_mla": W.small_config("valu_mla", kind=W.MLA, n_q_heads=16, d_k=192, d_v=128,
                                chunk_lens=(70, 64, 1, 130), batch=2, links=(1, 3), q_len=(9, 4),
                                self_len=(9, 6), q_std=1.0, scale=1 / math.sqrt(192)),
+    # MLA matrix-core kernel: 576-wide latent rows, ragged chunks, several 64-row blocks
+    "mla_mfma": W.small_config("mla_mfma", kind=W.MLA, n_q_heads=16, d_k=576, d_v=512,
+                               chunk_lens=(70, 64, 1, 130, 200), batch=3, links=(0, 4),
+                               q_len=(9, 4, 13), self_len=(9, 70, 13), q_std=1.0,
+                               scale=1 / math.sqrt(192)),
+    "mla_mfma_cross": W.small_config("mla_mfma_cross", kind=W.MLA, n_q_heads=16, d_k=576,
+                                     d_v=512, chunk_lens=(64, 129), batch=2, links=(1, 2),
+                                     q_len=(5, 2), self_len=None, q_std=1.0,
+                                     scale=1 / math.sqrt(192)),
     "valu_mla_f32": W.small_config("valu_mla_f32", dtype=W.F32, kind=W.MLA, n_q_heads=4, d_k=64,
                                    d_v=32, chunk_lens=(70, 1, 65), batch=2, links=(1, 3),
                                    q_len=(9, 4), self_len=(9, 6)),
@@ -169,6 +178,13 @@ def test_decode_multi_token_bf16(q_len, splits):
                          chunk_lens=(300, 64, 9, 1024), batch=3, links=(1, 3), q_len=q_len,
                          self_len=(40, 3, 70), decode=True)
     run_and_check(cfg, decode=True, num_splits=splits)
+
+
+def test_mla_decode_splits():
+    cfg = W.small_config("mla_decode", kind=W.MLA, n_q_heads=16, d_k=576, d_v=512,
+                         chunk_lens=(512, 300, 64), batch=3, links=(1, 3), q_len=1,
+                         self_len=(5, 1, 64), q_std=1.0, scale=1 / math.sqrt(192), decode=True)
+    run_and_check(cfg, decode=True, num_splits=3)
 
 
 def test_decode_f32_and_multi_token():
