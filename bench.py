@@ -32,6 +32,86 @@ PEAK_BF16_TFLOPS = 2500.0     # MI355X dense bf16 matrix peak
 PEAK_HBM_GBS = 8000.0         # MI355X HBM3E
 PEAK_FP32_VALU_TFLOPS = 157.3
 
+# Source file of each attention kernel: a traffic record measured with
+# rocprofv3 counters is used only while the kernel source is unchanged.
+KERNEL_SOURCES = {
+    "link_mfma_d128_kernel": "kernels_mfma_d128.hip",
+    "link_decode_d128_kernel": "kernels_decode_d128.hip",
+    "link_mla_kernel": "kernels_mla.hip",
+    "link_valu_kernel": "kernels_generic.hip",
+}
+PROFILES = os.path.join(ROOT, "profiles")
+
+
+def kernel_source_sha(kernel: str):
+    import hashlib
+    for k, f in KERNEL_SOURCES.items():
+        if kernel.startswith(k):
+            path = os.path.join(ROOT, "paper_2602_01519_amd", "csrc", f)
+            return hashlib.sha256(open(path, "rb").read()).hexdigest()[:16]
+    return None
+
+
+def traffic_record(kernel: str, workload: str):
+    """HBM bytes per launch from a committed counter record, if still valid."""
+    base = kernel.split("<")[0]
+    path = os.path.join(PROFILES, f"traffic_{base}_{workload}.json")
+    if not os.path.exists(path):
+        return None
+    rec = json.load(open(path))
+    if rec.get("kernel_source_sha") != kernel_source_sha(kernel):
+        return None
+    return rec.get("hbm_bytes_per_launch")
+
+
+def _pmc_per_dispatch(csv_path: str, kernel_prefix: str, counter: str):
+    import csv
+    vals = [float(r["Counter_Value"]) for r in csv.DictReader(open(csv_path))
+            if r["Counter_Name"] == counter and kernel_prefix in r["Kernel_Name"]]
+    if not vals:
+        raise SystemExit(f"no {counter} samples for {kernel_prefix} in {csv_path}")
+    return sum(vals) / len(vals)
+
+
+def summarize_traffic(args):
+    """Writes profiles/traffic_<kernel>_<workload>.json from four rocprofv3 --pmc
+    CSVs: FETCH_SIZE and WRITE_SIZE (KiB per dispatch) of the kernel, and of a
+    plain device copy of known size, whose ratio calibrates the counters."""
+    fetch_csv, write_csv, copy_fetch_csv, copy_write_csv = args.summarize_traffic
+    copy_bytes = args.copy_mib * (1 << 20)
+    cf = _pmc_per_dispatch(copy_fetch_csv, "copyBuffer", "FETCH_SIZE") * 1024.0
+    cw = _pmc_per_dispatch(copy_write_csv, "copyBuffer", "WRITE_SIZE") * 1024.0
+    kf = _pmc_per_dispatch(fetch_csv, args.kernel, "FETCH_SIZE") * 1024.0
+    kw = _pmc_per_dispatch(write_csv, args.kernel, "WRITE_SIZE") * 1024.0
+    f_scale, w_scale = copy_bytes / cf, copy_bytes / cw
+    rec = {
+        "kernel": args.kernel,
+        "workload": args.config,
+        "kernel_source_sha": kernel_source_sha(args.kernel),
+        "fetch_bytes_raw": kf, "write_bytes_raw": kw,
+        "copy_bytes": copy_bytes, "copy_fetch_raw": cf, "copy_write_raw": cw,
+        "fetch_scale": f_scale, "write_scale": w_scale,
+        "hbm_bytes_per_launch": kf * f_scale + kw * w_scale,
+    }
+    os.makedirs(PROFILES, exist_ok=True)
+    out = os.path.join(PROFILES, f"traffic_{args.kernel}_{args.config}.json")
+    json.dump(rec, open(out, "w"), indent=1)
+    print(json.dumps(rec))
+    return 0
+
+
+def copy_calibration(args):
+    """A plain device-to-device copy of --copy-mib MiB, for counter calibration."""
+    import torch
+    n = args.copy_mib * (1 << 20)
+    src = torch.empty(n, dtype=torch.uint8, device="cuda").random_(0, 255)
+    dst = torch.empty_like(src)
+    for _ in range(args.warmup + args.steps):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_bytes": n, "copies": args.warmup + args.steps}))
+    return 0
+
 
 def algorithmic(cfg, wl):
     from paper_2602_01519_amd import workloads as W
@@ -104,7 +184,14 @@ def main(argv=None):
                     help="workload: tiny_f32, llama_prefill, long_rag, decode, mla")
     ap.add_argument("--cpu-budget", type=float, default=15.0,
                     help="seconds of oracle time for the CPU baseline (0 = skip)")
+    ap.add_argument("--copy-mib", type=int, default=0,
+                    help="run a plain device copy of this many MiB instead (counter calibration)")
+    ap.add_argument("--summarize-traffic", nargs=4, metavar="CSV",
+                    help="kernel FETCH_SIZE csv, kernel WRITE_SIZE csv, copy FETCH csv, copy WRITE csv")
+    ap.add_argument("--kernel", default="link_mfma_d128_kernel")
     args = ap.parse_args(argv)
+    if args.summarize_traffic:
+        return summarize_traffic(args)
     if args.gpus != 1:
         print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported "
               f"(the link path shards by request with no exchange, see the design notes)",
@@ -119,6 +206,8 @@ def main(argv=None):
         print("bench.py needs a GPU", file=sys.stderr)
         return 2
     torch.cuda.set_device(0)
+    if args.copy_mib:
+        return copy_calibration(args)
     cfg = W.CONFIGS[args.config]
     wl = W.make_workload(cfg)
     keep = set(int(c) for c in wl.plan.chunk_index[wl.plan.chunk_offsets[0]:wl.plan.chunk_offsets[min(4, wl.plan.batch)]])
@@ -197,7 +286,7 @@ def main(argv=None):
             "peak": peak,
             "unit": unit,
             "frac": round(achieved / peak, 4),
-            "traffic": None,
+            "traffic": traffic_record(kname, cfg.name),
             "kernel_avg_us": round(kern_avg_ms * 1e3, 3),
             "launches": launches,
         },

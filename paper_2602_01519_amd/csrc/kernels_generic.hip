@@ -120,58 +120,86 @@ __global__ void gather_kernel(const LinkEntry *__restrict__ links, int32_t n_lin
 
 // ---------------------------------------------------------------------------
 // Own KV of a request laid out like a chunk slot (at its last link): K rows
-// head-major, V transposed, zero padding up to lp. One launch per call,
-// blockIdx.z = request.
+// head-major, V transposed, zero padding up to lp. One launch per call:
+// blockIdx.z = request; the first rows_blocks blocks copy K rows, the others
+// transpose 64x64 tiles of V.
 
-__global__ void prep_own_rows_kernel(const ReqEntry *__restrict__ reqs,
-                                     const LinkEntry *__restrict__ links,
-                                     const uint4 *__restrict__ src, int32_t heads, int32_t vpr) {
-  const ReqEntry R = reqs[blockIdx.z];
-  if (R.ls == 0) return;
-  const LinkEntry E = links[R.link0 + R.nlinks - 1];
-  uint4 *dst = (uint4 *)E.k;
-  const int64_t total = (int64_t)heads * E.lp * vpr;
-  for (int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; idx < total;
-       idx += (int64_t)gridDim.x * blockDim.x) {
-    const int64_t h = idx / ((int64_t)E.lp * vpr);
-    const int64_t rem = idx - h * E.lp * vpr;
-    const int64_t t = rem / vpr;
-    const int64_t c = rem - t * vpr;
+struct PrepParams {
+  const ReqEntry *reqs;
+  const LinkEntry *links;
+  const void *k_self, *v_self;
+  int32_t heads, d_k, d_v, mla, esz;
+  int32_t rows_blocks;        // blocks per request doing K rows
+};
+
+// One 64-token x 64-value tile of own V, transposed into the slot's V block.
+// 16-byte global loads of 8 values of one token, an LDS tile with padded rows,
+// then 16-byte global stores of 8 tokens of one value dim.
+template <typename E>
+__device__ __forceinline__ void prep_transposed_tile(const ReqEntry &R, const LinkEntry &L,
+                                                     const E *__restrict__ src, int heads,
+                                                     int width, int tile) {
+  constexpr int EPV = 16 / sizeof(E);          // elements per 16 bytes
+  constexpr int ROW = 64 + EPV;                // padded LDS row (elements)
+  __shared__ __attribute__((aligned(16))) E tile_s[64 * ROW];
+  const int eblocks = (width + 63) / 64;
+  const int per_h = (L.lp / 64) * eblocks;
+  const int h = tile / per_h, rem = tile - h * per_h;
+  const int64_t t0 = (int64_t)(rem / eblocks) * 64;
+  const int e0 = (rem % eblocks) * 64;
+  E *dst = (E *)L.v;
+  for (int i = threadIdx.x; i < 64 * (64 / EPV); i += blockDim.x) {
+    const int tl = i / (64 / EPV), ec = i % (64 / EPV);
+    const int64_t t = t0 + tl;
+    const int e = e0 + ec * EPV;
     uint4 v = make_uint4(0, 0, 0, 0);
-    if (t < R.ls) v = src[((R.s0 + t) * heads + h) * vpr + c];
-    dst[idx] = v;
+    if (t < R.ls && e < width) v = *(const uint4 *)(src + ((R.s0 + t) * heads + h) * width + e);
+    *(uint4 *)(tile_s + tl * ROW + ec * EPV) = v;
+  }
+  __syncthreads();
+  for (int i = threadIdx.x; i < 64 * (64 / EPV); i += blockDim.x) {
+    const int el = i / (64 / EPV), tc = i % (64 / EPV);
+    const int e = e0 + el;
+    if (e >= width) continue;
+    union {
+      uint4 u;
+      E e[EPV];
+    } vals;
+#pragma unroll
+    for (int x = 0; x < EPV; ++x) vals.e[x] = tile_s[(tc * EPV + x) * ROW + el];
+    *(uint4 *)(dst + ((int64_t)h * width + e) * L.lp + t0 + tc * EPV) = vals.u;
   }
 }
 
-template <typename E>
-__global__ void prep_own_transposed_kernel(const ReqEntry *__restrict__ reqs,
-                                           const LinkEntry *__restrict__ links,
-                                           const E *__restrict__ src, int32_t heads,
-                                           int32_t width) {
-  __shared__ E tile[64][65];
-  const ReqEntry R = reqs[blockIdx.z];
+__global__ void prep_own_kernel(PrepParams pp) {
+  const ReqEntry R = pp.reqs[blockIdx.z];
   if (R.ls == 0) return;
-  const LinkEntry L = links[R.link0 + R.nlinks - 1];
-  const int64_t t0 = (int64_t)blockIdx.x * 64;
-  if (t0 >= L.lp) return;
-  const int eblocks = (width + 63) / 64;
-  const int h = blockIdx.y / eblocks;
-  const int e0 = (blockIdx.y % eblocks) * 64;
-  E *dst = (E *)L.v;
-  for (int i = threadIdx.x; i < 64 * 64; i += blockDim.x) {
-    const int tl = i >> 6, el = i & 63;
-    const int64_t t = t0 + tl;
-    const int e = e0 + el;
-    E v = E(0);
-    if (t < R.ls && e < width) v = src[((R.s0 + t) * heads + h) * width + e];
-    tile[tl][el] = v;
+  const LinkEntry L = pp.links[R.link0 + R.nlinks - 1];
+  if ((int)blockIdx.x < pp.rows_blocks) {
+    const int vpr = pp.d_k * pp.esz / 16;
+    const uint4 *src = (const uint4 *)pp.k_self;
+    uint4 *dst = (uint4 *)L.k;
+    const int64_t total = (int64_t)pp.heads * L.lp * vpr;
+    for (int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; idx < total;
+         idx += (int64_t)pp.rows_blocks * blockDim.x) {
+      const int64_t h = idx / ((int64_t)L.lp * vpr);
+      const int64_t rem = idx - h * L.lp * vpr;
+      const int64_t t = rem / vpr;
+      const int64_t c = rem - t * vpr;
+      uint4 v = make_uint4(0, 0, 0, 0);
+      if (t < R.ls) v = src[((R.s0 + t) * pp.heads + h) * vpr + c];
+      dst[idx] = v;
+    }
+    return;
   }
-  __syncthreads();
-  for (int i = threadIdx.x; i < 64 * 64; i += blockDim.x) {
-    const int el = i >> 6, tl = i & 63;
-    const int e = e0 + el;
-    if (e < width) dst[((int64_t)h * width + e) * L.lp + t0 + tl] = tile[tl][el];
-  }
+  if (pp.mla) return;
+  const int tile = blockIdx.x - pp.rows_blocks;
+  const int tiles = pp.heads * (L.lp / 64) * ((pp.d_v + 63) / 64);
+  if (tile >= tiles) return;
+  if (pp.esz == 2)
+    prep_transposed_tile<uint16_t>(R, L, (const uint16_t *)pp.v_self, pp.heads, pp.d_v, tile);
+  else
+    prep_transposed_tile<uint32_t>(R, L, (const uint32_t *)pp.v_self, pp.heads, pp.d_v, tile);
 }
 
 // ---------------------------------------------------------------------------
@@ -496,21 +524,22 @@ hipError_t launch_gather(const LinkEntry *links, int32_t n_links, int64_t total_
 
 hipError_t launch_prep_own(const LinkParams &p, int32_t mla, int32_t esz, int32_t max_own_lp,
                            hipStream_t st) {
-  if (max_own_lp == 0 || p.batch == 0) return hipSuccess;
-  const int32_t vpr = p.d_k * esz / 16;
-  const int64_t per_req = (int64_t)p.n_kv_heads * max_own_lp * vpr;
-  const unsigned bx = (unsigned)std::min<int64_t>((per_req + 255) / 256, 4096);
-  hipLaunchKernelGGL(prep_own_rows_kernel, dim3(bx, 1, p.batch), dim3(256), 0, st, p.reqs, p.links,
-                     (const uint4 *)p.k_self, p.n_kv_heads, vpr);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess || mla) return e;
-  dim3 grid(max_own_lp / 64, p.n_kv_heads * ((p.d_v + 63) / 64), p.batch);
-  if (esz == 2)
-    hipLaunchKernelGGL(prep_own_transposed_kernel<uint16_t>, grid, dim3(256), 0, st, p.reqs, p.links,
-                       (const uint16_t *)p.v_self, p.n_kv_heads, p.d_v);
-  else
-    hipLaunchKernelGGL(prep_own_transposed_kernel<uint32_t>, grid, dim3(256), 0, st, p.reqs, p.links,
-                       (const uint32_t *)p.v_self, p.n_kv_heads, p.d_v);
+  if (p.batch == 0) return hipSuccess;
+  PrepParams pp;
+  pp.reqs = p.reqs;
+  pp.links = p.links;
+  pp.k_self = p.k_self;
+  pp.v_self = p.v_self;
+  pp.heads = p.n_kv_heads;
+  pp.d_k = p.d_k;
+  pp.d_v = p.d_v;
+  pp.mla = mla;
+  pp.esz = esz;
+  const int64_t rows_vec = (int64_t)p.n_kv_heads * max_own_lp * (p.d_k * esz / 16);
+  pp.rows_blocks = (int32_t)std::max<int64_t>(1, std::min<int64_t>((rows_vec + 1023) / 1024, 256));
+  const int64_t tblocks = mla ? 0 : (int64_t)p.n_kv_heads * (max_own_lp / 64) * ((p.d_v + 63) / 64);
+  dim3 grid((unsigned)(pp.rows_blocks + tblocks), 1, p.batch);
+  hipLaunchKernelGGL(prep_own_kernel, grid, dim3(256), 0, st, pp);
   return hipGetLastError();
 }
 

@@ -73,6 +73,7 @@ struct Slot {
 // slot is reused only after its event has completed.
 struct Stage {
   void *host = nullptr;
+  void *host_dev = nullptr;     // device-visible address of host
   void *dev = nullptr;
   size_t cap = 0;
   hipEvent_t done = nullptr;
@@ -127,6 +128,7 @@ pic_status stage_acquire(pic_store *s, size_t bytes, Stage **out) {
     st.cap = 0;
     size_t cap = std::max<size_t>(round_up((int64_t)bytes, 4096), 64 * 1024);
     HIP_TRY(hipHostMalloc(&st.host, cap, hipHostMallocDefault), "hipHostMalloc(stage)");
+    HIP_TRY(hipHostGetDevicePointer(&st.host_dev, st.host, 0), "hipHostGetDevicePointer(stage)");
     HIP_TRY(hipMalloc(&st.dev, cap), "hipMalloc(stage)");
     st.cap = cap;
   }
@@ -267,19 +269,28 @@ pic_status plan_call(pic_store *s, const pic_link_req *req, int32_t n_q_heads, c
   return PIC_OK;
 }
 
-// Copies the plan's tables into a staging slot and to the device.
-pic_status upload(pic_store *s, const Plan &P, hipStream_t st, Stage **stage, LinkParams &lp) {
+// Writes the plan's tables into a staging slot; with copy, also enqueues
+// their copy to the device.
+struct TableLayout {
+  size_t off_r, off_o, bytes;
+};
+
+pic_status upload(pic_store *s, const Plan &P, hipStream_t st, bool copy, Stage **stage,
+                  LinkParams &lp, TableLayout &tl) {
   const size_t nl = P.links.size(), nr = P.reqs.size();
-  const size_t off_r = round_up(sizeof(LinkEntry) * nl, 256);
-  const size_t off_o = off_r + round_up(sizeof(ReqEntry) * nr, 256);
-  const size_t bytes = off_o + round_up(sizeof(int32_t) * nr, 256);
+  tl.off_r = round_up(sizeof(LinkEntry) * nl, 256);
+  tl.off_o = tl.off_r + round_up(sizeof(ReqEntry) * nr, 256);
+  tl.bytes = tl.off_o + round_up(sizeof(int32_t) * nr, 256);
+  const size_t off_r = tl.off_r, off_o = tl.off_o, bytes = tl.bytes;
   pic_status rc = stage_acquire(s, bytes, stage);
   if (rc != PIC_OK) return rc;
   char *h = (char *)(*stage)->host;
   if (nl) memcpy(h, P.links.data(), sizeof(LinkEntry) * nl);
   memcpy(h + off_r, P.reqs.data(), sizeof(ReqEntry) * nr);
   memcpy(h + off_o, P.order.data(), sizeof(int32_t) * nr);
-  HIP_TRY(hipMemcpyAsync((*stage)->dev, h, bytes, hipMemcpyHostToDevice, st), "hipMemcpyAsync(table)");
+  if (copy)
+    HIP_TRY(hipMemcpyAsync((*stage)->dev, h, bytes, hipMemcpyHostToDevice, st),
+            "hipMemcpyAsync(table)");
   char *dv = (char *)(*stage)->dev;
   lp.links = (const LinkEntry *)dv;
   lp.reqs = (const ReqEntry *)(dv + off_r);
@@ -376,15 +387,19 @@ pic_status link_call(pic_store *s, const pic_link_req *req, int32_t n_q_heads, c
     }
   }
   lp.num_splits = splits;
+  // Own KV: the matrix-core prefill kernel reads it in place; the other
+  // kernels read it laid out like a chunk slot in the workspace.
+  const bool own_inline = false;
   // Workspace: [own KV slots][split partials].
   const size_t rows = (size_t)P.total_q * n_q_heads;
-  const size_t part_off = round_up(P.own_bytes, 256);
+  const size_t part_off = own_inline ? 0 : round_up(P.own_bytes, 256);
   const size_t part_bytes = splits > 1 ? rows * splits * (d.d_v + 2) * sizeof(float) : 0;
   if (part_off + part_bytes > 0) {
     rc = ensure_work(s, part_off + part_bytes);
     if (rc != PIC_OK) return rc;
   }
   for (auto &o : P.own) {
+    if (own_inline) break;
     LinkEntry &E = P.links[o.first];
     E.k = (char *)s->work + o.second;
     E.v = mla ? E.k : (const char *)E.k + (int64_t)E.lp * s->k_tok_elems * s->esz;
@@ -398,10 +413,11 @@ pic_status link_call(pic_store *s, const pic_link_req *req, int32_t n_q_heads, c
   DeviceGuard dg(s->device);
   if (!dg.ok) return fail(PIC_ERR_HIP, "cannot select the store's device");
   Stage *stage = nullptr;
-  rc = upload(s, P, st, &stage, lp);
+  TableLayout tl;
+  rc = upload(s, P, st, true, &stage, lp, tl);
   if (rc != PIC_OK) return rc;
 
-  if (P.max_own_lp > 0) {
+  if (P.max_own_lp > 0 && !own_inline) {
     hipError_t e = launch_prep_own(lp, mla, s->esz, P.max_own_lp, st);
     if (e != hipSuccess) return hip_fail(e, "prep_own kernels");
   }
