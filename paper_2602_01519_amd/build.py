@@ -24,6 +24,15 @@ SOURCES = [
     "kernels_mla.hip",
 ]
 
+# Per-file code generation flags. The MLA kernel keeps its accumulators in
+# vector registers and its 576-wide query fragments in the accumulation
+# registers (matrix-core operands may sit in either); the backend's default
+# (accumulators in accumulation registers) leaves no room for the query and
+# moves the output accumulators in and out on every tile.
+FILE_FLAGS = {
+    "kernels_mla.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"],
+}
+
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 COMMON = ["--offload-arch=gfx950", "-O3", "-fPIC", "-std=c++17", "-Wall",
           "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
@@ -34,7 +43,7 @@ def _compile(src: str) -> str:
     path = os.path.join(CSRC, src)
     obj = os.path.join(BUILD, os.path.splitext(src)[0] + ".o")
     lang = ["-x", "hip"] if src.endswith(".hip") else []
-    cmd = [HIPCC] + COMMON + lang + ["-c", path, "-o", obj]
+    cmd = [HIPCC] + COMMON + FILE_FLAGS.get(src, []) + lang + ["-c", path, "-o", obj]
     res = subprocess.run(cmd, capture_output=True, text=True)
     # the host pass does not know the packed-fp32 feature and says so; harmless
     noise = "'-packed-fp32-ops' is not a recognized feature"

@@ -9,18 +9,26 @@
 // head)), 64-key tiles of the latent rows staged in LDS (72 KB per tile,
 // double-buffered with load-to-LDS copies). Per tile:
 //   1. wave (rb, kb) computes S^T[32 keys kb][32 rows rb] = K Q^T over the 576
-//      latent dims (36 x v_mfma_f32_32x32x16_bf16, Q held in registers);
-//   2. the four waves exchange per-row tile maxima through LDS, update the
-//      shared running max (lazy rescale, identical in every wave), turn their
-//      scores into bf16 probabilities and publish them in LDS;
+//      latent dims (36 x v_mfma_f32_32x32x16_bf16, Q held in registers) and
+//      turns it into bf16 probabilities against the running max it already
+//      holds, publishing them and its per-row tile maxima in LDS;
+//   2. one barrier; every wave reads both halves' maxima and makes the same
+//      decision: normally the stale max stays in use and the accumulators are
+//      rescaled after the value product if the max grew by more than 2^8; a
+//      tile that raises some row's max by more than 2^64 (the first tile of
+//      every row, for one) is redone against the new max behind one more
+//      barrier, so probabilities never exceed 2^64;
 //   3. wave w owns value dims [128 w, 128 w + 128) of all 64 rows and adds
 //      O^T += V^T P^T (32 MFMAs): V^T fragments are read straight out of the
 //      key tile with transposing LDS reads (ds_read_b64_tr_b16), so the
-//      latent rows are stored once, row-major, and serve as K and as V.
-// K tile layout: row r (1152 bytes = 72 chunks of 16 B) keeps chunk c at
-// c ^ f(r), f(r) = ((r >> 1) & 1) << 2 | ((r >> 2) & 3), which makes both the
-// 16-byte QK fragment reads and the 8-byte transposing PV reads bank-conflict
-// free (64 banks).
+//      latent rows are stored once and serve as keys and as values;
+//   4. one barrier ends the tile (buffer and probability reuse).
+// Tile layout (16-byte chunks): latent part [64 rows][64 chunks], chunk c of
+// row r at r*64 + (c ^ f(r)), f(r) = (r & 3) << 2 | (r >> 2) & 3; rope part
+// [64 rows][8 chunks] after it, chunk c of row r at r*8 + (c ^ ((r >> 1) & 7)).
+// Both the 16-byte score-operand reads and the 8-byte transposing reads are
+// free of bank conflicts (64 banks), and a wave's tile copy needs only two
+// lane offsets.
 #include "pic_internal.hpp"
 
 namespace pic {
@@ -35,17 +43,20 @@ typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
 
 constexpr int kDK = 576;                 // key / query width
 constexpr int kDV = 512;                 // value width (latent part)
-constexpr int kChunks = kDK * 2 / 16;    // 72 chunks of 16 B per key row
-constexpr int kSteps = kDK / 16;         // 36 QK steps of 16 dims
+constexpr int kRowBytes = kDK * 2;       // 1152 bytes per latent row
+constexpr int kLatChunks = 64;           // 16-byte chunks of the latent part
+constexpr int kRopeChunks = 8;           // ... of the rope part
+constexpr int kSteps = kDK / 16;         // 36 score steps of 16 dims
+constexpr int kLatSteps = 32;            // of which over the latent part
 constexpr int kRowsMla = 64;             // rows per workgroup
-constexpr float kLazy = 8.0f;
-constexpr int kWin = 32;                 // link-table entries staged in LDS
-constexpr int kTileChunks = kTile * kChunks;   // 4608 chunks per key tile
-constexpr int kDmaPerLane = kTileChunks / 256; // 18 load-to-LDS per lane per tile
-constexpr int kAhead = 6;                // K fragment read lead in the QK loop
+constexpr int kRopeBase = kTile * kLatChunks;                   // 4096 chunks
+constexpr int kTileChunks = kTile * (kLatChunks + kRopeChunks); // 4608 chunks
+constexpr float kJump = 64.0f;           // redo a tile whose max jumps by 2^64
+constexpr int kAhead = 6;                // K fragment read lead in the score loop
+constexpr int kVLead = 3;                // value fragment read lead in the value loop
 
-__device__ __forceinline__ int swz(int r) { return (((r >> 1) & 1) << 2) | ((r >> 2) & 3); }
-__device__ __forceinline__ int kpos(int r, int c) { return r * kChunks + (c ^ swz(r)); }
+__device__ __forceinline__ int swz(int r) { return ((r & 3) << 2) | ((r >> 2) & 3); }
+__device__ __forceinline__ int swr(int r) { return (r >> 1) & 7; }
 
 __device__ __forceinline__ int key_of_m(int m) {
   const int a = m >> 3, gg = (m >> 2) & 1, c = m & 3;
@@ -53,12 +64,6 @@ __device__ __forceinline__ int key_of_m(int m) {
 }
 __device__ __forceinline__ bf16x8 as_bf16x8(uint4 u) { return __builtin_bit_cast(bf16x8, u); }
 __device__ __forceinline__ int uni(int x) { return __builtin_amdgcn_readfirstlane(x); }
-__device__ __forceinline__ const char *uni(const void *p) {
-  const uint64_t u = (uint64_t)p;
-  const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)u);
-  const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(u >> 32));
-  return (const char *)(((uint64_t)hi << 32) | lo);
-}
 __device__ __forceinline__ float half_swap_max(float x) {
   const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false,
                                                   false);
@@ -70,11 +75,17 @@ __device__ __forceinline__ float half_swap_sum(float x) {
   return __uint_as_float(r[0]) + __uint_as_float(r[1]);
 }
 
+// The two 72 KB key tiles are separate __shared__ arrays: with one array the
+// compiler cannot tell a tile's reads from the copy into the other tile and
+// waits for that copy before every read.
+__device__ __forceinline__ uint32_t lds_addr(const void *p) {
+  return (uint32_t)(uintptr_t)(lds_ptr)p;
+}
+
 struct MlaSmem {
-  uint4 k[2][kTileChunks];                 // two 72 KB key tiles
   uint4 p[2][2][2][64];                    // probabilities [rb][kb][h][lane]
-  float xm[4][32];                         // per-wave row maxima / row sums
-  LinkEntry win[kWin];
+  float xm[4][32];                         // per-wave row maxima of the tile / row sums
+  int4 jump;                               // per wave: some row's max jumped past kJump
 };
 
 struct TileRef {
@@ -82,66 +93,93 @@ struct TileRef {
   int nvalid, j0, own;
 };
 
+// Walks a request's links in order. The tables are read through the
+// constant address space, so every lookup is a scalar load and the cursor
+// lives in scalar registers (no LDS, no barrier).
+typedef __attribute__((address_space(4))) const LinkEntry *const_links;
+typedef __attribute__((address_space(4))) const ReqEntry *const_reqs;
+typedef __attribute__((address_space(4))) const int32_t *const_ints;
+
 struct Cursor {
-  const LinkParams *p;
-  ReqEntry R;
-  LinkEntry *win;
-  int li, wb;
+  const_links links;     // this request's links
+  int li;                // current link
+  const char *k;         // its first latent row
+  int len, tile0, end;   // its tokens, first tile and the tile after its last
 };
 
-__device__ __forceinline__ void load_window(Cursor &c) {
-  const int n = min(kWin, c.R.nlinks - c.wb);
-  for (int i = threadIdx.x; i < n; i += blockDim.x) c.win[i] = c.p->links[c.R.link0 + c.wb + i];
+__device__ __forceinline__ void cursor_load(Cursor &c) {
+  c.k = (const char *)c.links[c.li].k;
+  c.len = c.links[c.li].len;
+  c.tile0 = c.links[c.li].tile0;
+  c.end = c.tile0 + c.links[c.li].lp / kTile;
 }
 
-__device__ __forceinline__ TileRef tile_ref(Cursor &c, int t) {
-  for (;;) {
-    if (c.li - c.wb >= kWin) {
-      __syncthreads();
-      c.wb += kWin;
-      load_window(c);
-      __syncthreads();
-    }
-    const LinkEntry &e = c.win[c.li - c.wb];
-    const int tile0 = uni(e.tile0), lp = uni(e.lp);
-    if (t < tile0 + lp / kTile) {
-      const int tt = t - tile0;
-      TileRef r;
-      r.nvalid = min(kTile, uni(e.len) - tt * kTile);
-      r.j0 = tt * kTile;
-      r.own = t >= c.R.doc_tiles;
-      r.k = uni(e.k) + (int64_t)tt * kTile * kDK * 2;
-      return r;
-    }
+// Tile t of the request (tiles are visited in increasing order).
+__device__ __forceinline__ TileRef tile_ref(Cursor &c, int t, int doc_tiles) {
+  while (t >= c.end) {
     ++c.li;
+    cursor_load(c);
+  }
+  const int tt = t - c.tile0;
+  TileRef r;
+  r.nvalid = min(kTile, c.len - tt * kTile);
+  r.j0 = tt * kTile;
+  r.own = t >= doc_tiles;
+  r.k = c.k + (int64_t)tt * kTile * kRowBytes;
+  return r;
+}
+
+// Copy i (0..17) of one 64-key tile into an LDS buffer, 16 bytes per lane.
+// Latent part, i < 16: wave w fills row r = 4i + w (64 lanes x 16 B),
+// position j holding chunk j ^ f(r) = j ^ (w << 2) ^ (i & 3), so
+// lat_off = 16 (lane ^ (w << 2)). Rope part, i = 16 + u: slot s = 256 u + tid
+// holds chunk (s & 7) ^ ((s >> 4) & 7) of row s >> 3; rope_off is that offset
+// for u = 0 (u = 1 adds 32 rows). The tile base is uniform, so each copy is
+// a scalar base plus one 32-bit lane offset; dst is the LDS byte address of
+// the buffer.
+__device__ __forceinline__ void tile_copy(int i, const char *k, uint32_t dst, int wave,
+                                          uint32_t lat_off, uint32_t rope_off) {
+  if (i < kTile / 4) {
+    const int r = 4 * i + wave;
+    __builtin_amdgcn_global_load_lds(k + r * kRowBytes + (lat_off ^ (16u * (i & 3))),
+                                     (lds_ptr)(uintptr_t)(dst + r * kLatChunks * 16), 16, 0, 0);
+  } else {
+    const int u = i - kTile / 4;
+    __builtin_amdgcn_global_load_lds(k + u * 32 * kRowBytes + rope_off,
+                                     (lds_ptr)(uintptr_t)(dst + (kRopeBase + u * 256 + wave * 64) * 16),
+                                     16, 0, 0);
   }
 }
-
-// Copy of one 64-key tile (64 rows x 1152 B) into an LDS buffer: load u of a
-// lane fills slot (u * 256 + tid), which holds chunk (slot % 72) ^ f(row).
-__device__ __forceinline__ void issue_tile(const TileRef &r, const uint32_t (&goff)[kDmaPerLane],
-                                           uint4 *dst, int wave) {
-#pragma unroll
-  for (int u = 0; u < kDmaPerLane; ++u)
-    __builtin_amdgcn_global_load_lds(r.k + goff[u], (lds_ptr)(dst + u * 256 + wave * 64), 16, 0,
-                                     0);
-}
+constexpr int kCopies = kTile / 4 + 2;   // 18 copies per lane per tile
 
 __global__ __launch_bounds__(256, 1) void link_mla_kernel(LinkParams p) {
   __shared__ MlaSmem sm;
+  __shared__ uint4 sk0[kTileChunks], sk1[kTileChunks];
   const int lane = threadIdx.x & 63;
   const int wave = uni(threadIdx.x >> 6);
   const int n = lane & 31, g = lane >> 5;
   const int rb_s = wave >> 1, kb_s = wave & 1;      // this wave's score tile
 
+  // Blocks are dealt to the 8 XCDs round-robin; give each XCD a contiguous
+  // run of row blocks so the row blocks of one request share an L2.
+  int b = blockIdx.x;
+  if ((gridDim.x & 7) == 0) b = (b & 7) * (gridDim.x >> 3) + (b >> 3);
   const int nrb = p.nrb;
-  const int grp = blockIdx.x / nrb, rblk = blockIdx.x % nrb;
+  const int grp = b / nrb, rblk = b % nrb;
   const int split = blockIdx.y;
   if (grp >= p.batch) return;
-  Cursor cur;
-  cur.p = &p;
-  cur.R = p.reqs[p.order[grp]];
-  const ReqEntry &R = cur.R;
+  ReqEntry R;
+  {
+    const int ri = ((const_ints)p.order)[grp];
+    const_reqs rq = (const_reqs)p.reqs + ri;
+    R.link0 = rq->link0;
+    R.nlinks = rq->nlinks;
+    R.q0 = rq->q0;
+    R.lq = rq->lq;
+    R.ls = rq->ls;
+    R.doc_tiles = rq->doc_tiles;
+    R.tiles = rq->tiles;
+  }
   const int group = p.group;           // query heads (one latent kv head)
   const int nrows = R.lq * group;
   const int row0 = rblk * kRowsMla;
@@ -163,28 +201,30 @@ __global__ __launch_bounds__(256, 1) void link_mla_kernel(LinkParams p) {
     orow[rb] = (int64_t)(R.q0 + qi) * p.n_q_heads + qh;
   }
 
-  // Per-lane byte offsets of the tile copy.
-  uint32_t goff[kDmaPerLane];
-#pragma unroll
-  for (int u = 0; u < kDmaPerLane; ++u) {
-    const int s = u * 256 + wave * 64 + lane;
-    const int r = s / kChunks, q = s - r * kChunks;
-    goff[u] = (uint32_t)(r * kDK * 2 + (q ^ swz(r)) * 16);
-  }
+  const uint32_t lat_off = 16u * (uint32_t)(lane ^ (wave << 2));
+  const int tid = threadIdx.x;
+  const uint32_t rope_off = (uint32_t)((tid >> 3) * kRowBytes + kLatChunks * 16 +
+                                       16 * ((tid & 7) ^ ((tid >> 4) & 7)));
 
-  cur.win = sm.win;
+  Cursor cur;
+  cur.links = (const_links)p.links + R.link0;
   cur.li = 0;
-  cur.wb = 0;
-  load_window(cur);
-  __syncthreads();
+  cur.k = nullptr;
+  cur.len = cur.tile0 = cur.end = 0;
+  if (R.nlinks > 0) cursor_load(cur);
 
+  // The first tile is copied up front; every later one during its
+  // predecessor's score loop (the last tile re-copies itself into the idle
+  // buffer, which keeps the loop free of branches).
   TileRef ref0{}, ref1{};
   if (t_begin < t_end) {
-    ref0 = tile_ref(cur, t_begin);
-    issue_tile(ref0, goff, sm.k[0], wave);
+    ref0 = tile_ref(cur, t_begin, R.doc_tiles);
+#pragma unroll
+    for (int i = 0; i < kCopies; ++i)
+      tile_copy(i, ref0.k, lds_addr(sk0), wave, lat_off, rope_off);
   }
 
-  // Q of the score tile's row block: d = 16 st + 8 g + (0..7)
+  // Q^T operand of the score tile's row block: dims 16 st + 8 g + (0..7).
   bf16x8 qf[kSteps];
   {
     const uint4 *qrow = (const uint4 *)((const uint16_t *)p.q + orow[rb_s] * kDK);
@@ -203,85 +243,43 @@ __global__ __launch_bounds__(256, 1) void link_mla_kernel(LinkParams p) {
     for (int rb = 0; rb < 2; ++rb)
 #pragma unroll
       for (int x = 0; x < 16; ++x) o[db][rb][x] = 0.f;
+  // Running max (log2 domain) of both row blocks, identical in every wave.
   float m_used[2] = {-INFINITY, -INFINITY};
   float lsum = 0.f;             // partial row sum of the score tile (rb_s, kb_s)
   const float sc = p.scale_log2;
-  // QK fragment addresses (16-byte units): chunk 2 st + g of key row krow sits
-  // at krow * 72 + ((2 st + g) ^ f(krow)) = kq[st % 4] + 8 (st / 4).
+  // Score-operand addresses (16-byte units): lane (n, g) reads key row
+  // kr = 32 kb + key_of_m(n), chunk 2 st + g.
+  // Latent: kr*64 + ((2 st + g) ^ f(kr)) = kq[st % 8] + 16 (st / 8).
+  // Rope:   4096 + kr*8 + ((2 st' + g) ^ f'(kr)) = kp[st'], st' = st - 32.
+  // (f and f' do not depend on bit 5 of the row.)
   const int krow = 32 * kb_s + key_of_m(n);
-  int kq[4];
+  int kq[8], kp[4];
 #pragma unroll
-  for (int b = 0; b < 4; ++b) kq[b] = krow * kChunks + ((2 * b + g) ^ swz(krow));
+  for (int i = 0; i < 8; ++i) kq[i] = krow * kLatChunks + ((2 * i + g) ^ swz(krow));
+#pragma unroll
+  for (int i = 0; i < 4; ++i) kp[i] = kRopeBase + krow * kRopeChunks + ((2 * i + g) ^ swr(krow));
   // Transposing-read byte offsets: in read t, lane (q = lane/16, s = lane%16)
-  // points at key row 8 (q/2) + 4 t + s/4 (+16 ks) and value dims
-  // 128 wave + 32 db + 16 (q%2) + 4 (s%4) .. +3; with db = 2 a + b the
-  // offset is tr_off[t][b] + 128 a (+ ks * 16 rows).
-  int tr_off[2][2];
+  // points at key row 16 ks + 8 (q/2) + 4 t + s/4 and value dims
+  // 128 wave + 32 db + 16 (q%2) + 4 (s%4) .. +3; the offset is
+  // tr_off[t][db] + 16384 ks (f does not depend on bits 4-5 of the row).
+  int tr_off[2][4];
   {
     const int q4 = lane >> 4, s4 = lane & 15;
 #pragma unroll
     for (int t = 0; t < 2; ++t)
 #pragma unroll
-      for (int b = 0; b < 2; ++b) {
-        const int row = 8 * (q4 >> 1) + 4 * t + (s4 >> 2);
-        const int dv = 128 * wave + 32 * b + 16 * (q4 & 1) + 4 * (s4 & 3);
-        tr_off[t][b] = kpos(row, dv >> 3) * 16 + ((dv & 7) >> 2) * 8;
+      for (int db = 0; db < 4; ++db) {
+        const int r = 8 * (q4 >> 1) + 4 * t + (s4 >> 2);
+        const int dv = 128 * wave + 32 * db + 16 * (q4 & 1) + 4 * (s4 & 3);
+        tr_off[t][db] = (r * kLatChunks + ((dv >> 3) ^ swz(r))) * 16 + ((dv & 7) >> 2) * 8;
       }
   }
+  const bf16x2 ones = {(__bf16)1.0f, (__bf16)1.0f};
 
-  auto compute = [&](const uint4 *kt, const TileRef &ref) {
-    // 1. scores
-    f32x16 s;
-#pragma unroll
-    for (int x = 0; x < 16; ++x) s[x] = 0.f;
-#pragma unroll
-    for (int st = 0; st < kSteps; ++st) {
-      // chunk 2 st + g of key row krow: (2 st + g) ^ f keeps 8 (st / 4) intact
-      const bf16x8 kf = as_bf16x8(kt[kq[st & 3] + 8 * (st >> 2)]);
-      s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[st], s, 0, 0, 0);
-    }
-    // K fragment reads run kAhead steps ahead of their MFMA
-    __builtin_amdgcn_sched_group_barrier(0x100, kAhead, 0);
-#pragma unroll
-    for (int st = 0; st < kSteps; ++st) {
-      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-      if (st + kAhead < kSteps) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
-    }
-    // s[x]: key 32 kb_s + (x>>3)*16 + g*8 + (x&7) of row 32 rb_s + n
-    if (ref.own || ref.nvalid < kTile) {
-      const int kl = (ref.own ? min(lim[rb_s] - ref.j0, ref.nvalid - 1) : ref.nvalid - 1) -
-                     32 * kb_s - g * 8;
-#pragma unroll
-      for (int x = 0; x < 16; ++x)
-        if ((x >> 3) * 16 + (x & 7) > kl) s[x] = -INFINITY;
-    }
-    float tmax = -INFINITY;
-#pragma unroll
-    for (int x = 0; x < 16; x += 2) tmax = fmaxf(fmaxf(tmax, s[x]), s[x + 1]);
-    tmax = half_swap_max(tmax);
-    if (g == 0) sm.xm[wave][n] = tmax;
-    __syncthreads();
-    // 2. shared running max of both row blocks (same arithmetic in every wave)
-    float mnew[2];
-#pragma unroll
-    for (int rb = 0; rb < 2; ++rb)
-      mnew[rb] = fmaxf(m_used[rb], fmaxf(sm.xm[2 * rb][n], sm.xm[2 * rb + 1][n]) * sc);
-    if (__any(mnew[0] > m_used[0] + kLazy || mnew[1] > m_used[1] + kLazy)) {
-#pragma unroll
-      for (int rb = 0; rb < 2; ++rb) {
-        const float alpha =
-            mnew[rb] == m_used[rb] ? 1.f : __builtin_amdgcn_exp2f(m_used[rb] - mnew[rb]);
-        m_used[rb] = mnew[rb];
-        if (rb == rb_s) lsum *= alpha;
-#pragma unroll
-        for (int db = 0; db < 4; ++db)
-#pragma unroll
-          for (int x = 0; x < 16; ++x) o[db][rb][x] *= alpha;
-      }
-    }
-    const float mu = rb_s ? m_used[1] : m_used[0];
+  // Probabilities of the score tile against max mu, published in LDS; adds
+  // their (bf16-rounded) sum to lsum.
+  auto publish = [&](const f32x16 &s, float mu) {
     const float neg_m = mu == -INFINITY ? 0.f : -mu;
-    const bf16x2 ones = {(__bf16)1.0f, (__bf16)1.0f};
 #pragma unroll
     for (int h = 0; h < 2; ++h) {
       bf16x8 pf;
@@ -295,58 +293,136 @@ __global__ __launch_bounds__(256, 1) void link_mla_kernel(LinkParams p) {
       }
       sm.p[rb_s][kb_s][h][lane] = __builtin_bit_cast(uint4, pf);
     }
-    __syncthreads();
-    // 3. O^T += V^T P^T for this wave's 128 value dims
-    const char *kbytes = (const char *)kt;
+  };
+  // Moves the running max of both row blocks to mnew, rescaling O and lsum.
+  auto rescale = [&](const float (&mnew)[2]) {
 #pragma unroll
-    for (int ks = 0; ks < 4; ++ks) {
-      const bf16x8 pb0 = as_bf16x8(sm.p[0][ks >> 1][ks & 1][lane]);
-      const bf16x8 pb1 = as_bf16x8(sm.p[1][ks >> 1][ks & 1][lane]);
+    for (int rb = 0; rb < 2; ++rb) {
+      const float alpha =
+          mnew[rb] == m_used[rb] ? 1.f : __builtin_amdgcn_exp2f(m_used[rb] - mnew[rb]);
+      m_used[rb] = mnew[rb];
+      if (rb == rb_s) lsum *= alpha;
+      // one accumulator at a time, so that at most 16 of them pass through
+      // vector registers at once
 #pragma unroll
       for (int db = 0; db < 4; ++db) {
-        // transposing reads (see tr_off): key rows 16 ks + .., value block db
-        i16x4 part[2];
 #pragma unroll
-        for (int t = 0; t < 2; ++t)
-          part[t] = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-              (lds_i16x4 *)(kbytes + tr_off[t][db & 1] + ks * 16 * kChunks * 16 + (db >> 1) * 128));
-        const bf16x8 vf = __builtin_bit_cast(
-            bf16x8, (uint4){(uint32_t)(uint16_t)part[0][0] | ((uint32_t)(uint16_t)part[0][1] << 16),
-                            (uint32_t)(uint16_t)part[0][2] | ((uint32_t)(uint16_t)part[0][3] << 16),
-                            (uint32_t)(uint16_t)part[1][0] | ((uint32_t)(uint16_t)part[1][1] << 16),
-                            (uint32_t)(uint16_t)part[1][2] | ((uint32_t)(uint16_t)part[1][3] << 16)});
-        o[db][0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pb0, o[db][0], 0, 0, 0);
-        o[db][1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pb1, o[db][1], 0, 0, 0);
+        for (int x = 0; x < 16; ++x) o[db][rb][x] *= alpha;
+        __builtin_amdgcn_sched_barrier(0);
       }
     }
-    // per (ks, db): 2 transposing reads (+2 probability reads per ks) then 2 MFMAs
+  };
+
+  // One tile: scores, softmax and value product on kt, while the copy of
+  // the next tile (global nk -> LDS ndst) is spread over the score loop, one
+  // copy every second MFMA, so its issue never stalls the wave for long.
+  auto compute = [&](const uint4 *kt, const TileRef &ref, const char *nk, uint4 *ndst) {
+    // Opaque copies of the copy addresses: otherwise the compiler hoists all
+    // 36 LDS destinations and 18 source addresses out of the tile loop and
+    // spills them.
+    uint32_t lo = lat_off, ro = rope_off, nd = lds_addr(ndst);
+    const char *nkb = nk;
+    asm volatile("" : "+v"(lo), "+v"(ro), "+s"(nd), "+s"(nkb));
+    // 1. scores
+    // The loops are software-pipelined by hand (fragment reads kAhead steps
+    // ahead of their MFMA) and sched_barrier keeps that order.
+    f32x16 s;
 #pragma unroll
-    for (int ks = 0; ks < 4; ++ks) {
-      __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+    for (int x = 0; x < 16; ++x) s[x] = 0.f;
+    bf16x8 kf[kSteps];
+    auto kaddr = [&](int st) {
+      return st < kLatSteps ? kq[st & 7] + 16 * (st >> 3) : kp[st - kLatSteps];
+    };
 #pragma unroll
-      for (int db = 0; db < 4; ++db) {
-        __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
-        __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
+    for (int st = 0; st < kAhead; ++st) kf[st] = as_bf16x8(kt[kaddr(st)]);
+#pragma unroll
+    for (int st = 0; st < kSteps; ++st) {
+      if (st + kAhead < kSteps) kf[st + kAhead] = as_bf16x8(kt[kaddr(st + kAhead)]);
+      if ((st & 1) == 0) tile_copy(st >> 1, nkb, nd, wave, lo, ro);
+      s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[st], qf[st], s, 0, 0, 0);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    // s[x]: key 32 kb_s + (x>>3)*16 + g*8 + (x&7) of row 32 rb_s + n
+    if (ref.own || ref.nvalid < kTile) {
+      const int kl = (ref.own ? min(lim[rb_s] - ref.j0, ref.nvalid - 1) : ref.nvalid - 1) -
+                     32 * kb_s - g * 8;
+#pragma unroll
+      for (int x = 0; x < 16; ++x)
+        if ((x >> 3) * 16 + (x & 7) > kl) s[x] = -INFINITY;
+    }
+    float tmax = -INFINITY;
+#pragma unroll
+    for (int x = 0; x < 16; x += 2) tmax = fmaxf(fmaxf(tmax, s[x]), s[x + 1]);
+    tmax = half_swap_max(tmax) * sc;
+    const float mu = rb_s ? m_used[1] : m_used[0];
+    const bool jump = tmax > mu + kJump;
+    // 2. optimistic probabilities against the running max
+    const float lsum0 = lsum;
+    if (!jump) publish(s, mu);
+    if (g == 0) sm.xm[wave][n] = tmax;
+    const bool wjump = __any(jump);
+    if (lane == 0) ((int *)&sm.jump)[wave] = wjump;
+    __syncthreads();
+    const int4 jf = sm.jump;
+    if (jf.x | jf.y | jf.z | jf.w) {
+      // redo against the new max (uniform over the workgroup)
+      float mnew[2];
+#pragma unroll
+      for (int rb = 0; rb < 2; ++rb)
+        mnew[rb] = fmaxf(m_used[rb], fmaxf(sm.xm[2 * rb][n], sm.xm[2 * rb + 1][n]));
+      lsum = lsum0;
+      rescale(mnew);
+      publish(s, rb_s ? m_used[1] : m_used[0]);
+      __syncthreads();
+    }
+    // 3. O^T += V^T P^T for this wave's 128 value dims
+    // Fragment f = 4 ks + db: two transposing reads (key rows 16 ks ..,
+    // value block db), issued kVLead fragments ahead of its two MFMAs; the
+    // probability operands of step ks are read with fragment 4 ks.
+    const char *kbytes = (const char *)kt;
+    bf16x8 vf[16], pb[4][2];
+    auto read_frag = [&](int f) {
+      const int ks = f >> 2, db = f & 3;
+      if (db == 0) {
+        pb[ks][0] = as_bf16x8(sm.p[0][ks >> 1][ks & 1][lane]);
+        pb[ks][1] = as_bf16x8(sm.p[1][ks >> 1][ks & 1][lane]);
       }
+      i16x4 part[2];
+#pragma unroll
+      for (int t = 0; t < 2; ++t)
+        part[t] = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+            (lds_i16x4 *)(kbytes + tr_off[t][db] + ks * 16384));
+      vf[f] = __builtin_bit_cast(
+          bf16x8, (uint4){(uint32_t)(uint16_t)part[0][0] | ((uint32_t)(uint16_t)part[0][1] << 16),
+                          (uint32_t)(uint16_t)part[0][2] | ((uint32_t)(uint16_t)part[0][3] << 16),
+                          (uint32_t)(uint16_t)part[1][0] | ((uint32_t)(uint16_t)part[1][1] << 16),
+                          (uint32_t)(uint16_t)part[1][2] | ((uint32_t)(uint16_t)part[1][3] << 16)});
+    };
+#pragma unroll
+    for (int f = 0; f < kVLead; ++f) read_frag(f);
+#pragma unroll
+    for (int f = 0; f < 16; ++f) {
+      if (f + kVLead < 16) read_frag(f + kVLead);
+      const int ks = f >> 2, db = f & 3;
+      o[db][0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[f], pb[ks][0], o[db][0], 0, 0, 0);
+      o[db][1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[f], pb[ks][1], o[db][1], 0, 0, 0);
+      __builtin_amdgcn_sched_barrier(0);
     }
   };
 
   asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
   __syncthreads();
+  // Two tiles per trip, one per buffer, with no branch in between (any
+  // branch there makes the compiler copy all accumulators out of the
+  // accumulation registers on every trip): an odd tile count ends with an
+  // empty tile, whose keys are all masked.
   for (int t = t_begin; t < t_end; t += 2) {
-    if (t + 1 < t_end) {
-      ref1 = tile_ref(cur, t + 1);
-      issue_tile(ref1, goff, sm.k[1], wave);
-    }
-    compute(sm.k[0], ref0);
+    ref1 = t + 1 < t_end ? tile_ref(cur, t + 1, R.doc_tiles) : TileRef{ref0.k, 0, 0, 0};
+    compute(sk0, ref0, ref1.k, sk1);
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     __syncthreads();
-    if (t + 1 >= t_end) break;
-    if (t + 2 < t_end) {
-      ref0 = tile_ref(cur, t + 2);
-      issue_tile(ref0, goff, sm.k[0], wave);
-    }
-    compute(sm.k[1], ref1);
+    ref0 = t + 2 < t_end ? tile_ref(cur, t + 2, R.doc_tiles) : ref1;
+    compute(sk1, ref1, ref0.k, sk0);
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     __syncthreads();
   }

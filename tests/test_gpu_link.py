@@ -160,6 +160,23 @@ def test_small_parity(name):
     run_and_check(SMALL[name])
 
 
+def _many_links(kind):
+    rng = np.random.default_rng(5)
+    lens = tuple(int(x) for x in rng.integers(1, 90, size=60))
+    if kind == W.MLA:
+        return W.small_config("many_links_mla", kind=W.MLA, n_q_heads=16, d_k=576, d_v=512,
+                              chunk_lens=lens, batch=2, links=(40, 55), q_len=(6, 3),
+                              self_len=(70, 3), q_std=1.0, scale=1 / math.sqrt(192))
+    return W.small_config("many_links", d_k=128, chunk_lens=lens, batch=2, links=(40, 55),
+                          q_len=(33, 4), self_len=(100, 4))
+
+
+@pytest.mark.parametrize("kind", [W.GQA, W.MLA])
+def test_more_links_than_the_lds_window(kind):
+    """Requests with more links than the kernels' 32-entry LDS link window."""
+    run_and_check(_many_links(kind))
+
+
 DECODE = W.small_config("decode_small", d_k=128, n_q_heads=32, n_kv_heads=8,
                         chunk_lens=(1024, 700, 64, 1, 300, 512), batch=5, links=(0, 4), q_len=1,
                         self_len=(128, 1, 65, 3, 200), decode=True)
