@@ -11,6 +11,12 @@ Default workload: the Llama-3-8B-shaped prefill link (H_q 32, H_kv 8, d 128,
 8 requests x 10 linked chunks of 512 tokens + 256 query tokens with causal own
 KV, bf16). Prints one JSON line.
 
+Warm-up: the W untimed steps are extended, if needed, to at least
+--min-warmup-s seconds of work. The GPU's core clock ramps up over the first
+tens of milliseconds of sustained load; without this, a short warm-up times
+partly ramped clocks (measured: 200 vs 175 us per llama_prefill kernel).
+The JSON line reports both the requested W and the steps actually run.
+
 Algorithmic work counts visible (query, key) pairs only:
   FLOPs = sum_r H_q (2 d_k + 2 d_v) P_r,  P_r = L_q L_d + sum_{i<L_q} (i + 1 + L_s - L_q)
   bytes = Q + out + lse + own KV + each linked chunk's KV once.
@@ -180,6 +186,8 @@ def main(argv=None):
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--min-warmup-s", type=float, default=0.5,
+                    help="run untimed warm-up steps for at least this long (clock ramp-up)")
     ap.add_argument("--config", default="llama_prefill",
                     help="workload: tiny_f32, llama_prefill, long_rag, decode, mla")
     ap.add_argument("--cpu-budget", type=float, default=15.0,
@@ -213,9 +221,13 @@ def main(argv=None):
     keep = set(int(c) for c in wl.plan.chunk_index[wl.plan.chunk_offsets[0]:wl.plan.chunk_offsets[min(4, wl.plan.batch)]])
     dw = runner.upload(wl, keep_host=keep)
     stream = torch.cuda.current_stream()
-    for _ in range(args.warmup):
-        dw.run()
-    torch.cuda.synchronize()
+    warm_run = 0
+    t_w = time.perf_counter()
+    while warm_run < args.warmup or time.perf_counter() - t_w < args.min_warmup_s:
+        for _ in range(max(1, min(args.warmup, 20))):
+            dw.run()
+            warm_run += 1
+        torch.cuda.synchronize()
 
     ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     pic.prof_begin()
@@ -253,6 +265,7 @@ def main(argv=None):
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
+        "warmup_steps_run": warm_run,
         "ms_per_step": round(step_ms, 5),
         "higher_is_better": True,
         "scaling": "weak",

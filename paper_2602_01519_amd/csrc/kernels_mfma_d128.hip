@@ -16,6 +16,10 @@
 // distinct LDS arrays; the tile loop is unrolled by two so every access names
 // its buffer statically, which lets the compiler see that a tile's reads and
 // the next tile's copy never alias (no wait on the copy before the reads).
+// The next tile's 8 copies per lane are spread over the current tile's QK
+// loop (one per QK step) rather than issued as one burst: a burst from all
+// 8 waves of a CU at once stalls every wave at issue until the copy path
+// drains.
 // The store keeps V transposed per chunk, so a V^T tile is 128 rows of 128
 // contiguous bytes. The M index of the QK^T product is permuted (key row
 // pi(m) feeds M index m) so that the scores a lane receives for a 16-key PV
@@ -43,7 +47,6 @@ constexpr int kWaves = 4;
 constexpr int kRowsPerWave = 32;
 constexpr int kRows = kWaves * kRowsPerWave;
 constexpr float kLazy = 8.0f;
-constexpr int kWin = 32;     // link-table entries staged in LDS
 #ifndef PIC_QK_AHEAD
 #define PIC_QK_AHEAD 5
 #endif
@@ -79,12 +82,6 @@ __device__ __forceinline__ int key_of_m(int m) {
 __device__ __forceinline__ bf16x8 as_bf16x8(uint4 u) { return __builtin_bit_cast(bf16x8, u); }
 
 __device__ __forceinline__ int uni(int x) { return __builtin_amdgcn_readfirstlane(x); }
-__device__ __forceinline__ const char *uni(const void *p) {
-  const uint64_t u = (uint64_t)p;
-  const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)u);
-  const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(u >> 32));
-  return (const char *)(((uint64_t)hi << 32) | lo);
-}
 
 // Max / sum of a value over lanes i and i ^ 32 (the two key halves of a row).
 __device__ __forceinline__ float half_swap_max(float x) {
@@ -108,62 +105,67 @@ struct TileRef {
   int own;           // the tile belongs to the request's own KV (causal mask)
 };
 
+// The link and request tables are read through the constant address space:
+// every lookup is a scalar load and the link cursor lives in scalar
+// registers (no LDS, no barrier).
+typedef __attribute__((address_space(4))) const LinkEntry *const_links;
+typedef __attribute__((address_space(4))) const ReqEntry *const_reqs;
+typedef __attribute__((address_space(4))) const int32_t *const_ints;
+
 struct Ctx {
-  const LinkParams *p;
   ReqEntry R;
   int kvh, wave, lane, n, g;
-  LinkEntry *win;    // link-table window in LDS
-  int li, wb;        // cursor: current link, first link held in the window
+  const_links links;           // the request's links
+  int li;                      // cursor: current link
+  const char *lk, *lv;         // its K / V^T blocks
+  int llen, llp, ltile0, lend; // its tokens, padded tokens, first tile, tile after its last
   uint32_t koff[4];  // byte offsets of this lane's 4 K chunks within a tile
   uint32_t vrow[4], vcol[4];   // row / byte column of its 4 V^T chunks
 };
 
-__device__ __forceinline__ void load_window(Ctx &c) {
-  const int n = min(kWin, c.R.nlinks - c.wb);
-  for (int i = threadIdx.x; i < n; i += blockDim.x) c.win[i] = c.p->links[c.R.link0 + c.wb + i];
+__device__ __forceinline__ void cursor_load(Ctx &c) {
+  c.lk = (const char *)c.links[c.li].k;
+  c.lv = (const char *)c.links[c.li].v;
+  c.llen = c.links[c.li].len;
+  c.llp = c.links[c.li].lp;
+  c.ltile0 = c.links[c.li].tile0;
+  c.lend = c.ltile0 + c.llp / kTile;
 }
 
-// Tile t of the request (t only grows across calls). Workgroup-uniform: it
-// may reload the link window between two barriers.
+// Tile t of the request (t only grows across calls).
 __device__ __forceinline__ TileRef tile_ref(Ctx &c, int t) {
-  for (;;) {
-    if (c.li - c.wb >= kWin) {
-      __syncthreads();
-      c.wb += kWin;
-      load_window(c);
-      __syncthreads();
-    }
-    const LinkEntry &e = c.win[c.li - c.wb];
-    const int tile0 = uni(e.tile0), lp = uni(e.lp);
-    if (t < tile0 + lp / kTile) {
-      const int tt = t - tile0;
-      TileRef r;
-      r.lp = lp;
-      r.nvalid = min(kTile, uni(e.len) - tt * kTile);
-      r.j0 = tt * kTile;
-      r.own = t >= c.R.doc_tiles;
-      r.k = uni(e.k) + ((int64_t)c.kvh * lp + tt * kTile) * kD * 2;
-      r.v = uni(e.v) + ((int64_t)c.kvh * kD * lp + tt * kTile) * 2;
-      return r;
-    }
+  while (t >= c.lend) {
     ++c.li;
+    cursor_load(c);
   }
+  const int tt = t - c.ltile0;
+  TileRef r;
+  r.lp = c.llp;
+  r.nvalid = min(kTile, c.llen - tt * kTile);
+  r.j0 = tt * kTile;
+  r.own = t >= c.R.doc_tiles;
+  r.k = c.lk + ((int64_t)c.kvh * c.llp + tt * kTile) * kD * 2;
+  r.v = c.lv + ((int64_t)c.kvh * kD * c.llp + tt * kTile) * 2;
+  return r;
 }
 
 // Copies of a tile into LDS: lane i of a load-to-LDS lands at slot base + i,
 // so each lane fetches the global chunk that belongs at that slot of the
 // swizzled layout (uniform base address + per-lane 32-bit offset).
-__device__ __forceinline__ void issue_k(const Ctx &c, const TileRef &r, uint4 *kdst) {
-#pragma unroll
-  for (int u = 0; u < 4; ++u)
-    __builtin_amdgcn_global_load_lds(r.k + c.koff[u], (lds_ptr)(kdst + (u * kWaves + c.wave) * 64),
+// Copy i (0..7) of a tile: i < 4 is K chunk set i, i >= 4 V^T chunk set i-4.
+__device__ __forceinline__ void tile_copy(const Ctx &c, int i, const TileRef &r, uint4 *kdst,
+                                          uint4 *vdst) {
+  if (i < 4)
+    __builtin_amdgcn_global_load_lds(r.k + c.koff[i], (lds_ptr)(kdst + (i * kWaves + c.wave) * 64),
                                      16, 0, 0);
+  else
+    __builtin_amdgcn_global_load_lds(r.v + (c.vrow[i - 4] * (uint32_t)r.lp * 2u + c.vcol[i - 4]),
+                                     (lds_ptr)(vdst + ((i - 4) * kWaves + c.wave) * 64), 16, 0, 0);
 }
-__device__ __forceinline__ void issue_v(const Ctx &c, const TileRef &r, uint4 *vdst) {
+__device__ __forceinline__ void issue_tile(const Ctx &c, const TileRef &r, uint4 *kdst,
+                                           uint4 *vdst) {
 #pragma unroll
-  for (int u = 0; u < 4; ++u)
-    __builtin_amdgcn_global_load_lds(r.v + (c.vrow[u] * (uint32_t)r.lp * 2u + c.vcol[u]),
-                                     (lds_ptr)(vdst + (u * kWaves + c.wave) * 64), 16, 0, 0);
+  for (int i = 0; i < 8; ++i) tile_copy(c, i, r, kdst, vdst);
 }
 
 struct Acc {
@@ -194,7 +196,8 @@ __device__ __forceinline__ void mask_tile(const Ctx &c, f32x16 &s0, f32x16 &s1, 
 // MFMA does not wait on the read issued right before it.
 __device__ __forceinline__ void compute_tile(const Ctx &c, const uint4 *kt, const uint4 *vt,
                                              const bf16x8 (&qf)[8], Acc &a, int nvalid, int j0,
-                                             int own, int lim, float sc) {
+                                             int own, int lim, float sc, const TileRef &nref,
+                                             uint4 *nk, uint4 *nv) {
   const int krow0 = key_of_m(c.n);
   f32x16 s0, s1;
 #pragma unroll
@@ -202,19 +205,24 @@ __device__ __forceinline__ void compute_tile(const Ctx &c, const uint4 *kt, cons
     s0[x] = 0.f;
     s1[x] = 0.f;
   }
+  // QK, pipelined by hand: K reads kQkAhead steps ahead of their MFMAs, one
+  // copy of the next tile per step; sched_barrier keeps that order.
+  bf16x8 ka[8], kb[8];
 #pragma unroll
-  for (int st = 0; st < 8; ++st) {
-    const bf16x8 ka = as_bf16x8(kt[k_slot(krow0, st * 2 + c.g)]);
-    const bf16x8 kb = as_bf16x8(kt[k_slot(32 + krow0, st * 2 + c.g)]);
-    s0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka, qf[st], s0, 0, 0, 0);
-    s1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kb, qf[st], s1, 0, 0, 0);
+  for (int st = 0; st < kQkAhead; ++st) {
+    ka[st] = as_bf16x8(kt[k_slot(krow0, st * 2 + c.g)]);
+    kb[st] = as_bf16x8(kt[k_slot(32 + krow0, st * 2 + c.g)]);
   }
-  // K reads run kQkAhead steps (2 reads per step) ahead of the MFMAs
-  __builtin_amdgcn_sched_group_barrier(0x100, 2 * kQkAhead, 0);
 #pragma unroll
   for (int st = 0; st < 8; ++st) {
-    __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
-    if (st + kQkAhead < 8) __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+    if (st + kQkAhead < 8) {
+      ka[st + kQkAhead] = as_bf16x8(kt[k_slot(krow0, (st + kQkAhead) * 2 + c.g)]);
+      kb[st + kQkAhead] = as_bf16x8(kt[k_slot(32 + krow0, (st + kQkAhead) * 2 + c.g)]);
+    }
+    tile_copy(c, st, nref, nk, nv);
+    s0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka[st], qf[st], s0, 0, 0, 0);
+    s1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kb[st], qf[st], s1, 0, 0, 0);
+    __builtin_amdgcn_sched_barrier(0);
   }
   mask_tile(c, s0, s1, nvalid, j0, own, lim);
 
@@ -272,10 +280,8 @@ __device__ __forceinline__ void compute_tile(const Ctx &c, const uint4 *kt, cons
 __global__ __launch_bounds__(256, 2) void link_mfma_d128_kernel(LinkParams p) {
   __shared__ uint4 sk0[kTile * 16], sk1[kTile * 16];
   __shared__ uint4 sv0[kD * 8], sv1[kD * 8];
-  __shared__ LinkEntry win[kWin];
 
   Ctx c;
-  c.p = &p;
   c.lane = threadIdx.x & 63;
   c.wave = uni(threadIdx.x >> 6);
   c.n = c.lane & 31;
@@ -290,9 +296,18 @@ __global__ __launch_bounds__(256, 2) void link_mfma_d128_kernel(LinkParams p) {
   const int rb = j % p.nrb;
   const int split = blockIdx.y;
   if (grp >= p.batch * p.n_kv_heads) return;
-  const int req_i = p.order[grp / p.n_kv_heads];
+  const int req_i = ((const_ints)p.order)[grp / p.n_kv_heads];
   c.kvh = grp % p.n_kv_heads;
-  c.R = p.reqs[req_i];
+  {
+    const_reqs rq = (const_reqs)p.reqs + req_i;
+    c.R.link0 = rq->link0;
+    c.R.nlinks = rq->nlinks;
+    c.R.q0 = rq->q0;
+    c.R.lq = rq->lq;
+    c.R.ls = rq->ls;
+    c.R.doc_tiles = rq->doc_tiles;
+    c.R.tiles = rq->tiles;
+  }
   const ReqEntry &R = c.R;
   const int group = p.group;
   const int nrows = R.lq * group;
@@ -320,18 +335,17 @@ __global__ __launch_bounds__(256, 2) void link_mfma_d128_kernel(LinkParams p) {
     c.vcol[u] = (uint32_t)(((s & 7) ^ hv(dv & 31)) * 16);
   }
 
-  c.win = win;
+  c.links = (const_links)p.links + c.R.link0;
   c.li = 0;
-  c.wb = 0;
-  load_window(c);
-  __syncthreads();
+  c.lk = c.lv = nullptr;
+  c.llen = c.llp = c.ltile0 = c.lend = 0;
+  if (c.R.nlinks > 0) cursor_load(c);
 
   // masking facts of the tile held in each buffer pair
   TileRef ref0{}, ref1{};
   if (t_begin < t_end) {
     ref0 = tile_ref(c, t_begin);
-    issue_k(c, ref0, sk0);
-    issue_v(c, ref0, sv0);
+    issue_tile(c, ref0, sk0, sv0);
   }
 
   // Q fragments: d = step*16 + g*8 + (0..7)
@@ -358,25 +372,20 @@ __global__ __launch_bounds__(256, 2) void link_mfma_d128_kernel(LinkParams p) {
   asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
   __syncthreads();
 
-  // Unrolled by two so every access names its buffers statically.
+  // Unrolled by two so every access names its buffers statically. The
+  // copy of the next tile runs inside the current tile's QK loop; after the
+  // last tile that copy repeats the current tile into the idle buffers,
+  // which keeps the loop free of branches around it.
   for (int t = t_begin; t < t_end; t += 2) {
     // tile t in buffers 0; copy tile t+1 into buffers 1
-    if (t + 1 < t_end) {
-      ref1 = tile_ref(c, t + 1);
-      issue_k(c, ref1, sk1);
-      issue_v(c, ref1, sv1);
-    }
-    compute_tile(c, sk0, sv0, qf, a, ref0.nvalid, ref0.j0, ref0.own, lim, sc);
+    ref1 = t + 1 < t_end ? tile_ref(c, t + 1) : ref0;
+    compute_tile(c, sk0, sv0, qf, a, ref0.nvalid, ref0.j0, ref0.own, lim, sc, ref1, sk1, sv1);
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     __syncthreads();
     if (t + 1 >= t_end) break;
     // tile t+1 in buffers 1; copy tile t+2 into buffers 0
-    if (t + 2 < t_end) {
-      ref0 = tile_ref(c, t + 2);
-      issue_k(c, ref0, sk0);
-      issue_v(c, ref0, sv0);
-    }
-    compute_tile(c, sk1, sv1, qf, a, ref1.nvalid, ref1.j0, ref1.own, lim, sc);
+    ref0 = t + 2 < t_end ? tile_ref(c, t + 2) : ref1;
+    compute_tile(c, sk1, sv1, qf, a, ref1.nvalid, ref1.j0, ref1.own, lim, sc, ref0, sk0, sv0);
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     __syncthreads();
   }
