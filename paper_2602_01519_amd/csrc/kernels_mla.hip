@@ -11,13 +11,16 @@
 //   1. wave (rb, kb) computes S^T[32 keys kb][32 rows rb] = K Q^T over the 576
 //      latent dims (36 x v_mfma_f32_32x32x16_bf16, Q held in registers) and
 //      turns it into bf16 probabilities against the running max it already
-//      holds, publishing them and its per-row tile maxima in LDS;
-//   2. one barrier; every wave reads both halves' maxima and makes the same
-//      decision: normally the stale max stays in use and the accumulators are
-//      rescaled after the value product if the max grew by more than 2^8; a
-//      tile that raises some row's max by more than 2^64 (the first tile of
-//      every row, for one) is redone against the new max behind one more
-//      barrier, so probabilities never exceed 2^64;
+//      holds, publishing them in LDS with one flag: some probability of the
+//      wave may exceed 2^64 (its partial row sum does), or a row has no
+//      running max yet;
+//   2. one barrier; if any wave raised the flag (the first tile of every
+//      row, and tiles whose max jumps by more than 2^64 over the running
+//      max), all waves redo the tile: exact tile maxima through LDS, new
+//      running max, rescaled accumulators, probabilities published again.
+//      Otherwise the running max stays as it is: fp32 and bf16 keep their
+//      relative precision at any magnitude, and probabilities stay <= 2^64,
+//      so no per-tile rescale is needed;
 //   3. wave w owns value dims [128 w, 128 w + 128) of all 64 rows and adds
 //      O^T += V^T P^T (32 MFMAs): V^T fragments are read straight out of the
 //      key tile with transposing LDS reads (ds_read_b64_tr_b16), so the
@@ -51,7 +54,7 @@ constexpr int kLatSteps = 32;            // of which over the latent part
 constexpr int kRowsMla = 64;             // rows per workgroup
 constexpr int kRopeBase = kTile * kLatChunks;                   // 4096 chunks
 constexpr int kTileChunks = kTile * (kLatChunks + kRopeChunks); // 4608 chunks
-constexpr float kJump = 64.0f;           // redo a tile whose max jumps by 2^64
+constexpr float kJumpSum = 18446744073709551616.0f;  // 2^64: redo a tile past it
 constexpr int kAhead = 6;                // K fragment read lead in the score loop
 constexpr int kVLead = 3;                // value fragment read lead in the value loop
 
@@ -85,7 +88,7 @@ __device__ __forceinline__ uint32_t lds_addr(const void *p) {
 struct MlaSmem {
   uint4 p[2][2][2][64];                    // probabilities [rb][kb][h][lane]
   float xm[4][32];                         // per-wave row maxima of the tile / row sums
-  int4 jump;                               // per wave: some row's max jumped past kJump
+  int4 jump;                               // per wave: the tile must be redone
 };
 
 struct TileRef {
@@ -276,10 +279,11 @@ __global__ __launch_bounds__(256, 1) void link_mla_kernel(LinkParams p) {
   }
   const bf16x2 ones = {(__bf16)1.0f, (__bf16)1.0f};
 
-  // Probabilities of the score tile against max mu, published in LDS; adds
-  // their (bf16-rounded) sum to lsum.
+  // Probabilities of the score tile against max mu, published in LDS;
+  // returns their (bf16-rounded) sum over this lane's keys.
   auto publish = [&](const f32x16 &s, float mu) {
     const float neg_m = mu == -INFINITY ? 0.f : -mu;
+    float ts = 0.f;
 #pragma unroll
     for (int h = 0; h < 2; ++h) {
       bf16x8 pf;
@@ -289,10 +293,11 @@ __global__ __launch_bounds__(256, 1) void link_mla_kernel(LinkParams p) {
 #pragma unroll
       for (int x = 0; x < 8; x += 2) {
         const bf16x2 pp = {pf[x], pf[x + 1]};
-        lsum = __builtin_amdgcn_fdot2_f32_bf16(pp, ones, lsum, false);
+        ts = __builtin_amdgcn_fdot2_f32_bf16(pp, ones, ts, false);
       }
       sm.p[rb_s][kb_s][h][lane] = __builtin_bit_cast(uint4, pf);
     }
+    return ts;
   };
   // Moves the running max of both row blocks to mnew, rescaling O and lsum.
   auto rescale = [&](const float (&mnew)[2]) {
@@ -350,31 +355,18 @@ __global__ __launch_bounds__(256, 1) void link_mla_kernel(LinkParams p) {
       for (int x = 0; x < 16; ++x)
         if ((x >> 3) * 16 + (x & 7) > kl) s[x] = -INFINITY;
     }
-    float tmax = -INFINITY;
-#pragma unroll
-    for (int x = 0; x < 16; x += 2) tmax = fmaxf(fmaxf(tmax, s[x]), s[x + 1]);
-    tmax = half_swap_max(tmax) * sc;
+    // 2. probabilities against the running max as it stands. A lane whose
+    // partial sum stays <= 2^64 has every probability <= 2^64; the
+    // tile's own max is only computed when some lane of the workgroup fails
+    // that test (or has no running max yet).
     const float mu = rb_s ? m_used[1] : m_used[0];
-    const bool jump = tmax > mu + kJump;
-    // 2. optimistic probabilities against the running max
     const float lsum0 = lsum;
-    if (!jump) publish(s, mu);
-    if (g == 0) sm.xm[wave][n] = tmax;
+    const float ts = publish(s, mu);
+    lsum += ts;
+    const bool jump = !(ts <= kJumpSum) || (mu == -INFINITY && ts > 0.f);
     const bool wjump = __any(jump);
     if (lane == 0) ((int *)&sm.jump)[wave] = wjump;
     __syncthreads();
-    const int4 jf = sm.jump;
-    if (jf.x | jf.y | jf.z | jf.w) {
-      // redo against the new max (uniform over the workgroup)
-      float mnew[2];
-#pragma unroll
-      for (int rb = 0; rb < 2; ++rb)
-        mnew[rb] = fmaxf(m_used[rb], fmaxf(sm.xm[2 * rb][n], sm.xm[2 * rb + 1][n]));
-      lsum = lsum0;
-      rescale(mnew);
-      publish(s, rb_s ? m_used[1] : m_used[0]);
-      __syncthreads();
-    }
     // 3. O^T += V^T P^T for this wave's 128 value dims
     // Fragment f = 4 ks + db: two transposing reads (key rows 16 ks ..,
     // value block db), issued kVLead fragments ahead of its two MFMAs; the
@@ -398,6 +390,24 @@ __global__ __launch_bounds__(256, 1) void link_mla_kernel(LinkParams p) {
                           (uint32_t)(uint16_t)part[1][0] | ((uint32_t)(uint16_t)part[1][1] << 16),
                           (uint32_t)(uint16_t)part[1][2] | ((uint32_t)(uint16_t)part[1][3] << 16)});
     };
+    const int4 jf = sm.jump;
+    if (jf.x | jf.y | jf.z | jf.w) {
+      // redo the tile against the new running max (uniform over the workgroup)
+      float tmax = -INFINITY;
+#pragma unroll
+      for (int x = 0; x < 16; x += 2) tmax = fmaxf(fmaxf(tmax, s[x]), s[x + 1]);
+      tmax = half_swap_max(tmax) * sc;
+      if (g == 0) sm.xm[wave][n] = tmax;
+      __syncthreads();
+      float mnew[2];
+#pragma unroll
+      for (int rb = 0; rb < 2; ++rb)
+        mnew[rb] = fmaxf(m_used[rb], fmaxf(sm.xm[2 * rb][n], sm.xm[2 * rb + 1][n]));
+      lsum = lsum0;
+      rescale(mnew);
+      lsum += publish(s, rb_s ? m_used[1] : m_used[0]);
+      __syncthreads();
+    }
 #pragma unroll
     for (int f = 0; f < kVLead; ++f) read_frag(f);
 #pragma unroll
