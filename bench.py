@@ -248,7 +248,9 @@ def main(argv=None):
     gbs = nbytes / (step_ms * 1e-3) / 1e9
     if cfg.dtype == W.F32:
         bound, peak, unit, achieved = "alu", PEAK_FP32_VALU_TFLOPS, "TFLOP/s", flops / (kern_avg_ms * 1e-3) / 1e12
-    elif cfg.decode:
+    elif flops / nbytes < PEAK_BF16_TFLOPS * 1e12 / (PEAK_HBM_GBS * 1e9):
+        # below the ridge point (about 312 FLOP/B): decode, and short questions
+        # over long documents
         bound, peak, unit, achieved = "hbm", PEAK_HBM_GBS, "GB/s", nbytes / (kern_avg_ms * 1e-3) / 1e9
     else:
         bound, peak, unit, achieved = "mfma", PEAK_BF16_TFLOPS, "TFLOP/s", flops / (kern_avg_ms * 1e-3) / 1e12

@@ -130,6 +130,10 @@ typedef struct pic_link_req {
  * n_q_heads must be a multiple of n_kv_heads. softmax_scale (positive,
  * finite) multiplies the dot products (Eq. 2 and 7 use 1/sqrt(d)). The chunk table of the call is
  * copied to the device on `stream`; all host arrays are consumed on return.
+ * When the batch has too few query rows to fill the GPU (short questions
+ * over long documents), the library splits each request's keys and merges
+ * the partial softmax states exactly, as pic_link_decode does; the result
+ * is the same up to floating-point rounding order.
  * Errors: INVALID, NOT_FOUND, UNSUPPORTED, HIP. */
 pic_status pic_link_attn(pic_store *store, const pic_link_req *req, int32_t n_q_heads,
                          const void *q, const void *k_self, const void *v_self,

@@ -316,7 +316,11 @@ __global__ __launch_bounds__(256, 2) void link_mfma_d128_kernel(LinkParams p) {
   const int t_begin = (int)((int64_t)R.tiles * split / p.num_splits);
   const int t_end = (int)((int64_t)R.tiles * (split + 1) / p.num_splits);
 
-  // This lane's row.
+  // This lane's row. A wave whose 32 rows are all past the request's rows
+  // (short questions: a 16-token question fills 64 of the 128 rows) only
+  // copies its share of every tile and meets the barriers, leaving its SIMD
+  // to the other workgroup on the CU.
+  const bool active = row0 + c.wave * kRowsPerWave < nrows;
   const int row = row0 + c.wave * kRowsPerWave + c.n;
   const bool rvalid = row < nrows;
   const int qi = rvalid ? row / group : 0;
@@ -379,13 +383,19 @@ __global__ __launch_bounds__(256, 2) void link_mfma_d128_kernel(LinkParams p) {
   for (int t = t_begin; t < t_end; t += 2) {
     // tile t in buffers 0; copy tile t+1 into buffers 1
     ref1 = t + 1 < t_end ? tile_ref(c, t + 1) : ref0;
-    compute_tile(c, sk0, sv0, qf, a, ref0.nvalid, ref0.j0, ref0.own, lim, sc, ref1, sk1, sv1);
+    if (active)
+      compute_tile(c, sk0, sv0, qf, a, ref0.nvalid, ref0.j0, ref0.own, lim, sc, ref1, sk1, sv1);
+    else
+      issue_tile(c, ref1, sk1, sv1);
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     __syncthreads();
     if (t + 1 >= t_end) break;
     // tile t+1 in buffers 1; copy tile t+2 into buffers 0
     ref0 = t + 2 < t_end ? tile_ref(c, t + 2) : ref1;
-    compute_tile(c, sk1, sv1, qf, a, ref1.nvalid, ref1.j0, ref1.own, lim, sc, ref0, sk0, sv0);
+    if (active)
+      compute_tile(c, sk1, sv1, qf, a, ref1.nvalid, ref1.j0, ref1.own, lim, sc, ref0, sk0, sv0);
+    else
+      issue_tile(c, ref0, sk0, sv0);
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     __syncthreads();
   }

@@ -375,31 +375,44 @@ pic_status link_call(pic_store *s, const pic_link_req *req, int32_t n_q_heads, c
   if (kern == K::Mfma128) lp.n_groups = (int32_t)round_up(lp.n_groups, 8);
 
   int32_t splits = 1;
+  const int64_t blocks = (int64_t)req->batch * d.n_kv_heads * lp.nrb;
   if (mode == Mode::Decode) {
     if (num_splits > 0) {
       splits = num_splits;
     } else {
       // about 2048 work items (one wave each for the decode kernel, a
       // workgroup each otherwise), never more splits than tiles
-      const int64_t blocks = (int64_t)req->batch * d.n_kv_heads * lp.nrb;
       splits = (int32_t)std::max<int64_t>(1, std::min<int64_t>((2048 + blocks - 1) / blocks, 256));
       splits = std::min(splits, std::max(1, P.max_tiles));
     }
+  } else if (kern == K::Mfma128 || kern == K::Mla) {
+    // Short queries over long documents (the regime the paper targets: a
+    // few dozen dynamic tokens after thousands of cached ones) leave one
+    // row block per (request, kv head), and the longest request sets the
+    // kernel time. Split every request's key range so that its longest
+    // piece is no longer than the average work per workgroup slot of the
+    // GPU (2 per CU for the d=128 kernel, 1 for MLA), with >= 8 tiles per
+    // piece and at most 16 pieces.
+    const int64_t slots = kern == K::Mla ? 256 : 512;
+    int64_t work = 0;   // tiles summed over all non-empty workgroups
+    for (const ReqEntry &R : P.reqs) {
+      const int64_t rows = (int64_t)R.lq * lp.group;
+      work += (int64_t)d.n_kv_heads * ((rows + rows_per_block - 1) / rows_per_block) * R.tiles;
+    }
+    const int64_t per_slot = std::max<int64_t>(8, (work + slots - 1) / slots);
+    splits = (int32_t)std::min<int64_t>(16, (P.max_tiles + per_slot - 1) / per_slot);
+    splits = std::max(1, std::min(splits, P.max_tiles / 8));
   }
   lp.num_splits = splits;
-  // Own KV: the matrix-core prefill kernel reads it in place; the other
-  // kernels read it laid out like a chunk slot in the workspace.
-  const bool own_inline = false;
-  // Workspace: [own KV slots][split partials].
+  // Workspace: [own KV slots, laid out like chunk slots][split partials].
   const size_t rows = (size_t)P.total_q * n_q_heads;
-  const size_t part_off = own_inline ? 0 : round_up(P.own_bytes, 256);
+  const size_t part_off = round_up(P.own_bytes, 256);
   const size_t part_bytes = splits > 1 ? rows * splits * (d.d_v + 2) * sizeof(float) : 0;
   if (part_off + part_bytes > 0) {
     rc = ensure_work(s, part_off + part_bytes);
     if (rc != PIC_OK) return rc;
   }
   for (auto &o : P.own) {
-    if (own_inline) break;
     LinkEntry &E = P.links[o.first];
     E.k = (char *)s->work + o.second;
     E.v = mla ? E.k : (const char *)E.k + (int64_t)E.lp * s->k_tok_elems * s->esz;
@@ -417,7 +430,7 @@ pic_status link_call(pic_store *s, const pic_link_req *req, int32_t n_q_heads, c
   rc = upload(s, P, st, true, &stage, lp, tl);
   if (rc != PIC_OK) return rc;
 
-  if (P.max_own_lp > 0 && !own_inline) {
+  if (P.max_own_lp > 0) {
     hipError_t e = launch_prep_own(lp, mla, s->esz, P.max_own_lp, st);
     if (e != hipSuccess) return hip_fail(e, "prep_own kernels");
   }

@@ -94,6 +94,8 @@ class LinkConfig:
 _BASE_SEED = 20260201
 
 # The five workloads the measurements are quoted on.
+SKINNY_Q = tuple((16, 32, 48)[r % 3] for r in range(32))
+
 CONFIGS = {
     # 4 ordered links out of a 16-chunk store, 32 query tokens with causal own KV, fp32.
     "tiny_f32": LinkConfig("tiny_f32", F32, GQA, 8, 2, 64, 64, 16, 128, 1, (4, 4), 32, 32,
@@ -111,6 +113,12 @@ CONFIGS = {
     # DeepSeek-V2-Lite MLA, absorbed: one latent KV row of 512 + 64 rope dims, 16 heads.
     "mla": LinkConfig("mla", BF16, MLA, 16, 1, 576, 512, 64, 512, 8, (12, 12), 256, 256,
                       1.0, 1.0 / math.sqrt(192.0), _BASE_SEED + 5),
+    # The paper's own regime: a few dozen dynamic (question) tokens after 4K-16K cached
+    # document tokens. Llama-3-8B head shape, 32 requests each linking 4..16 private
+    # chunks of 1024 tokens; question lengths 16 / 32 / 48 tokens, own KV = the question.
+    "skinny_rag": LinkConfig("skinny_rag", BF16, GQA, 32, 8, 128, 128, 512, 1024, 32, (4, 16),
+                             SKINNY_Q, SKINNY_Q, 1.0 / math.sqrt(128.0), 1.0, _BASE_SEED + 6,
+                             disjoint=True),
 }
 
 

@@ -246,6 +246,24 @@ def test_config_mla():
     run_and_check(W.CONFIGS["mla"], requests=[3])
 
 
+def test_config_skinny_rag():
+    cfg = W.CONFIGS["skinny_rag"]
+    p = W.make_plan(cfg)
+    n = np.diff(p.chunk_offsets)
+    # the longest and the shortest link lists, and one request per question length
+    run_and_check(cfg, requests=sorted({int(np.argmax(n)), int(np.argmin(n)), 0, 1, 2}))
+
+
+# Short questions over long documents: the prefill entry splits the key range
+# of each (request, kv head) and merges the partial softmax states.
+@pytest.mark.parametrize("q_len", [(16, 32, 48), (48, 16, 32)])
+def test_skinny_split_prefill(q_len):
+    cfg = W.small_config("skinny_small", d_k=128, n_q_heads=8, n_kv_heads=2,
+                         chunk_lens=(1024, 700, 1024, 513, 1024, 900, 64, 1024), batch=3,
+                         links=(3, 6), q_len=q_len, self_len=q_len, seed=11)
+    run_and_check(cfg)
+
+
 # ---------------------------------------------------------------------------
 # invariants on the GPU
 
