@@ -390,10 +390,10 @@ pic_status link_call(pic_store *s, const pic_link_req *req, int32_t n_q_heads, c
     // few dozen dynamic tokens after thousands of cached ones) leave one
     // row block per (request, kv head), and the longest request sets the
     // kernel time. Split every request's key range so that its longest
-    // piece is no longer than the average work per workgroup slot of the
-    // GPU (2 per CU for the d=128 kernel, 1 for MLA), with >= 8 tiles per
-    // piece and at most 16 pieces.
-    const int64_t slots = kern == K::Mla ? 256 : 512;
+    // piece is no longer than the average work per resident workgroup of
+    // the GPU (256 CUs times the kernel's workgroups per CU), with >= 8
+    // tiles per piece and at most 16 pieces.
+    const int64_t slots = 256 * (kern == K::Mla ? 1 : mfma_d128_blocks_per_cu());
     int64_t work = 0;   // tiles summed over all non-empty workgroups
     for (const ReqEntry &R : P.reqs) {
       const int64_t rows = (int64_t)R.lq * lp.group;

@@ -88,6 +88,7 @@ int valu_rows_per_block();
 // bf16 GQA link attention on MFMA, d_k = d_v = 128 (prefill-shaped).
 hipError_t launch_link_mfma_d128(const LinkParams &p, hipStream_t st, const char **name);
 int mfma_d128_rows_per_block();
+int mfma_d128_blocks_per_cu();   // resident workgroups per CU (2 waves per SIMD)
 
 // bf16 GQA decode-shaped link attention, d_k = d_v = 128, at most
 // decode_d128_max_rows() rows per (request, kv head); one wave per split.
