@@ -120,7 +120,12 @@ pic_status stage_acquire(pic_store *s, size_t bytes, Stage **out) {
     HIP_TRY(hipEventSynchronize(st.done), "hipEventSynchronize(stage)");
     st.pending = false;
   }
-  if (!st.done) HIP_TRY(hipEventCreateWithFlags(&st.done, hipEventDisableTiming), "hipEventCreate");
+  // Completion only (the host waits for the copy out of the staging buffer
+  // to be done): no system-scope fence, which would write back and
+  // invalidate caches after every call.
+  if (!st.done)
+    HIP_TRY(hipEventCreateWithFlags(&st.done, hipEventDisableTiming | hipEventDisableSystemFence),
+            "hipEventCreate");
   if (st.cap < bytes) {
     if (st.host) (void)hipHostFree(st.host);
     if (st.dev) (void)hipFree(st.dev);
@@ -305,7 +310,10 @@ void prof_start(hipStream_t st, std::pair<hipEvent_t, hipEvent_t> *ev) {
   if (!g_prof.spare.empty()) {
     *ev = g_prof.spare.back();
     g_prof.spare.pop_back();
-  } else if (hipEventCreate(&ev->first) != hipSuccess || hipEventCreate(&ev->second) != hipSuccess) {
+  } else if (hipEventCreateWithFlags(&ev->first, hipEventDisableSystemFence) != hipSuccess ||
+             hipEventCreateWithFlags(&ev->second, hipEventDisableSystemFence) != hipSuccess) {
+    // timing-only events: a system-scope fence would add a cache writeback
+    // and invalidation around the timed kernel
     ev->first = ev->second = nullptr;
     return;
   }
