@@ -186,6 +186,8 @@ def main(argv=None):
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--no-measured-peaks", action="store_true",
+                    help="skip the achievable-peak microbenchmarks (second roofline denominator)")
     ap.add_argument("--min-warmup-s", type=float, default=0.5,
                     help="run untimed warm-up steps for at least this long (clock ramp-up)")
     ap.add_argument("--config", default="llama_prefill",
@@ -255,6 +257,21 @@ def main(argv=None):
     else:
         bound, peak, unit, achieved = "mfma", PEAK_BF16_TFLOPS, "TFLOP/s", flops / (kern_avg_ms * 1e-3) / 1e12
 
+    # Achievable peaks on this GPU (after the timed region, at the ramped-up
+    # clock): the bf16 matrix-core rate with every SIMD busy, and a streaming
+    # read of 2 GiB (far beyond the last-level cache).
+    measured = None
+    if not args.no_measured_peaks and bound in ("mfma", "hbm"):
+        if bound == "mfma":
+            pic.peak_mfma_bf16(64)
+            measured = max(pic.peak_mfma_bf16(256) for _ in range(3))
+        else:
+            buf = torch.empty(2 << 30, dtype=torch.uint8, device="cuda")
+            pic.peak_hbm_read(buf, buf.numel())
+            measured = max(pic.peak_hbm_read(buf, buf.numel()) for _ in range(3))
+            del buf
+            torch.cuda.empty_cache()
+
     cpu = None
     if args.cpu_budget > 0:
         cpu = cpu_baseline(cfg, wl, dw, args.cpu_budget)
@@ -301,6 +318,8 @@ def main(argv=None):
             "peak": peak,
             "unit": unit,
             "frac": round(achieved / peak, 4),
+            "measured_peak": round(measured, 1) if measured else None,
+            "measured_frac": round(achieved / measured, 4) if measured else None,
             "traffic": traffic_record(kname, cfg.name),
             "kernel_avg_us": round(kern_avg_ms * 1e3, 3),
             "launches": launches,

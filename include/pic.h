@@ -167,6 +167,19 @@ pic_status pic_debug_gather(pic_store *store, const uint64_t *ids, int32_t n, vo
 pic_status pic_prof_begin(void);
 pic_status pic_prof_end(double *kernel_ms, int64_t *launches, char *name_buf, int32_t name_len);
 
+/* Achievable peaks of this GPU, a second roofline denominator next to the
+ * spec peaks (measurement helpers, not part of the method; blocking, they
+ * synchronise `stream`, allocate and free a 512 KB scratch buffer).
+ * pic_peak_mfma_bf16: bf16 dense matrix-core rate in TFLOP/s of `iters`
+ *   rounds of four independent 32x32x16 MFMAs per wave, two waves per SIMD
+ *   on every CU (iters 1..2^22; ~4096 gives a ~10 ms run).
+ * pic_peak_hbm_read: HBM read rate in GB/s of one streaming pass over buf
+ *   (device memory, 16-byte aligned, bytes a positive multiple of 16; use a
+ *   buffer far larger than the last-level cache).
+ * Errors: INVALID, HIP. */
+pic_status pic_peak_mfma_bf16(int32_t iters, double *tflops, void *stream);
+pic_status pic_peak_hbm_read(const void *buf, int64_t bytes, double *gbs, void *stream);
+
 const char *pic_status_str(pic_status status);
 const char *pic_last_error(void);
 

@@ -22,6 +22,7 @@ SOURCES = [
     "kernels_mfma_d128.hip",
     "kernels_decode_d128.hip",
     "kernels_mla.hip",
+    "kernels_peaks.hip",
 ]
 
 # Per-file code generation flags. The MLA kernel keeps its accumulators in

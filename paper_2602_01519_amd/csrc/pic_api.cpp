@@ -10,6 +10,7 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
+#include <functional>
 #include <mutex>
 #include <string>
 #include <unordered_map>
@@ -660,6 +661,58 @@ pic_status pic_prof_end(double *kernel_ms, int64_t *launches, char *name_buf, in
   }
   for (auto &ev : g_prof.events) g_prof.spare.push_back(ev);
   g_prof.events.clear();
+  return PIC_OK;
+}
+
+// Times one launch of a peak microbenchmark on `stream` (blocking).
+static pic_status time_peak(hipStream_t st, double *ms_out,
+                            const std::function<hipError_t(float *)> &launch) {
+  float *scratch = nullptr;
+  HIP_TRY(hipMalloc(&scratch, (size_t)pic::peak_out_floats() * sizeof(float)), "hipMalloc(peak)");
+  hipEvent_t e0 = nullptr, e1 = nullptr;
+  hipError_t e = hipEventCreateWithFlags(&e0, hipEventDisableSystemFence);
+  if (e == hipSuccess) e = hipEventCreateWithFlags(&e1, hipEventDisableSystemFence);
+  if (e == hipSuccess) e = hipEventRecord(e0, st);
+  if (e == hipSuccess) e = launch(scratch);
+  if (e == hipSuccess) e = hipEventRecord(e1, st);
+  if (e == hipSuccess) e = hipEventSynchronize(e1);
+  float ms = 0.f;
+  if (e == hipSuccess) e = hipEventElapsedTime(&ms, e0, e1);
+  if (e0) (void)hipEventDestroy(e0);
+  if (e1) (void)hipEventDestroy(e1);
+  (void)hipFree(scratch);
+  if (e != hipSuccess) return hip_fail(e, "peak microbenchmark");
+  *ms_out = ms;
+  return PIC_OK;
+}
+
+pic_status pic_peak_mfma_bf16(int32_t iters, double *tflops, void *stream) {
+  if (!tflops) return fail(PIC_ERR_INVALID, "tflops is NULL");
+  if (iters <= 0 || iters > (1 << 22)) return fail(PIC_ERR_INVALID, "iters must be 1..2^22");
+  double ms = 0.0;
+  const pic_status rc = time_peak((hipStream_t)stream, &ms, [&](float *out) {
+    return pic::launch_peak_mfma(out, iters, (hipStream_t)stream);
+  });
+  if (rc != PIC_OK) return rc;
+  *tflops = ms > 0.0 ? pic::peak_mfma_flops(iters) / (ms * 1e-3) / 1e12 : 0.0;
+  return PIC_OK;
+}
+
+pic_status pic_peak_hbm_read(const void *buf, int64_t bytes, double *gbs, void *stream) {
+  if (!gbs || !buf) return fail(PIC_ERR_INVALID, "buf and gbs must not be NULL");
+  if (bytes <= 0 || bytes % 16 != 0 || (uintptr_t)buf % 16 != 0)
+    return fail(PIC_ERR_INVALID, "bytes must be a positive multiple of 16 and buf 16-byte aligned");
+  hipPointerAttribute_t at{};
+  if (hipPointerGetAttributes(&at, buf) != hipSuccess || at.type != hipMemoryTypeDevice) {
+    (void)hipGetLastError();
+    return fail(PIC_ERR_INVALID, "buf is not device memory");
+  }
+  double ms = 0.0;
+  const pic_status rc = time_peak((hipStream_t)stream, &ms, [&](float *out) {
+    return pic::launch_peak_read(buf, bytes, out, (hipStream_t)stream);
+  });
+  if (rc != PIC_OK) return rc;
+  *gbs = ms > 0.0 ? (double)bytes / (ms * 1e-3) / 1e9 : 0.0;
   return PIC_OK;
 }
 

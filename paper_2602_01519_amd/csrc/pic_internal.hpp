@@ -100,6 +100,12 @@ int decode_d128_max_rows();
 hipError_t launch_link_mla(const LinkParams &p, hipStream_t st, const char **name);
 int mla_rows_per_block();
 
+// Achievable-peak microbenchmarks (out: peak_out_floats() floats of scratch).
+int64_t peak_out_floats();
+double peak_mfma_flops(int32_t iters);
+hipError_t launch_peak_mfma(float *out, int32_t iters, hipStream_t st);
+hipError_t launch_peak_read(const void *src, int64_t bytes, float *out, hipStream_t st);
+
 // Log-sum-exp merge of split partials into out / lse.
 hipError_t launch_combine(const LinkParams &p, int dtype, hipStream_t st);
 

@@ -76,6 +76,8 @@ def lib():
             "pic_debug_gather": [vp, vp, i32, vp, vp, vp],
             "pic_prof_begin": [],
             "pic_prof_end": [vp, vp, vp, i32],
+            "pic_peak_mfma_bf16": [i32, vp, vp],
+            "pic_peak_hbm_read": [vp, i64, vp, vp],
         }
         for name, args in sig.items():
             fn = getattr(L, name)
@@ -194,6 +196,20 @@ def debug_gather(store: Store, ids, k_out, v_out, stream: Optional[int] = None):
     ids = np.ascontiguousarray(ids, dtype=np.uint64)
     _check(lib().pic_debug_gather(store.handle, ids.ctypes.data if ids.size else None, len(ids),
                                   _ptr(k_out), _ptr(v_out), stream))
+
+
+def peak_mfma_bf16(iters: int = 4096, stream: Optional[int] = None) -> float:
+    """Achievable bf16 matrix-core rate (TFLOP/s) of this GPU; blocking."""
+    out = ctypes.c_double()
+    _check(lib().pic_peak_mfma_bf16(int(iters), ctypes.byref(out), stream))
+    return out.value
+
+
+def peak_hbm_read(buf, nbytes: int, stream: Optional[int] = None) -> float:
+    """Achievable HBM read rate (GB/s) over device buffer buf; blocking."""
+    out = ctypes.c_double()
+    _check(lib().pic_peak_hbm_read(_ptr(buf), int(nbytes), ctypes.byref(out), stream))
+    return out.value
 
 
 def prof_begin():

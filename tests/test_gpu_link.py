@@ -365,3 +365,24 @@ def test_store_put_errors():
         store.lookup(99)
     assert e.value.status == pic.ERR_NOT_FOUND
     store.close()
+
+
+# ---------------------------------------------------------------------------
+# achievable-peak microbenchmarks (second roofline denominator)
+
+
+def test_peak_microbenchmarks():
+    pic.peak_mfma_bf16(16)             # the first launch includes the module load
+    tf = pic.peak_mfma_bf16(256)
+    assert 100.0 < tf < 2600.0         # below the 2.5 PF dense bf16 spec
+    buf = torch.empty(64 << 20, dtype=torch.uint8, device="cuda")
+    gbs = pic.peak_hbm_read(buf, buf.numel())
+    assert 10.0 < gbs < 1e6            # a 64 MiB pass may be served from cache
+    with pytest.raises(pic.PicError):
+        pic.peak_mfma_bf16(0)
+    with pytest.raises(pic.PicError):
+        pic.peak_hbm_read(buf, 15)
+    host = np.zeros(1024, np.uint8)
+    with pytest.raises(pic.PicError):
+        pic.peak_hbm_read(host, host.nbytes)
+
