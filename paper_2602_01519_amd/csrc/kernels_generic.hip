@@ -399,41 +399,86 @@ __global__ __launch_bounds__(256) void link_valu_kernel(LinkParams p) {
 }
 
 // ---------------------------------------------------------------------------
-// Split-K combine: one wave per output row.
-//   M = max_s m_s,  w_s = 2^(m_s - M),  L = sum_s w_s l_s,
-//   out = sum_s w_s o_s / L,  lse = (M + log2 L) ln 2.
+// Split-K combine: one wave per output row. Lane j covers value dims
+// 2j, 2j+1 of every 128-wide chunk (8-byte loads, a row's partials of one
+// split are one coalesced 512-byte read per chunk). The partial outputs of
+// the first kPre splits are loaded before the split maxima are reduced, so
+// a row costs one memory round trip rather than two; each split's weight
+// exp2(m_s - M) is computed once (lane s) and broadcast with readlane.
+// Every (split, row) partial is written by the attention kernels (zeros with
+// m = -inf for an empty split), so the loads need no guard.
 template <typename T>
 __global__ __launch_bounds__(256) void combine_kernel(LinkParams p) {
+  constexpr int kPre = 8;
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  const int64_t total_rows = (int64_t)p.total_q * p.n_q_heads;
+  const int64_t rows = (int64_t)p.total_q * p.n_q_heads;
   const int64_t orow = (int64_t)blockIdx.x * 4 + wave;
-  if (orow >= total_rows) return;
-  const int S = p.num_splits;
-  float M = -INFINITY;
-  for (int s = lane; s < S; s += 64) M = fmaxf(M, p.part_m[s * total_rows + orow]);
+  if (orow >= rows) return;
+  const int S = p.num_splits, dv = p.d_v;
+  const int nchunk = (dv + 127) / 128;
+  auto po = [&](int s, int e) {
+    return *(const float2 *)(p.part_o + (s * rows + orow) * dv + e);
+  };
+  // prefetch: chunk 0 of the first kPre splits
+  const int e0 = 2 * lane;
+  float2 pre[kPre];
+#pragma unroll
+  for (int s = 0; s < kPre; ++s)
+    pre[s] = (s < S && e0 < dv) ? po(s, e0) : make_float2(0.f, 0.f);
+  // split maxima and weights: lane l holds splits l, l + 64, l + 128, l + 192
+  float ms[4], ls[4], M = -INFINITY;
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const int sj = lane + 64 * j;
+    ms[j] = sj < S ? p.part_m[sj * rows + orow] : -INFINITY;
+    ls[j] = sj < S ? p.part_l[sj * rows + orow] : 0.f;
+    M = fmaxf(M, ms[j]);
+  }
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) M = fmaxf(M, __shfl_xor(M, o));
-  T *out = (T *)p.out + orow * p.d_v;
+  T *out = (T *)p.out + orow * dv;
   if (M == -INFINITY) {
-    for (int e = lane; e < p.d_v; e += 64) out[e] = from_f32<T>(0.f);
+    for (int e = lane; e < dv; e += 64) out[e] = from_f32<T>(0.f);
     if (p.lse && lane == 0) p.lse[orow] = -INFINITY;
     return;
   }
-  float L = 0.f;
-  for (int s = lane; s < S; s += 64) {
-    const float ms = p.part_m[s * total_rows + orow];
-    if (ms != -INFINITY) L += exp2f(ms - M) * p.part_l[s * total_rows + orow];
+  float w[4], L = 0.f;
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const int sj = lane + 64 * j;
+    w[j] = ms[j] == -INFINITY ? 0.f : exp2f(ms[j] - M);
+    if (sj < S) L += w[j] * ls[j];
   }
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) L += __shfl_xor(L, o);
   const float inv = 1.f / L;
-  for (int e = lane; e < p.d_v; e += 64) {
-    float a = 0.f;
-    for (int s = 0; s < S; ++s) {
-      const float ms = p.part_m[s * total_rows + orow];
-      if (ms != -INFINITY) a += exp2f(ms - M) * p.part_o[(s * total_rows + orow) * p.d_v + e];
+  auto weight = [&](int s) {   // s is uniform
+    const float wj = s < 64 ? w[0] : s < 128 ? w[1] : s < 192 ? w[2] : w[3];
+    return __builtin_amdgcn_readlane(__float_as_int(wj), s & 63);
+  };
+  for (int c = 0; c < nchunk; ++c) {
+    const int e = 128 * c + e0;
+    float ax = 0.f, ay = 0.f;
+#pragma unroll
+    for (int s = 0; s < kPre; ++s) {
+      if (s >= S) break;
+      const float ws = __int_as_float(weight(s));
+      const float2 v = c == 0 ? pre[s] : (e < dv ? po(s, e) : make_float2(0.f, 0.f));
+      ax += ws * v.x;
+      ay += ws * v.y;
     }
-    out[e] = from_f32<T>(a * inv);
+    for (int s = kPre; s < S; ++s) {
+      const float ws = __int_as_float(weight(s));
+      if (e < dv) {
+        const float2 v = po(s, e);
+        ax += ws * v.x;
+        ay += ws * v.y;
+      }
+    }
+    if (e < dv) {
+      out[e] = from_f32<T>(ax * inv);
+      out[e + 1] = from_f32<T>(ay * inv);
+    }
   }
   if (p.lse && lane == 0) p.lse[orow] = (M + log2f(L)) * 0.69314718055994531f;
 }
