@@ -281,8 +281,8 @@ struct TableLayout {
   size_t off_r, off_o, bytes;
 };
 
-pic_status upload(pic_store *s, const Plan &P, hipStream_t st, bool copy, Stage **stage,
-                  LinkParams &lp, TableLayout &tl) {
+pic_status upload(pic_store *s, const Plan &P, hipStream_t st, Stage **stage, LinkParams &lp,
+                  TableLayout &tl) {
   const size_t nl = P.links.size(), nr = P.reqs.size();
   tl.off_r = round_up(sizeof(LinkEntry) * nl, 256);
   tl.off_o = tl.off_r + round_up(sizeof(ReqEntry) * nr, 256);
@@ -294,9 +294,8 @@ pic_status upload(pic_store *s, const Plan &P, hipStream_t st, bool copy, Stage 
   if (nl) memcpy(h, P.links.data(), sizeof(LinkEntry) * nl);
   memcpy(h + off_r, P.reqs.data(), sizeof(ReqEntry) * nr);
   memcpy(h + off_o, P.order.data(), sizeof(int32_t) * nr);
-  if (copy)
-    HIP_TRY(hipMemcpyAsync((*stage)->dev, h, bytes, hipMemcpyHostToDevice, st),
-            "hipMemcpyAsync(table)");
+  HIP_TRY(launch_table_copy((*stage)->host_dev, (*stage)->dev, (int64_t)bytes, st),
+          "table_copy_kernel");
   char *dv = (char *)(*stage)->dev;
   lp.links = (const LinkEntry *)dv;
   lp.reqs = (const ReqEntry *)(dv + off_r);
@@ -436,7 +435,7 @@ pic_status link_call(pic_store *s, const pic_link_req *req, int32_t n_q_heads, c
   if (!dg.ok) return fail(PIC_ERR_HIP, "cannot select the store's device");
   Stage *stage = nullptr;
   TableLayout tl;
-  rc = upload(s, P, st, true, &stage, lp, tl);
+  rc = upload(s, P, st, &stage, lp, tl);
   if (rc != PIC_OK) return rc;
 
   if (P.max_own_lp > 0) {
@@ -625,8 +624,8 @@ pic_status pic_debug_gather(pic_store *s, const uint64_t *ids, int32_t n, void *
   pic_status rc = stage_acquire(s, sizeof(LinkEntry) * n, &stage);
   if (rc != PIC_OK) return rc;
   memcpy(stage->host, links.data(), sizeof(LinkEntry) * n);
-  HIP_TRY(hipMemcpyAsync(stage->dev, stage->host, sizeof(LinkEntry) * n, hipMemcpyHostToDevice, st),
-          "hipMemcpyAsync(gather table)");
+  HIP_TRY(launch_table_copy(stage->host_dev, stage->dev, (int64_t)(sizeof(LinkEntry) * n), st),
+          "table_copy_kernel");
   const pic_store_desc &d = s->desc;
   hipError_t e = launch_gather((const LinkEntry *)stage->dev, n, toks, d.n_kv_heads,
                                d.d_k, d.d_v, !gqa, s->esz, k_out, v_out, st);

@@ -75,6 +75,9 @@ hipError_t launch_gather(const LinkEntry *links, int32_t n_links, int64_t total_
                          int32_t heads, int32_t d_k, int32_t d_v, int32_t mla, int32_t esz,
                          void *k_out, void *v_out, hipStream_t st);
 
+// Copies bytes (a multiple of 16) from a host-mapped buffer to the device.
+hipError_t launch_table_copy(const void *src, void *dst, int64_t bytes, hipStream_t st);
+
 // Lays each request's own KV (token-major k_self / v_self) out like a chunk
 // slot at its own link (the request's last link), zero-padded to lp.
 hipError_t launch_prep_own(const LinkParams &p, int32_t mla, int32_t esz, int32_t max_own_lp,
