@@ -393,23 +393,27 @@ pic_status link_call(pic_store *s, const pic_link_req *req, int32_t n_q_heads, c
       splits = (int32_t)std::max<int64_t>(1, std::min<int64_t>((2048 + blocks - 1) / blocks, 256));
       splits = std::min(splits, std::max(1, P.max_tiles));
     }
-  } else if (kern == K::Mfma128 || kern == K::Mla) {
-    // Short queries over long documents (the regime the paper targets: a
-    // few dozen dynamic tokens after thousands of cached ones) leave one
-    // row block per (request, kv head), and the longest request sets the
-    // kernel time. Split every request's key range so that its longest
-    // piece is no longer than the average work per resident workgroup of
-    // the GPU (256 CUs times the kernel's workgroups per CU), with >= 8
-    // tiles per piece and at most 16 pieces.
-    const int64_t slots = 256 * (kern == K::Mla ? 1 : mfma_d128_blocks_per_cu());
+  } else {
+    // Few row blocks per call -- short queries over long documents (the
+    // regime the paper targets: a few dozen dynamic tokens after thousands
+    // of cached ones), or a single small request -- leave most CUs idle and
+    // let the longest request set the kernel time. Split every request's
+    // key range so that its longest piece is no longer than the average work
+    // per resident workgroup of the GPU (256 CUs times the kernel's
+    // workgroups per CU), with a minimum piece (8 tiles for the matrix-core
+    // kernels, 1 for the vector-ALU kernel, whose tiles are slow) and at
+    // most 16 pieces.
+    const int64_t per_cu = kern == K::Mla ? 1 : kern == K::Mfma128 ? mfma_d128_blocks_per_cu() : 4;
+    const int min_piece = kern == K::Valu ? 1 : 8;
+    const int64_t slots = 256 * per_cu;
     int64_t work = 0;   // tiles summed over all non-empty workgroups
     for (const ReqEntry &R : P.reqs) {
       const int64_t rows = (int64_t)R.lq * lp.group;
       work += (int64_t)d.n_kv_heads * ((rows + rows_per_block - 1) / rows_per_block) * R.tiles;
     }
-    const int64_t per_slot = std::max<int64_t>(8, (work + slots - 1) / slots);
+    const int64_t per_slot = std::max<int64_t>(min_piece, (work + slots - 1) / slots);
     splits = (int32_t)std::min<int64_t>(16, (P.max_tiles + per_slot - 1) / per_slot);
-    splits = std::max(1, std::min(splits, P.max_tiles / 8));
+    splits = std::max(1, std::min(splits, P.max_tiles / min_piece));
   }
   lp.num_splits = splits;
   // Workspace: [own KV slots, laid out like chunk slots][split partials].
