@@ -5,6 +5,7 @@ mean-abs <= 2e-3 over the compared outputs; fp32 inputs max-abs and mean-abs
 <= 1e-4. The log-sum-exp is compared to 2e-3 (bf16) / 1e-4 (fp32) absolute.
 The gather hook must be bit-exact.
 """
+import dataclasses
 import math
 
 import numpy as np
@@ -39,8 +40,17 @@ def compare(cfg, out, lse, ref, ref_lse, sel=None, label=""):
         assert np.abs(lse[fin] - ref_lse[fin]).max() <= lse_tol, f"{label}: lse err"
 
 
-def run_and_check(cfg, decode=None, num_splits=0, requests=None):
+def run_and_check(cfg, decode=None, num_splits=0, requests=None, links=None):
+    """links: optional per-request lists of store chunk indices replacing the
+    seeded plan's links (duplicates and empty lists allowed)."""
     wl = W.make_workload(cfg)
+    if links is not None:
+        assert len(links) == cfg.batch
+        offs = np.zeros(cfg.batch + 1, np.int32)
+        offs[1:] = np.cumsum([len(l) for l in links])
+        idx = np.array([c for l in links for c in l], dtype=np.int64)
+        wl = dataclasses.replace(wl, plan=dataclasses.replace(wl.plan, chunk_offsets=offs,
+                                                              chunk_index=idx))
     keep = None
     sel = None
     if requests is not None:
@@ -160,6 +170,44 @@ def test_small_parity(name):
     run_and_check(SMALL[name])
 
 
+# Degenerate requests in one batch: a duplicated link, a request with no
+# query rows, one with own KV only (no links), one linking every chunk.
+DEGENERATE_LINKS = [[2, 0, 2], [1, 3], [], [0, 1, 2, 3], [3, 3]]
+
+
+def _degenerate(kind, dtype=W.BF16):
+    common = dict(chunk_lens=(70, 64, 1, 130), batch=5, q_len=(5, 0, 7, 3, 9),
+                  self_len=(5, 0, 9, 3, 70), seed=13, links=(0, 0))
+    if kind == W.MLA:
+        return W.small_config("degenerate_mla", kind=W.MLA, n_q_heads=16, d_k=576, d_v=512,
+                              q_std=1.0, scale=1 / math.sqrt(192), **common)
+    if dtype == W.F32:
+        return W.small_config("degenerate_f32", dtype=W.F32, d_k=64, **common)
+    return W.small_config("degenerate_gqa", d_k=128, **common)
+
+
+@pytest.mark.parametrize("case", ["gqa", "mla", "f32"])
+def test_degenerate_requests(case):
+    cfg = _degenerate(W.MLA if case == "mla" else W.GQA, W.F32 if case == "f32" else W.BF16)
+    run_and_check(cfg, links=DEGENERATE_LINKS)
+
+
+@pytest.mark.parametrize("case", ["gqa", "mla"])
+def test_empty_key_sets(case):
+    """Cross-only attention with a request that links nothing: its rows see no
+    key at all (out = 0, lse = -inf)."""
+    kw = dict(chunk_lens=(70, 64, 129), batch=3, q_len=(4, 6, 2), self_len=None, links=(0, 0))
+    if case == "mla":
+        cfg = W.small_config("empty_keys_mla", kind=W.MLA, n_q_heads=16, d_k=576, d_v=512,
+                             q_std=1.0, scale=1 / math.sqrt(192), **kw)
+    else:
+        cfg = W.small_config("empty_keys_gqa", d_k=128, **kw)
+    out, lse = run_and_check(cfg, links=[[0, 2], [], [1]])
+    rows = slice(4, 10)
+    assert np.all(out[rows] == 0)
+    assert np.all(np.isneginf(lse[rows]))
+
+
 def _many_links(kind):
     rng = np.random.default_rng(5)
     lens = tuple(int(x) for x in rng.integers(1, 90, size=60))
@@ -182,7 +230,7 @@ DECODE = W.small_config("decode_small", d_k=128, n_q_heads=32, n_kv_heads=8,
                         self_len=(128, 1, 65, 3, 200), decode=True)
 
 
-@pytest.mark.parametrize("splits", [1, 2, 7, 0])
+@pytest.mark.parametrize("splits", [1, 2, 7, 0, 256])
 def test_decode_splits(splits):
     run_and_check(DECODE, decode=True, num_splits=splits)
 
