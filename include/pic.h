@@ -60,36 +60,43 @@ typedef enum {
 enum { PIC_F32 = 0, PIC_BF16 = 1 };     /* pic_store_desc.dtype */
 enum { PIC_GQA = 0, PIC_MLA = 1 };      /* pic_store_desc.kind  */
 
-/* Shape of one layer's chunk caches. d_k and d_v must be multiples of 8.
+/* Shape of a store's chunk caches. d_k and d_v must be multiples of 8.
  * GQA: n_kv_heads >= 1, separate K [.., d_k] and V [.., d_v] per head.
  * MLA: n_kv_heads == 1, d_v <= d_k, the value is the first d_v of each key row.
- * capacity_tokens: pool size in tokens. Each chunk occupies its length
- * rounded up to a multiple of 64 tokens. */
+ * n_layers: cross-attention layers per chunk, 0 or 1 for one. Comb
+ *   interleaves L_cross cross-attention layers with the decoder (Sec. 4.2
+ *   and 4.3, Fig. 3: 8 among 32 decoder layers; Eq. 12), and each reads its
+ *   own K and V of every document; a chunk's caches of all layers are put
+ *   together and each link call names its layer.
+ * capacity_tokens: pool size in tokens per layer. Each chunk occupies its
+ * length rounded up to a multiple of 64 tokens in every layer. */
 typedef struct pic_store_desc {
   int32_t kind;
   int32_t dtype;
   int32_t n_kv_heads;
   int32_t d_k;
   int32_t d_v;
-  int32_t reserved;          /* must be 0 */
+  int32_t n_layers;          /* 0..256; 0 and 1 both mean one layer */
   int64_t capacity_tokens;
 } pic_store_desc;
 
 typedef struct pic_store pic_store;
 
 /* Creates a chunk store on the current HIP device and reserves its pool
- * (the PIC allocator's reservation, Sec. 5.3). *out receives the handle.
+ * (the PIC allocator's reservation, Sec. 5.3): capacity_tokens per layer.
+ * *out receives the handle.
  * Errors: INVALID (desc), UNSUPPORTED (shape), HIP (allocation failed). */
 pic_status pic_store_create(const pic_store_desc *desc, pic_store **out);
 
 /* Waits for the device, then frees the store and everything it owns.
- * NULL is accepted and ignored. */
+ * NULL is accepted and ignored. Errors: INVALID while link plans of the
+ * store are alive (destroy them first). */
 pic_status pic_store_destroy(pic_store *store);
 
 /* Compile-stage entry (Sec. 3 steps 3-4): copies one chunk's caches into the
  * pool and records chunk_id -> slot in the store's hash table.
- *   k: device, token-major [n_tokens][n_kv_heads][d_k]
- *   v: device, token-major [n_tokens][n_kv_heads][d_v] for GQA; NULL for MLA
+ *   k: device, [n_layers][n_tokens][n_kv_heads][d_k] (token-major per layer)
+ *   v: device, [n_layers][n_tokens][n_kv_heads][d_v] for GQA; NULL for MLA
  * The copy (into the store's internal layout) is ordered on `stream`; the
  * caller may reuse k and v once the stream has passed it.
  * Errors: INVALID, EXISTS (id present), OOM (pool full), HIP. */
@@ -114,7 +121,7 @@ pic_status pic_store_usage(const pic_store *store, int64_t *used_tokens,
  *     cross-attention only (no own KV, every row sees only the documents). */
 typedef struct pic_link_req {
   int32_t batch;
-  int32_t reserved;          /* must be 0 */
+  int32_t layer;             /* the store layer whose chunk caches are read (0 for one layer) */
   const int32_t *chunk_offsets;
   const uint64_t *chunk_ids;
   const int32_t *q_offsets;
@@ -151,13 +158,43 @@ pic_status pic_link_decode(pic_store *store, const pic_link_req *req, int32_t n_
                            float softmax_scale, int32_t num_splits, void *out, float *lse,
                            void *stream);
 
+/* A request batch resolved once for repeated calls. Comb runs the same
+ * links in each of its cross-attention layers and again at every decode
+ * step (generated tokens attend to the same documents, Sec. 4 and Eq. 12);
+ * a plan looks the chunk ids up, chooses kernel and splits, and puts the
+ * link tables of every layer and the call's workspace on the device once,
+ * so that a run enqueues kernels only: no host-side lookup, no copy, no
+ * allocation.
+ * pic_link_plan_create: req as for pic_link_attn (req->layer must be 0);
+ *   mode PIC_PREFILL (num_splits must be 0) computes as pic_link_attn,
+ *   PIC_DECODE as pic_link_decode with the given num_splits (0 = auto).
+ *   Blocking: copies the tables to the device before returning. The plan
+ *   keeps no pointer into req; the store must outlive it
+ *   (pic_store_destroy refuses while plans are alive).
+ * pic_link_plan_run: one call of the planned batch on cross-attention layer
+ *   `layer`, with tensors as for pic_link_attn (sizes from the plan's
+ *   offsets). Runs of one plan share its workspace: enqueue them on one
+ *   stream, or order them.
+ * pic_link_plan_destroy: waits for the device and frees the plan; NULL is
+ *   ignored.
+ * Errors: INVALID, NOT_FOUND, UNSUPPORTED, OOM, HIP. */
+enum { PIC_PREFILL = 0, PIC_DECODE = 1 };   /* pic_link_plan_create mode */
+typedef struct pic_link_plan pic_link_plan;
+pic_status pic_link_plan_create(pic_store *store, const pic_link_req *req, int32_t n_q_heads,
+                                int32_t mode, int32_t num_splits, pic_link_plan **out);
+pic_status pic_link_plan_run(pic_link_plan *plan, int32_t layer, const void *q,
+                             const void *k_self, const void *v_self, float softmax_scale,
+                             void *out, float *lse, void *stream);
+pic_status pic_link_plan_destroy(pic_link_plan *plan);
+
 /* Test hook: materialises the concatenation (Sec. 4.2) of the listed chunks
- * in the given order, reading the pool through the same address resolution
- * the attention kernels use. k_out: device token-major [sum len][H_kv][d_k];
- * v_out: device [sum len][H_kv][d_v] (GQA) or NULL (MLA). Bit-exact copies.
+ * of one layer, in the given order, reading the pool through the same
+ * address resolution the attention kernels use. k_out: device token-major
+ * [sum len][H_kv][d_k]; v_out: device [sum len][H_kv][d_v] (GQA) or NULL
+ * (MLA). Bit-exact copies.
  * Errors: INVALID, NOT_FOUND, HIP. */
-pic_status pic_debug_gather(pic_store *store, const uint64_t *ids, int32_t n, void *k_out,
-                            void *v_out, void *stream);
+pic_status pic_debug_gather(pic_store *store, const uint64_t *ids, int32_t n, int32_t layer,
+                            void *k_out, void *v_out, void *stream);
 
 /* Kernel timing for measurement. pic_prof_begin() clears and enables
  * recording of HIP events around every launch of the main attention kernel;

@@ -103,6 +103,9 @@ struct pic_store {
   char *pool = nullptr;
   int64_t capacity = 0;          // padded tokens
   int64_t used = 0;
+  int32_t n_layers = 1;
+  int64_t layer_bytes = 0;       // bytes of one layer's pool; layer l of a slot is l * layer_bytes on
+  int64_t live_plans = 0;
   int64_t k_tok_elems = 0;       // K elements per padded token (all heads)
   int64_t v_tok_elems = 0;       // V elements per padded token (GQA)
   std::unordered_map<uint64_t, Slot> map;
@@ -174,14 +177,33 @@ struct Plan {
   int32_t total_q = 0;
   int32_t max_rows = 0;          // max over requests of lq * group
   int32_t max_tiles = 0;
+  bool self = false;             // requests carry own KV
+  int64_t total_self = 0;        // own tokens over the batch
 };
 
-pic_status plan_call(pic_store *s, const pic_link_req *req, int32_t n_q_heads, const void *q,
-                     const void *k_self, const void *v_self, float scale, void *out,
-                     int32_t max_q_per_req, Plan &P) {
+// Tensor arguments of a call against its plan.
+pic_status check_tensors(const pic_store *s, const Plan &P, const void *q, const void *k_self,
+                         const void *v_self, const void *out) {
+  if (P.total_q > 0 && (!q || !out)) return fail(PIC_ERR_INVALID, "q/out is NULL");
+  if (P.self) {
+    if (P.total_self > 0 && !k_self) return fail(PIC_ERR_INVALID, "k_self is NULL");
+    if (s->desc.kind == PIC_GQA && P.total_self > 0 && !v_self)
+      return fail(PIC_ERR_INVALID, "v_self is NULL");
+    if (s->desc.kind == PIC_MLA && v_self) return fail(PIC_ERR_INVALID, "v_self must be NULL for MLA");
+  } else if (k_self || v_self) {
+    return fail(PIC_ERR_INVALID, "k_self/v_self given without self_offsets");
+  }
+  return PIC_OK;
+}
+
+// Validates a request batch and resolves its chunk ids into the link and
+// request tables, with chunk addresses in cross-attention layer `layer`.
+pic_status plan_call(pic_store *s, const pic_link_req *req, int32_t n_q_heads, float scale,
+                     int32_t layer, int32_t max_q_per_req, Plan &P) {
   if (!s) return fail(PIC_ERR_INVALID, "store is NULL");
   if (!req) return fail(PIC_ERR_INVALID, "req is NULL");
-  if (req->reserved != 0) return fail(PIC_ERR_INVALID, "req->reserved must be 0");
+  if (layer < 0 || layer >= s->n_layers)
+    return fail(PIC_ERR_INVALID, "layer %d outside the store's %d layers", layer, s->n_layers);
   const pic_store_desc &d = s->desc;
   const int32_t B = req->batch;
   if (B < 0) return fail(PIC_ERR_INVALID, "batch < 0");
@@ -199,15 +221,9 @@ pic_status plan_call(pic_store *s, const pic_link_req *req, int32_t n_q_heads, c
   const int64_t tq = req->q_offsets[B];
   const int64_t ts = self ? req->self_offsets[B] : 0;
   if (n_links > 0 && !req->chunk_ids) return fail(PIC_ERR_INVALID, "chunk_ids is NULL");
-  if (tq > 0 && (!q || !out)) return fail(PIC_ERR_INVALID, "q/out is NULL");
   if (tq * n_q_heads > INT32_MAX / 2) return fail(PIC_ERR_INVALID, "too many query rows");
-  if (self) {
-    if (ts > 0 && !k_self) return fail(PIC_ERR_INVALID, "k_self is NULL");
-    if (d.kind == PIC_GQA && ts > 0 && !v_self) return fail(PIC_ERR_INVALID, "v_self is NULL");
-    if (d.kind == PIC_MLA && v_self) return fail(PIC_ERR_INVALID, "v_self must be NULL for MLA");
-  } else if (k_self || v_self) {
-    return fail(PIC_ERR_INVALID, "k_self/v_self given without self_offsets");
-  }
+  P.self = self;
+  P.total_self = ts;
   const int group = n_q_heads / d.n_kv_heads;
   const int64_t slot_tok_bytes = (s->k_tok_elems + s->v_tok_elems) * s->esz;
   P.links.clear();
@@ -237,7 +253,7 @@ pic_status plan_call(pic_store *s, const pic_link_req *req, int32_t n_q_heads, c
                     c, (unsigned long long)id);
       const Slot &sl = it->second;
       LinkEntry E;
-      E.k = s->pool + sl.off_tokens * slot_tok_bytes;
+      E.k = s->pool + (int64_t)layer * s->layer_bytes + sl.off_tokens * slot_tok_bytes;
       E.v = d.kind == PIC_GQA ? (const char *)E.k + (int64_t)sl.lp * s->k_tok_elems * s->esz : E.k;
       E.len = (int32_t)sl.len;
       E.lp = sl.lp;
@@ -329,27 +345,31 @@ void prof_stop(hipStream_t st, std::pair<hipEvent_t, hipEvent_t> *ev, const char
 }
 
 enum class Mode { Prefill, Decode };
+enum class Kern { Valu, Mfma128, Decode128, Mla };
 
-pic_status link_call(pic_store *s, const pic_link_req *req, int32_t n_q_heads, const void *q,
-                     const void *k_self, const void *v_self, float scale, int32_t num_splits,
-                     void *out, float *lse, void *stream, Mode mode) {
+// Everything about a call that does not depend on its tensors: the resolved
+// tables, the kernel, the split count and the workspace layout
+// [own KV slots, laid out like chunk slots][split partials].
+struct Setup {
+  Plan P;
+  Kern kern = Kern::Valu;
+  int32_t splits = 1;
+  LinkParams lp{};               // shapes only: no tables, tensors or scale yet
+  size_t part_off = 0, part_bytes = 0;
+  size_t work_bytes() const { return part_off + part_bytes; }
+};
+
+pic_status setup_call(pic_store *s, const pic_link_req *req, int32_t n_q_heads, float scale,
+                      int32_t layer, int32_t num_splits, Mode mode, Setup &C) {
   if (mode == Mode::Decode && (num_splits < 0 || num_splits > 256))
     return fail(PIC_ERR_INVALID, "num_splits must be 0..256");
-  Plan P;
-  pic_status rc = plan_call(s, req, n_q_heads, q, k_self, v_self, scale, out,
+  Plan &P = C.P;
+  pic_status rc = plan_call(s, req, n_q_heads, scale, layer,
                             mode == Mode::Decode ? 16 : INT32_MAX, P);
   if (rc != PIC_OK) return rc;
-  if (req->batch == 0 || P.total_q == 0) return PIC_OK;
   const pic_store_desc &d = s->desc;
   const bool mla = d.kind == PIC_MLA;
-  const hipStream_t st = (hipStream_t)stream;
-
-  LinkParams lp{};
-  lp.q = q;
-  lp.k_self = k_self;
-  lp.v_self = v_self;
-  lp.out = out;
-  lp.lse = lse;
+  LinkParams &lp = C.lp;
   lp.batch = req->batch;
   lp.n_q_heads = n_q_heads;
   lp.n_kv_heads = d.n_kv_heads;
@@ -357,7 +377,7 @@ pic_status link_call(pic_store *s, const pic_link_req *req, int32_t n_q_heads, c
   lp.d_k = d.d_k;
   lp.d_v = d.d_v;
   lp.total_q = P.total_q;
-  lp.scale_log2 = scale * 1.4426950408889634f;
+  if (req->batch == 0 || P.total_q == 0) return PIC_OK;
 
   // Kernel choice.
   //   bf16 GQA d=128: decode-shaped calls with at most 16 rows per (request,
@@ -366,21 +386,23 @@ pic_status link_call(pic_store *s, const pic_link_req *req, int32_t n_q_heads, c
   //   Other shapes / fp32 / MLA: the generic vector-ALU kernel.
   //   bf16 MLA with 576-wide latent rows and 512-wide values: the MLA
   //   matrix-core kernel (split when decoding).
-  enum class K { Valu, Mfma128, Decode128, Mla } kern = K::Valu;
+  Kern kern = Kern::Valu;
   const bool bf16_128 = d.dtype == PIC_BF16 && !mla && d.d_k == 128 && d.d_v == 128;
   if (bf16_128)
-    kern = mode == Mode::Decode && P.max_rows <= decode_d128_max_rows() ? K::Decode128 : K::Mfma128;
-  if (d.dtype == PIC_BF16 && mla && d.d_k == 576 && d.d_v == 512) kern = K::Mla;
-  if (kern == K::Valu && valu_lds_bytes_for(s->esz, mla, d.d_k, d.d_v) > 160 * 1024)
+    kern = mode == Mode::Decode && P.max_rows <= decode_d128_max_rows() ? Kern::Decode128
+                                                                         : Kern::Mfma128;
+  if (d.dtype == PIC_BF16 && mla && d.d_k == 576 && d.d_v == 512) kern = Kern::Mla;
+  if (kern == Kern::Valu && valu_lds_bytes_for(s->esz, mla, d.d_k, d.d_v) > 160 * 1024)
     return fail(PIC_ERR_UNSUPPORTED, "head widths d_k=%d d_v=%d exceed the generic kernel's LDS",
                 d.d_k, d.d_v);
-  const int rows_per_block = kern == K::Mfma128   ? mfma_d128_rows_per_block()
-                             : kern == K::Valu    ? valu_rows_per_block()
-                             : kern == K::Mla     ? mla_rows_per_block()
-                                                  : decode_d128_max_rows();
+  C.kern = kern;
+  const int rows_per_block = kern == Kern::Mfma128 ? mfma_d128_rows_per_block()
+                             : kern == Kern::Valu  ? valu_rows_per_block()
+                             : kern == Kern::Mla   ? mla_rows_per_block()
+                                                   : decode_d128_max_rows();
   lp.nrb = std::max(1, (P.max_rows + rows_per_block - 1) / rows_per_block);
   lp.n_groups = req->batch * d.n_kv_heads;
-  if (kern == K::Mfma128) lp.n_groups = (int32_t)round_up(lp.n_groups, 8);
+  if (kern == Kern::Mfma128) lp.n_groups = (int32_t)round_up(lp.n_groups, 8);
 
   int32_t splits = 1;
   const int64_t blocks = (int64_t)req->batch * d.n_kv_heads * lp.nrb;
@@ -403,8 +425,9 @@ pic_status link_call(pic_store *s, const pic_link_req *req, int32_t n_q_heads, c
     // workgroups per CU), with a minimum piece (8 tiles for the matrix-core
     // kernels, 1 for the vector-ALU kernel, whose tiles are slow) and at
     // most 16 pieces.
-    const int64_t per_cu = kern == K::Mla ? 1 : kern == K::Mfma128 ? mfma_d128_blocks_per_cu() : 4;
-    const int min_piece = kern == K::Valu ? 1 : 8;
+    const int64_t per_cu =
+        kern == Kern::Mla ? 1 : kern == Kern::Mfma128 ? mfma_d128_blocks_per_cu() : 4;
+    const int min_piece = kern == Kern::Valu ? 1 : 8;
     const int64_t slots = 256 * per_cu;
     int64_t work = 0;   // tiles summed over all non-empty workgroups
     for (const ReqEntry &R : P.reqs) {
@@ -415,61 +438,113 @@ pic_status link_call(pic_store *s, const pic_link_req *req, int32_t n_q_heads, c
     splits = (int32_t)std::min<int64_t>(16, (P.max_tiles + per_slot - 1) / per_slot);
     splits = std::max(1, std::min(splits, P.max_tiles / min_piece));
   }
+  C.splits = splits;
   lp.num_splits = splits;
-  // Workspace: [own KV slots, laid out like chunk slots][split partials].
   const size_t rows = (size_t)P.total_q * n_q_heads;
-  const size_t part_off = round_up(P.own_bytes, 256);
-  const size_t part_bytes = splits > 1 ? rows * splits * (d.d_v + 2) * sizeof(float) : 0;
-  if (part_off + part_bytes > 0) {
-    rc = ensure_work(s, part_off + part_bytes);
-    if (rc != PIC_OK) return rc;
-  }
+  C.part_off = round_up(P.own_bytes, 256);
+  C.part_bytes = splits > 1 ? rows * splits * (d.d_v + 2) * sizeof(float) : 0;
+  return PIC_OK;
+}
+
+// Points the own-KV links of `links` (the plan's tables) at their slots in
+// the workspace `work`.
+void place_own(const pic_store *s, const Plan &P, void *work, LinkEntry *links) {
+  const bool mla = s->desc.kind == PIC_MLA;
   for (auto &o : P.own) {
-    LinkEntry &E = P.links[o.first];
-    E.k = (char *)s->work + o.second;
+    LinkEntry &E = links[o.first];
+    E.k = (char *)work + o.second;
     E.v = mla ? E.k : (const char *)E.k + (int64_t)E.lp * s->k_tok_elems * s->esz;
   }
-  if (splits > 1) {
-    lp.part_o = (float *)((char *)s->work + part_off);
-    lp.part_m = lp.part_o + rows * splits * d.d_v;
-    lp.part_l = lp.part_m + rows * splits;
+}
+
+// Enqueues a call whose tables are already on the device (lp.links, reqs,
+// order set): own-KV staging, the attention kernel, the split combine.
+pic_status launch_call(const pic_store *s, const Setup &C, LinkParams lp, void *work,
+                       const void *q, const void *k_self, const void *v_self, float scale,
+                       void *out, float *lse, hipStream_t st) {
+  const pic_store_desc &d = s->desc;
+  const bool mla = d.kind == PIC_MLA;
+  lp.q = q;
+  lp.k_self = k_self;
+  lp.v_self = v_self;
+  lp.out = out;
+  lp.lse = lse;
+  lp.scale_log2 = scale * 1.4426950408889634f;
+  if (C.splits > 1) {
+    const size_t rows = (size_t)C.P.total_q * lp.n_q_heads;
+    lp.part_o = (float *)((char *)work + C.part_off);
+    lp.part_m = lp.part_o + rows * C.splits * d.d_v;
+    lp.part_l = lp.part_m + rows * C.splits;
   }
-
-  DeviceGuard dg(s->device);
-  if (!dg.ok) return fail(PIC_ERR_HIP, "cannot select the store's device");
-  Stage *stage = nullptr;
-  TableLayout tl;
-  rc = upload(s, P, st, &stage, lp, tl);
-  if (rc != PIC_OK) return rc;
-
-  if (P.max_own_lp > 0) {
-    hipError_t e = launch_prep_own(lp, mla, s->esz, P.max_own_lp, st);
+  if (C.P.max_own_lp > 0) {
+    hipError_t e = launch_prep_own(lp, mla, s->esz, C.P.max_own_lp, st);
     if (e != hipSuccess) return hip_fail(e, "prep_own kernels");
   }
   std::pair<hipEvent_t, hipEvent_t> ev;
   const char *name = "";
   prof_start(st, &ev);
   hipError_t e;
-  if (kern == K::Decode128)
+  if (C.kern == Kern::Decode128)
     e = launch_link_decode_d128(lp, st, &name);
-  else if (kern == K::Mla)
+  else if (C.kern == Kern::Mla)
     e = launch_link_mla(lp, st, &name);
-  else if (kern == K::Mfma128)
+  else if (C.kern == Kern::Mfma128)
     e = launch_link_mfma_d128(lp, st, &name);
   else
     e = launch_link_valu(lp, d.dtype, mla, st, &name);
   prof_stop(st, &ev, name);
   if (e != hipSuccess) return hip_fail(e, name);
-  if (splits > 1) {
+  if (C.splits > 1) {
     e = launch_combine(lp, d.dtype, st);
     if (e != hipSuccess) return hip_fail(e, "combine_kernel");
   }
+  return PIC_OK;
+}
+
+pic_status link_call(pic_store *s, const pic_link_req *req, int32_t n_q_heads, const void *q,
+                     const void *k_self, const void *v_self, float scale, int32_t num_splits,
+                     void *out, float *lse, void *stream, Mode mode) {
+  if (!req) return fail(PIC_ERR_INVALID, "req is NULL");
+  Setup C;
+  pic_status rc = setup_call(s, req, n_q_heads, scale, req->layer, num_splits, mode, C);
+  if (rc != PIC_OK) return rc;
+  if (req->batch == 0) return PIC_OK;
+  rc = check_tensors(s, C.P, q, k_self, v_self, out);
+  if (rc != PIC_OK) return rc;
+  if (C.P.total_q == 0) return PIC_OK;
+  const hipStream_t st = (hipStream_t)stream;
+  if (C.work_bytes() > 0) {
+    rc = ensure_work(s, C.work_bytes());
+    if (rc != PIC_OK) return rc;
+  }
+  place_own(s, C.P, s->work, C.P.links.data());
+  DeviceGuard dg(s->device);
+  if (!dg.ok) return fail(PIC_ERR_HIP, "cannot select the store's device");
+  Stage *stage = nullptr;
+  TableLayout tl;
+  LinkParams lp = C.lp;
+  rc = upload(s, C.P, st, &stage, lp, tl);
+  if (rc != PIC_OK) return rc;
+  rc = launch_call(s, C, lp, s->work, q, k_self, v_self, scale, out, lse, st);
+  if (rc != PIC_OK) return rc;
   HIP_TRY(hipEventRecord(stage->done, st), "hipEventRecord(stage)");
   stage->pending = true;
   return PIC_OK;
 }
 
 }  // namespace
+
+// A request batch resolved once for repeated calls: the link tables of every
+// layer and the call's workspace live on the device for the plan's lifetime.
+struct pic_link_plan {
+  pic_store *store = nullptr;
+  Setup C;
+  int32_t batch = 0;
+  void *dev = nullptr;           // [layer tables][workspace]
+  size_t table_bytes = 0;        // one layer's tables, 256-byte aligned
+  size_t off_r = 0, off_o = 0;   // request / order tables within a layer's tables
+  void *work = nullptr;          // inside dev
+};
 
 extern "C" {
 
@@ -479,7 +554,7 @@ pic_status pic_store_create(const pic_store_desc *desc, pic_store **out) {
   const pic_store_desc &d = *desc;
   if (d.kind != PIC_GQA && d.kind != PIC_MLA) return fail(PIC_ERR_INVALID, "unknown kind %d", d.kind);
   if (d.dtype != PIC_F32 && d.dtype != PIC_BF16) return fail(PIC_ERR_INVALID, "unknown dtype %d", d.dtype);
-  if (d.reserved != 0) return fail(PIC_ERR_INVALID, "desc->reserved must be 0");
+  if (d.n_layers < 0 || d.n_layers > 256) return fail(PIC_ERR_INVALID, "n_layers must be 0..256");
   if (d.n_kv_heads <= 0 || d.d_k <= 0 || d.d_v <= 0 || d.capacity_tokens <= 0)
     return fail(PIC_ERR_INVALID, "n_kv_heads, d_k, d_v and capacity_tokens must be positive");
   if (d.kind == PIC_MLA && (d.n_kv_heads != 1 || d.d_v > d.d_k))
@@ -494,11 +569,10 @@ pic_status pic_store_create(const pic_store_desc *desc, pic_store **out) {
   s->capacity = round_up(d.capacity_tokens, kTile);
   s->k_tok_elems = (int64_t)d.n_kv_heads * d.d_k;
   s->v_tok_elems = d.kind == PIC_GQA ? (int64_t)d.n_kv_heads * d.d_v : 0;
+  s->n_layers = d.n_layers > 1 ? d.n_layers : 1;
+  s->layer_bytes = s->capacity * (s->k_tok_elems + s->v_tok_elems) * s->esz;
   hipError_t e = hipGetDevice(&s->device);
-  if (e == hipSuccess) {
-    const size_t bytes = (size_t)s->capacity * (s->k_tok_elems + s->v_tok_elems) * s->esz;
-    e = hipMalloc((void **)&s->pool, bytes);
-  }
+  if (e == hipSuccess) e = hipMalloc((void **)&s->pool, (size_t)s->layer_bytes * s->n_layers);
   if (e != hipSuccess) {
     delete s;
     return hip_fail(e, "hipMalloc(pool)");
@@ -509,6 +583,9 @@ pic_status pic_store_create(const pic_store_desc *desc, pic_store **out) {
 
 pic_status pic_store_destroy(pic_store *s) {
   if (!s) return PIC_OK;
+  if (s->live_plans > 0)
+    return fail(PIC_ERR_INVALID, "%lld link plans of this store are still alive",
+                (long long)s->live_plans);
   DeviceGuard dg(s->device);
   (void)hipDeviceSynchronize();
   for (Stage &st : s->ring) {
@@ -549,13 +626,21 @@ pic_status pic_store_put(pic_store *s, uint64_t chunk_id, int64_t n_tokens, cons
   }
   const hipStream_t st = (hipStream_t)stream;
   const pic_store_desc &d = s->desc;
-  char *kdst = s->pool + (size_t)s->used * (s->k_tok_elems + s->v_tok_elems) * s->esz;
-  hipError_t e = launch_put_rows(k, kdst, n_tokens, (int32_t)lp, d.n_kv_heads, d.d_k, s->esz, st);
-  if (e != hipSuccess) return hip_fail(e, "put_rows_kernel");
-  if (gqa) {
-    char *vdst = kdst + (size_t)lp * s->k_tok_elems * s->esz;
-    e = launch_put_transposed(v, vdst, n_tokens, (int32_t)lp, d.n_kv_heads, d.d_v, s->esz, st);
-    if (e != hipSuccess) return hip_fail(e, "put_transposed_kernel");
+  // layer l of the caller's buffers -> layer l of the slot
+  const int64_t k_src_layer = n_tokens * s->k_tok_elems * s->esz;
+  const int64_t v_src_layer = n_tokens * s->v_tok_elems * s->esz;
+  for (int32_t l = 0; l < s->n_layers; ++l) {
+    char *kdst = s->pool + (int64_t)l * s->layer_bytes +
+                 s->used * (s->k_tok_elems + s->v_tok_elems) * s->esz;
+    hipError_t e = launch_put_rows((const char *)k + l * k_src_layer, kdst, n_tokens, (int32_t)lp,
+                                   d.n_kv_heads, d.d_k, s->esz, st);
+    if (e != hipSuccess) return hip_fail(e, "put_rows_kernel");
+    if (gqa) {
+      char *vdst = kdst + (size_t)lp * s->k_tok_elems * s->esz;
+      e = launch_put_transposed((const char *)v + l * v_src_layer, vdst, n_tokens, (int32_t)lp,
+                                d.n_kv_heads, d.d_v, s->esz, st);
+      if (e != hipSuccess) return hip_fail(e, "put_transposed_kernel");
+    }
   }
   // A slot is its K block followed by its V block; slot offsets count padded
   // tokens of (K + V) elements.
@@ -597,10 +682,121 @@ pic_status pic_link_decode(pic_store *s, const pic_link_req *req, int32_t n_q_he
                    stream, Mode::Decode);
 }
 
-pic_status pic_debug_gather(pic_store *s, const uint64_t *ids, int32_t n, void *k_out,
-                            void *v_out, void *stream) {
+pic_status pic_link_plan_create(pic_store *s, const pic_link_req *req, int32_t n_q_heads,
+                                int32_t mode, int32_t num_splits, pic_link_plan **out) {
+  if (!out) return fail(PIC_ERR_INVALID, "out is NULL");
+  *out = nullptr;
+  if (!s) return fail(PIC_ERR_INVALID, "store is NULL");
+  if (!req) return fail(PIC_ERR_INVALID, "req is NULL");
+  if (req->layer != 0) return fail(PIC_ERR_INVALID, "req->layer must be 0 (each run names its layer)");
+  if (mode != PIC_PREFILL && mode != PIC_DECODE) return fail(PIC_ERR_INVALID, "unknown mode %d", mode);
+  if (mode == PIC_PREFILL && num_splits != 0)
+    return fail(PIC_ERR_INVALID, "num_splits must be 0 for prefill plans");
+  pic_link_plan *pl = new (std::nothrow) pic_link_plan();
+  if (!pl) return fail(PIC_ERR_OOM, "host allocation failed");
+  // the scale only has to pass validation here; each run passes its own
+  pic_status rc = setup_call(s, req, n_q_heads, 1.0f, 0, num_splits,
+                             mode == PIC_DECODE ? Mode::Decode : Mode::Prefill, pl->C);
+  if (rc != PIC_OK) {
+    delete pl;
+    return rc;
+  }
+  pl->store = s;
+  pl->batch = req->batch;
+  const Plan &P = pl->C.P;
+  const size_t nl = P.links.size(), nr = P.reqs.size();
+  pl->off_r = round_up(sizeof(LinkEntry) * nl, 256);
+  pl->off_o = pl->off_r + round_up(sizeof(ReqEntry) * nr, 256);
+  pl->table_bytes = round_up(pl->off_o + sizeof(int32_t) * nr, 256);
+  const size_t tables = pl->table_bytes * s->n_layers;
+  const size_t bytes = tables + pl->C.work_bytes();
+  if (bytes > 0) {
+    DeviceGuard dg(s->device);
+    if (!dg.ok) {
+      delete pl;
+      return fail(PIC_ERR_HIP, "cannot select the store's device");
+    }
+    hipError_t e = hipMalloc(&pl->dev, bytes);
+    if (e != hipSuccess) {
+      delete pl;
+      return hip_fail(e, "hipMalloc(plan)");
+    }
+    pl->work = (char *)pl->dev + tables;
+    // Every layer's tables differ only in the chunk links' addresses: layer
+    // l of a slot sits l pool layers further on; own-KV links point at the
+    // plan's workspace in every layer.
+    std::vector<char> host(tables, 0);
+    std::vector<LinkEntry> links(P.links);
+    place_own(s, P, pl->work, links.data());
+    std::vector<bool> own(nl, false);
+    for (auto &o : P.own) own[o.first] = true;
+    for (int32_t l = 0; l < s->n_layers; ++l) {
+      char *h = host.data() + (size_t)l * pl->table_bytes;
+      LinkEntry *L = (LinkEntry *)h;
+      for (size_t i = 0; i < nl; ++i) {
+        L[i] = links[i];
+        if (!own[i]) {
+          L[i].k = (const char *)links[i].k + (int64_t)l * s->layer_bytes;
+          L[i].v = (const char *)links[i].v + (int64_t)l * s->layer_bytes;
+        }
+      }
+      if (nr) memcpy(h + pl->off_r, P.reqs.data(), sizeof(ReqEntry) * nr);
+      if (nr) memcpy(h + pl->off_o, P.order.data(), sizeof(int32_t) * nr);
+    }
+    e = hipMemcpy(pl->dev, host.data(), tables, hipMemcpyHostToDevice);
+    if (e != hipSuccess) {
+      (void)hipFree(pl->dev);
+      delete pl;
+      return hip_fail(e, "hipMemcpy(plan tables)");
+    }
+  }
+  ++s->live_plans;
+  *out = pl;
+  return PIC_OK;
+}
+
+pic_status pic_link_plan_run(pic_link_plan *pl, int32_t layer, const void *q, const void *k_self,
+                             const void *v_self, float softmax_scale, void *out, float *lse,
+                             void *stream) {
+  if (!pl) return fail(PIC_ERR_INVALID, "plan is NULL");
+  pic_store *s = pl->store;
+  if (layer < 0 || layer >= s->n_layers)
+    return fail(PIC_ERR_INVALID, "layer %d outside the store's %d layers", layer, s->n_layers);
+  if (!std::isfinite(softmax_scale) || !(softmax_scale > 0.f))
+    return fail(PIC_ERR_INVALID, "softmax_scale must be positive and finite");
+  if (pl->batch == 0) return PIC_OK;
+  pic_status rc = check_tensors(s, pl->C.P, q, k_self, v_self, out);
+  if (rc != PIC_OK) return rc;
+  if (pl->C.P.total_q == 0) return PIC_OK;
+  DeviceGuard dg(s->device);
+  if (!dg.ok) return fail(PIC_ERR_HIP, "cannot select the store's device");
+  LinkParams lp = pl->C.lp;
+  const char *t = (const char *)pl->dev + (size_t)layer * pl->table_bytes;
+  lp.links = (const LinkEntry *)t;
+  lp.reqs = (const ReqEntry *)(t + pl->off_r);
+  lp.order = (const int32_t *)(t + pl->off_o);
+  return launch_call(s, pl->C, lp, pl->work, q, k_self, v_self, softmax_scale, out, lse,
+                     (hipStream_t)stream);
+}
+
+pic_status pic_link_plan_destroy(pic_link_plan *pl) {
+  if (!pl) return PIC_OK;
+  if (pl->dev) {
+    DeviceGuard dg(pl->store->device);
+    (void)hipDeviceSynchronize();
+    (void)hipFree(pl->dev);
+  }
+  --pl->store->live_plans;
+  delete pl;
+  return PIC_OK;
+}
+
+pic_status pic_debug_gather(pic_store *s, const uint64_t *ids, int32_t n, int32_t layer,
+                            void *k_out, void *v_out, void *stream) {
   if (!s) return fail(PIC_ERR_INVALID, "store is NULL");
   if (n < 0 || (n > 0 && !ids)) return fail(PIC_ERR_INVALID, "bad id list");
+  if (layer < 0 || layer >= s->n_layers)
+    return fail(PIC_ERR_INVALID, "layer %d outside the store's %d layers", layer, s->n_layers);
   const bool gqa = s->desc.kind == PIC_GQA;
   std::vector<LinkEntry> links(n);
   int64_t toks = 0;
@@ -610,7 +806,8 @@ pic_status pic_debug_gather(pic_store *s, const uint64_t *ids, int32_t n, void *
                                         (unsigned long long)ids[i]);
     const Slot &sl = it->second;
     LinkEntry &E = links[i];
-    E.k = s->pool + sl.off_tokens * (s->k_tok_elems + s->v_tok_elems) * s->esz;
+    E.k = s->pool + (int64_t)layer * s->layer_bytes +
+          sl.off_tokens * (s->k_tok_elems + s->v_tok_elems) * s->esz;
     E.v = gqa ? (const char *)E.k + (int64_t)sl.lp * s->k_tok_elems * s->esz : E.k;
     E.len = (int32_t)sl.len;
     E.lp = sl.lp;

@@ -25,6 +25,7 @@ _lib = None
 OK, ERR_INVALID, ERR_NOT_FOUND, ERR_EXISTS, ERR_OOM, ERR_HIP, ERR_UNSUPPORTED = 0, -1, -2, -3, -4, -5, -6
 F32, BF16 = 0, 1
 GQA, MLA = 0, 1
+PREFILL, DECODE = 0, 1
 
 
 class PicError(RuntimeError):
@@ -43,12 +44,12 @@ def status_name(st: int) -> str:
 
 class StoreDesc(ctypes.Structure):
     _fields_ = [("kind", ctypes.c_int32), ("dtype", ctypes.c_int32), ("n_kv_heads", ctypes.c_int32),
-                ("d_k", ctypes.c_int32), ("d_v", ctypes.c_int32), ("reserved", ctypes.c_int32),
+                ("d_k", ctypes.c_int32), ("d_v", ctypes.c_int32), ("n_layers", ctypes.c_int32),
                 ("capacity_tokens", ctypes.c_int64)]
 
 
 class LinkReq(ctypes.Structure):
-    _fields_ = [("batch", ctypes.c_int32), ("reserved", ctypes.c_int32),
+    _fields_ = [("batch", ctypes.c_int32), ("layer", ctypes.c_int32),
                 ("chunk_offsets", ctypes.c_void_p), ("chunk_ids", ctypes.c_void_p),
                 ("q_offsets", ctypes.c_void_p), ("self_offsets", ctypes.c_void_p)]
 
@@ -73,7 +74,10 @@ def lib():
             "pic_store_usage": [vp, vp, vp, vp],
             "pic_link_attn": [vp, vp, i32, vp, vp, vp, f32, vp, vp, vp],
             "pic_link_decode": [vp, vp, i32, vp, vp, vp, f32, i32, vp, vp, vp],
-            "pic_debug_gather": [vp, vp, i32, vp, vp, vp],
+            "pic_debug_gather": [vp, vp, i32, i32, vp, vp, vp],
+            "pic_link_plan_create": [vp, vp, i32, i32, i32, vp],
+            "pic_link_plan_run": [vp, i32, vp, vp, vp, f32, vp, vp, vp],
+            "pic_link_plan_destroy": [vp],
             "pic_prof_begin": [],
             "pic_prof_end": [vp, vp, vp, i32],
             "pic_peak_mfma_bf16": [i32, vp, vp],
@@ -124,8 +128,9 @@ def _host_i32(a):
 class Store:
     """A chunk store (pool + hash table) on the current HIP device."""
 
-    def __init__(self, kind: int, dtype: int, n_kv_heads: int, d_k: int, d_v: int, capacity_tokens: int):
-        self.desc = StoreDesc(kind, dtype, n_kv_heads, d_k, d_v, 0, capacity_tokens)
+    def __init__(self, kind: int, dtype: int, n_kv_heads: int, d_k: int, d_v: int, capacity_tokens: int,
+                 n_layers: int = 1):
+        self.desc = StoreDesc(kind, dtype, n_kv_heads, d_k, d_v, n_layers, capacity_tokens)
         h = ctypes.c_void_p()
         _check(lib().pic_store_create(ctypes.byref(self.desc), ctypes.byref(h)))
         self.handle = h
@@ -161,41 +166,78 @@ class Store:
         return u.value, c.value, n.value
 
 
-def _req(chunk_offsets, chunk_ids, q_offsets, self_offsets, keep: list):
+def _req(chunk_offsets, chunk_ids, q_offsets, self_offsets, keep: list, layer: int = 0):
     co = _host_i32(chunk_offsets)
     ids = np.ascontiguousarray(chunk_ids, dtype=np.uint64)
     qo = _host_i32(q_offsets)
     so = _host_i32(self_offsets)
     keep += [co, ids, qo, so]
-    return LinkReq(len(qo) - 1, 0, co.ctypes.data, ids.ctypes.data if ids.size else None,
+    return LinkReq(len(qo) - 1, int(layer), co.ctypes.data, ids.ctypes.data if ids.size else None,
                    qo.ctypes.data, None if so is None else so.ctypes.data)
 
 
 def link_attn(store: Store, chunk_offsets, chunk_ids, q_offsets, self_offsets, n_q_heads: int, q,
-              k_self, v_self, softmax_scale: float, out, lse=None, stream: Optional[int] = None):
-    """pic_link_attn: prefill-shaped link attention."""
+              k_self, v_self, softmax_scale: float, out, lse=None, stream: Optional[int] = None,
+              layer: int = 0):
+    """pic_link_attn: prefill-shaped link attention on store layer `layer`."""
     keep: list = []
-    req = _req(chunk_offsets, chunk_ids, q_offsets, self_offsets, keep)
+    req = _req(chunk_offsets, chunk_ids, q_offsets, self_offsets, keep, layer)
     _check(lib().pic_link_attn(store.handle, ctypes.byref(req), int(n_q_heads), _ptr(q), _ptr(k_self),
                                _ptr(v_self), float(softmax_scale), _ptr(out), _ptr(lse), stream))
 
 
 def link_decode(store: Store, chunk_offsets, chunk_ids, q_offsets, self_offsets, n_q_heads: int, q,
                 k_self, v_self, softmax_scale: float, out, lse=None, num_splits: int = 0,
-                stream: Optional[int] = None):
-    """pic_link_decode: decode-shaped link attention with split-K."""
+                stream: Optional[int] = None, layer: int = 0):
+    """pic_link_decode: decode-shaped link attention with split-K on store layer `layer`."""
     keep: list = []
-    req = _req(chunk_offsets, chunk_ids, q_offsets, self_offsets, keep)
+    req = _req(chunk_offsets, chunk_ids, q_offsets, self_offsets, keep, layer)
     _check(lib().pic_link_decode(store.handle, ctypes.byref(req), int(n_q_heads), _ptr(q), _ptr(k_self),
                                  _ptr(v_self), float(softmax_scale), int(num_splits), _ptr(out),
                                  _ptr(lse), stream))
 
 
-def debug_gather(store: Store, ids, k_out, v_out, stream: Optional[int] = None):
-    """pic_debug_gather: materialise the concatenation of the listed chunks."""
+def debug_gather(store: Store, ids, k_out, v_out, stream: Optional[int] = None, layer: int = 0):
+    """pic_debug_gather: materialise the concatenation of the listed chunks of one layer."""
     ids = np.ascontiguousarray(ids, dtype=np.uint64)
     _check(lib().pic_debug_gather(store.handle, ids.ctypes.data if ids.size else None, len(ids),
-                                  _ptr(k_out), _ptr(v_out), stream))
+                                  int(layer), _ptr(k_out), _ptr(v_out), stream))
+
+
+class LinkPlan:
+    """pic_link_plan_*: a request batch resolved once, run per layer / decode step."""
+
+    def __init__(self, store: Store, chunk_offsets, chunk_ids, q_offsets, self_offsets, n_q_heads: int,
+                 mode: int = PREFILL, num_splits: int = 0):
+        keep: list = []
+        req = _req(chunk_offsets, chunk_ids, q_offsets, self_offsets, keep)
+        h = ctypes.c_void_p()
+        _check(lib().pic_link_plan_create(store.handle, ctypes.byref(req), int(n_q_heads), int(mode),
+                                          int(num_splits), ctypes.byref(h)))
+        self.handle = h.value
+        self.store = store          # the store must outlive the plan
+
+    def run(self, layer: int, q, k_self, v_self, softmax_scale: float, out, lse=None,
+            stream: Optional[int] = None):
+        _check(lib().pic_link_plan_run(self.handle, int(layer), _ptr(q), _ptr(k_self), _ptr(v_self),
+                                       float(softmax_scale), _ptr(out), _ptr(lse), stream))
+
+    def close(self):
+        if getattr(self, "handle", None):
+            _check(lib().pic_link_plan_destroy(self.handle))
+            self.handle = None
+
+    def __enter__(self):
+        return self
+
+    def __exit__(self, *exc):
+        self.close()
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
 
 
 def peak_mfma_bf16(iters: int = 4096, stream: Optional[int] = None) -> float:

@@ -172,13 +172,15 @@ def _normal(rng, shape, std, dtype):
     return f32_to_bf16_bits(x) if dtype == BF16 else x
 
 
-def make_chunk(cfg: LinkConfig, index: int):
-    """KV of the store's index-th chunk, token-major.
+def make_chunk(cfg: LinkConfig, index: int, layer: int = 0):
+    """KV of the store's index-th chunk in cross-attention layer `layer`, token-major.
 
     GQA: (k [len, H_kv, d_k], v [len, H_kv, d_v]); MLA: (k [len, 1, d_k], None),
-    the value being the first d_v entries of each latent row.
+    the value being the first d_v entries of each latent row. Every layer
+    draws its own values (layer 0 keeps the single-layer stream).
     """
-    rng = np.random.Generator(np.random.PCG64(np.random.SeedSequence([cfg.seed, _STREAM_CHUNK, index])))
+    entropy = [cfg.seed, _STREAM_CHUNK, index] + ([layer] if layer else [])
+    rng = np.random.Generator(np.random.PCG64(np.random.SeedSequence(entropy)))
     n = cfg.chunk_length(index)
     k = _normal(rng, (n, cfg.n_kv_heads, cfg.d_k), 1.0, cfg.dtype)
     v = None if cfg.kind == MLA else _normal(rng, (n, cfg.n_kv_heads, cfg.d_v), 1.0, cfg.dtype)

@@ -31,13 +31,14 @@ def test_status_strings():
     (dict(n_kv_heads=0), pic.ERR_INVALID),
     (dict(d_k=0), pic.ERR_INVALID),
     (dict(capacity_tokens=0), pic.ERR_INVALID),
-    (dict(reserved=1), pic.ERR_INVALID),
+    (dict(n_layers=-1), pic.ERR_INVALID),
+    (dict(n_layers=257), pic.ERR_INVALID),
     (dict(kind=pic.MLA, n_kv_heads=2), pic.ERR_INVALID),
     (dict(kind=pic.MLA, n_kv_heads=1, d_v=256, d_k=128), pic.ERR_INVALID),
     (dict(d_k=12), pic.ERR_UNSUPPORTED),
 ])
 def test_store_create_rejects_bad_descriptors(desc, status):
-    base = dict(kind=pic.GQA, dtype=pic.BF16, n_kv_heads=2, d_k=64, d_v=64, reserved=0,
+    base = dict(kind=pic.GQA, dtype=pic.BF16, n_kv_heads=2, d_k=64, d_v=64, n_layers=0,
                 capacity_tokens=1024)
     base.update(desc)
     d = pic.StoreDesc(**base)
@@ -57,5 +58,11 @@ def test_null_arguments_are_rejected():
     assert L.pic_store_usage(None, None, None, None) == pic.ERR_INVALID
     assert L.pic_link_attn(None, None, 8, None, None, None, 1.0, None, None, None) == pic.ERR_INVALID
     assert L.pic_link_decode(None, None, 8, None, None, None, 1.0, 0, None, None, None) == pic.ERR_INVALID
-    assert L.pic_debug_gather(None, None, 0, None, None, None) == pic.ERR_INVALID
+    assert L.pic_debug_gather(None, None, 0, 0, None, None, None) == pic.ERR_INVALID
     assert "NULL" in pic.last_error()
+    h = ctypes.c_void_p(123)
+    assert L.pic_link_plan_create(None, None, 8, pic.PREFILL, 0, ctypes.byref(h)) == pic.ERR_INVALID
+    assert not h.value
+    assert L.pic_link_plan_create(None, None, 8, pic.PREFILL, 0, None) == pic.ERR_INVALID
+    assert L.pic_link_plan_run(None, 0, None, None, None, 1.0, None, None, None) == pic.ERR_INVALID
+    assert L.pic_link_plan_destroy(None) == pic.OK
