@@ -196,6 +196,30 @@ pic_status pic_link_plan_destroy(pic_link_plan *plan);
 pic_status pic_debug_gather(pic_store *store, const uint64_t *ids, int32_t n, int32_t layer,
                             void *k_out, void *v_out, void *stream);
 
+/* Dense per-head projections around absorbed MLA link attention, for the
+ * DeepSeek-V2-Lite backbone (Sec. 5.1): per head h its latent rows c (512)
+ * give non-absorbed keys [W_UK[h] c | k_rope] and values W_UV[h] c, with
+ * W_UK[h] and W_UV[h] 128 x 512. Absorbing W_UK into the query turns the
+ * attention into the latent form pic_link_attn computes on an MLA store
+ * (d_k 576, d_v 512); W_UV then maps its latent output to the 128 value dims.
+ * bf16 in and out (round to nearest even), fp32 accumulation.
+ * pic_mla_absorb_q: q_out[t,h,0:512] = W_UK[h]^T q[t,h,0:128] and
+ *   q_out[t,h,512:576] = q[t,h,128:192] (the rope part, copied).
+ *   q device [n_tokens][n_heads][192] (q_nope 128 | q_rope 64)
+ *   w_uk_t device [n_heads][512][128]: W_UK[h] transposed (row j holds the
+ *     128 weights of latent dim j)
+ *   q_out device [n_tokens][n_heads][576]
+ * pic_mla_up_v: out[t,h,0:128] = W_UV[h] o_lat[t,h,0:512].
+ *   o_lat device [n_tokens][n_heads][512] (pic_link_attn's output)
+ *   w_uv device [n_heads][128][512]
+ *   out device [n_tokens][n_heads][128]
+ * All pointers 16-byte aligned; n_heads 1..1024; n_tokens 0 does nothing.
+ * Errors: INVALID, HIP. */
+pic_status pic_mla_absorb_q(int32_t n_tokens, int32_t n_heads, const void *q, const void *w_uk_t,
+                            void *q_out, void *stream);
+pic_status pic_mla_up_v(int32_t n_tokens, int32_t n_heads, const void *o_lat, const void *w_uv,
+                        void *out, void *stream);
+
 /* Kernel timing for measurement. pic_prof_begin() clears and enables
  * recording of HIP events around every launch of the main attention kernel;
  * pic_prof_end() waits for them, disables recording and returns the summed

@@ -142,3 +142,6 @@ def run_workload(wl, chunks, row_select=None):
                      links=workload_links(wl, chunks), q=wl.q, q_offsets=wl.plan.q_offsets,
                      k_self=wl.k_self, v_self=wl.v_self, self_offsets=wl.plan.self_offsets,
                      tau=float(np.float32(cfg.scale)), row_select=row_select)
+
+
+from .mla_proj import mla_absorb_q, mla_up_v  # noqa: E402  (dense MLA projections, fp64)

@@ -23,6 +23,7 @@ SOURCES = [
     "kernels_decode_d128.hip",
     "kernels_mla.hip",
     "kernels_peaks.hip",
+    "kernels_mla_proj.hip",
 ]
 
 # Per-file code generation flags. The MLA kernel keeps its accumulators in

@@ -1,0 +1,186 @@
+// Dense per-head projections around absorbed MLA link attention (the
+// DeepSeek-V2-Lite backbone of Sec. 5.1, whose non-absorbed keys and values
+// are k_nope = W_UK c and v = W_UV c of the latent row c):
+//   absorb: q_out[t,h, 0:512]   = W_UK[h]^T q[t,h, 0:128]   (the query side of
+//           q_nope . (W_UK c) = (W_UK^T q_nope) . c); q_out[t,h, 512:576] =
+//           q[t,h, 128:192] (the rope part passes through)
+//   up:     out[t,h, 0:128]     = W_UV[h] o[t,h, 0:512]     (sum_j p_j W_UV c_j
+//           = W_UV sum_j p_j c_j)
+// Both are C^T[n][t] = sum_k W[n][k] A[t][k] per head, with the weight stored
+// [N][K] (K contiguous) and the activation rows strided by tokens, computed
+// on v_mfma_f32_32x32x16_bf16 with fp32 accumulation and bf16 outputs
+// (round to nearest even). Each of a workgroup's four waves holds a 128 (n)
+// x 128 (k) slice of the head's weights in registers, read once, and the
+// workgroup then walks its share of the 32-token blocks: with N = 512 the
+// waves split n (one 128-wide range each, K = 128 in full), with K = 512
+// they split k and add their partial tiles through LDS. Per block a wave
+// loads its eight 16-byte activation fragments per lane and issues 32 MFMAs.
+// These projections move more bytes than they compute (about 100 FLOP/B),
+// so HBM bounds them; reading the weights from L2 for every block instead
+// made them 2-3x slower.
+#include "pic_internal.hpp"
+
+#include <algorithm>
+
+namespace pic {
+namespace {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+
+__device__ __forceinline__ bf16x8 as_bf16x8(uint4 u) { return __builtin_bit_cast(bf16x8, u); }
+
+struct ProjArgs {
+  const uint16_t *a;      // activation, row (t, h) at a + t * a_tok + h * a_head
+  const uint16_t *w;      // weights [H][N][K]
+  uint16_t *c;            // output, row (t, h) at c + t * c_tok + h * c_head
+  int64_t a_tok, a_head, c_tok, c_head;
+  int32_t n_tokens, n_heads;
+  int32_t parts;          // workgroups per head
+};
+
+// kRope: also copy a[.., 128:192] to c[.., 512:576] (the absorb projection).
+// Workgroup (head h, part j) of `parts` per head walks token blocks j,
+// j + parts, ... Consecutive workgroup ids go round-robin to the 8 XCDs;
+// when the head count allows, all parts of a head go to one XCD, so that
+// its weights are fetched into one L2 only.
+template <int K, int N, bool kRope>
+__global__ __launch_bounds__(256, 1) void proj_kernel(ProjArgs p) {
+  static_assert((K == 128 && N == 512) || (K == 512 && N == 128), "one 128 x 128 slice per wave");
+  constexpr bool kSplitK = K > 128;
+  __shared__ float red[kSplitK ? 4 * 32 * 128 : 1];     // partial tiles of the k slices
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int parts = p.parts;
+  int h, part;
+  if (p.n_heads % 8 == 0) {
+    const int xcd = blockIdx.x & 7, j = blockIdx.x >> 3;
+    h = xcd + 8 * (j / parts);
+    part = j % parts;
+  } else {
+    h = blockIdx.x / parts;
+    part = blockIdx.x % parts;
+  }
+  const int g = lane >> 5;
+  const int n0 = kSplitK ? 0 : wave * 128;       // this wave's n range
+  const int k0 = kSplitK ? wave * 128 : 0;       // this wave's k range
+  const uint16_t *ah = p.a + (int64_t)h * p.a_head;
+  uint16_t *ch = p.c + (int64_t)h * p.c_head;
+
+  // weight fragments: w[nt][s] = W[n0 + nt*32 + (lane&31)][k0 + s*16 + g*8 .. +8]
+  bf16x8 w[4][8];
+  {
+    const uint16_t *wh = p.w + (int64_t)h * N * K + (int64_t)(n0 + (lane & 31)) * K + k0 + g * 8;
+#pragma unroll
+    for (int nt = 0; nt < 4; ++nt)
+#pragma unroll
+      for (int s = 0; s < 8; ++s) w[nt][s] = as_bf16x8(*(const uint4 *)(wh + nt * 32 * K + s * 16));
+  }
+
+  const int n_blocks = (p.n_tokens + 31) / 32;
+  // activation fragments of a block: b[s] = A[t][k0 + s*16 + g*8 .. +8]
+  auto load_a = [&](int tb, bf16x8 (&b)[8]) {
+    const int t = tb * 32 + (lane & 31);
+    const bool tv = tb < n_blocks && t < p.n_tokens;
+    const uint16_t *arow = ah + (tv ? (int64_t)t * p.a_tok : 0) + k0 + g * 8;
+#pragma unroll
+    for (int s = 0; s < 8; ++s)
+      b[s] = as_bf16x8(tv ? *(const uint4 *)(arow + s * 16) : make_uint4(0, 0, 0, 0));
+  };
+  bf16x8 b[8], bn[8];
+  load_a(part, b);
+  for (int tb = part; tb < n_blocks; tb += parts) {
+    const int t = tb * 32 + (lane & 31);
+    const bool tv = t < p.n_tokens;
+    load_a(tb + parts, bn);         // the next block's fragments load during this one
+    if (kRope) {
+      // 32 tokens x 128 bytes of rope, one 16-byte piece per thread
+      const int tt = tb * 32 + (threadIdx.x >> 3), piece = threadIdx.x & 7;
+      if (tt < p.n_tokens)
+        *(uint4 *)(ch + (int64_t)tt * p.c_tok + 512 + piece * 8) =
+            *(const uint4 *)(ah + (int64_t)tt * p.a_tok + 128 + piece * 8);
+    }
+    f32x16 acc[4];
+#pragma unroll
+    for (int nt = 0; nt < 4; ++nt)
+#pragma unroll
+      for (int x = 0; x < 16; ++x) acc[nt][x] = 0.f;
+#pragma unroll
+    for (int s = 0; s < 8; ++s)
+#pragma unroll
+      for (int nt = 0; nt < 4; ++nt)
+        acc[nt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(w[nt][s], b[s], acc[nt], 0, 0, 0);
+
+    // C^T tile: lane holds token t and n = nt*32 + jj*8 + g*4 + (0..3)
+    if (kSplitK) {
+      // partial tiles to LDS as [wave][n][token], then wave w adds the four
+      // partials of n tile w and stores it
+      float *mine = red + wave * 32 * 128;
+#pragma unroll
+      for (int nt = 0; nt < 4; ++nt)
+#pragma unroll
+        for (int x = 0; x < 16; ++x)
+          mine[(nt * 32 + (x >> 2) * 8 + g * 4 + (x & 3)) * 32 + (lane & 31)] = acc[nt][x];
+      __syncthreads();
+      if (tv) {
+        uint16_t *crow = ch + (int64_t)t * p.c_tok;
+#pragma unroll
+        for (int jj = 0; jj < 4; ++jj) {
+          __bf16 v4[4];
+#pragma unroll
+          for (int x = 0; x < 4; ++x) {
+            const int n = wave * 32 + jj * 8 + g * 4 + x;
+            float sum = 0.f;
+#pragma unroll
+            for (int q = 0; q < 4; ++q) sum += red[q * 32 * 128 + n * 32 + (lane & 31)];
+            v4[x] = (__bf16)sum;
+          }
+          *(uint2 *)(crow + wave * 32 + jj * 8 + g * 4) = __builtin_bit_cast(uint2, v4);
+        }
+      }
+      __syncthreads();      // before the next block overwrites the partials
+    } else if (tv) {
+      uint16_t *crow = ch + (int64_t)t * p.c_tok + n0;
+#pragma unroll
+      for (int nt = 0; nt < 4; ++nt)
+#pragma unroll
+        for (int jj = 0; jj < 4; ++jj) {
+          __bf16 v4[4];
+#pragma unroll
+          for (int x = 0; x < 4; ++x) v4[x] = (__bf16)acc[nt][jj * 4 + x];
+          *(uint2 *)(crow + nt * 32 + jj * 8 + g * 4) = __builtin_bit_cast(uint2, v4);
+        }
+    }
+#pragma unroll
+    for (int st = 0; st < 8; ++st) b[st] = bn[st];
+  }
+}
+
+// Workgroups per head: about one per CU over all heads, never more than
+// the head's token blocks.
+int proj_parts(int32_t n_tokens, int32_t n_heads) {
+  const int blocks = (n_tokens + 31) / 32;
+  return std::max(1, std::min(blocks, (256 + n_heads - 1) / n_heads));
+}
+
+}  // namespace
+
+hipError_t launch_mla_absorb_q(const void *q, const void *w_uk_t, void *q_out, int32_t n_tokens,
+                               int32_t n_heads, hipStream_t st) {
+  ProjArgs p{(const uint16_t *)q, (const uint16_t *)w_uk_t, (uint16_t *)q_out,
+             (int64_t)n_heads * 192, 192, (int64_t)n_heads * 576, 576, n_tokens, n_heads,
+             proj_parts(n_tokens, n_heads)};
+  hipLaunchKernelGGL((proj_kernel<128, 512, true>), dim3(p.parts * n_heads), dim3(256), 0, st, p);
+  return hipGetLastError();
+}
+
+hipError_t launch_mla_up_v(const void *o_lat, const void *w_uv, void *out, int32_t n_tokens,
+                           int32_t n_heads, hipStream_t st) {
+  ProjArgs p{(const uint16_t *)o_lat, (const uint16_t *)w_uv, (uint16_t *)out,
+             (int64_t)n_heads * 512, 512, (int64_t)n_heads * 128, 128, n_tokens, n_heads,
+             proj_parts(n_tokens, n_heads)};
+  hipLaunchKernelGGL((proj_kernel<512, 128, false>), dim3(p.parts * n_heads), dim3(256), 0, st, p);
+  return hipGetLastError();
+}
+
+}  // namespace pic

@@ -11,6 +11,7 @@
 #include <cstdio>
 #include <cstring>
 #include <functional>
+#include <initializer_list>
 #include <mutex>
 #include <string>
 #include <unordered_map>
@@ -833,6 +834,42 @@ pic_status pic_debug_gather(pic_store *s, const uint64_t *ids, int32_t n, int32_
   if (e != hipSuccess) return hip_fail(e, "gather_kernel");
   HIP_TRY(hipEventRecord(stage->done, st), "hipEventRecord(stage)");
   stage->pending = true;
+  return PIC_OK;
+}
+
+namespace {
+
+// Shared checks of the two MLA projections: sizes, 16-byte aligned device
+// buffers.
+pic_status check_proj(int32_t n_tokens, int32_t n_heads, std::initializer_list<const void *> bufs) {
+  if (n_tokens < 0 || n_heads <= 0 || n_heads > 1024)
+    return fail(PIC_ERR_INVALID, "n_tokens must be >= 0 and n_heads 1..1024");
+  if ((int64_t)n_tokens * n_heads > INT32_MAX / 4) return fail(PIC_ERR_INVALID, "too many rows");
+  if (n_tokens == 0) return PIC_OK;
+  for (const void *b : bufs) {
+    if (!b) return fail(PIC_ERR_INVALID, "a tensor pointer is NULL");
+    if ((uintptr_t)b % 16) return fail(PIC_ERR_INVALID, "tensors must be 16-byte aligned");
+  }
+  return PIC_OK;
+}
+
+}  // namespace
+
+pic_status pic_mla_absorb_q(int32_t n_tokens, int32_t n_heads, const void *q, const void *w_uk_t,
+                            void *q_out, void *stream) {
+  pic_status rc = check_proj(n_tokens, n_heads, {q, w_uk_t, q_out});
+  if (rc != PIC_OK || n_tokens == 0) return rc;
+  hipError_t e = launch_mla_absorb_q(q, w_uk_t, q_out, n_tokens, n_heads, (hipStream_t)stream);
+  if (e != hipSuccess) return hip_fail(e, "proj_kernel (absorb)");
+  return PIC_OK;
+}
+
+pic_status pic_mla_up_v(int32_t n_tokens, int32_t n_heads, const void *o_lat, const void *w_uv,
+                        void *out, void *stream) {
+  pic_status rc = check_proj(n_tokens, n_heads, {o_lat, w_uv, out});
+  if (rc != PIC_OK || n_tokens == 0) return rc;
+  hipError_t e = launch_mla_up_v(o_lat, w_uv, out, n_tokens, n_heads, (hipStream_t)stream);
+  if (e != hipSuccess) return hip_fail(e, "proj_kernel (up)");
   return PIC_OK;
 }
 

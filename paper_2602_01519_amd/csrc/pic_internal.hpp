@@ -80,6 +80,10 @@ hipError_t launch_table_copy(const void *src, void *dst, int64_t bytes, hipStrea
 
 // Lays each request's own KV (token-major k_self / v_self) out like a chunk
 // slot at its own link (the request's last link), zero-padded to lp.
+hipError_t launch_mla_absorb_q(const void *q, const void *w_uk_t, void *q_out, int32_t n_tokens,
+                               int32_t n_heads, hipStream_t st);
+hipError_t launch_mla_up_v(const void *o_lat, const void *w_uv, void *out, int32_t n_tokens,
+                           int32_t n_heads, hipStream_t st);
 hipError_t launch_prep_own(const LinkParams &p, int32_t mla, int32_t esz, int32_t max_own_lp,
                            hipStream_t st);
 

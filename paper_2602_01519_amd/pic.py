@@ -78,6 +78,8 @@ def lib():
             "pic_link_plan_create": [vp, vp, i32, i32, i32, vp],
             "pic_link_plan_run": [vp, i32, vp, vp, vp, f32, vp, vp, vp],
             "pic_link_plan_destroy": [vp],
+            "pic_mla_absorb_q": [i32, i32, vp, vp, vp, vp],
+            "pic_mla_up_v": [i32, i32, vp, vp, vp, vp],
             "pic_prof_begin": [],
             "pic_prof_end": [vp, vp, vp, i32],
             "pic_peak_mfma_bf16": [i32, vp, vp],
@@ -238,6 +240,16 @@ class LinkPlan:
             self.close()
         except Exception:
             pass
+
+
+def mla_absorb_q(n_tokens: int, n_heads: int, q, w_uk_t, q_out, stream: Optional[int] = None):
+    """pic_mla_absorb_q: q_out = [W_UK^T q_nope | q_rope] per head (bf16)."""
+    _check(lib().pic_mla_absorb_q(int(n_tokens), int(n_heads), _ptr(q), _ptr(w_uk_t), _ptr(q_out), stream))
+
+
+def mla_up_v(n_tokens: int, n_heads: int, o_lat, w_uv, out, stream: Optional[int] = None):
+    """pic_mla_up_v: out = W_UV o_lat per head (bf16)."""
+    _check(lib().pic_mla_up_v(int(n_tokens), int(n_heads), _ptr(o_lat), _ptr(w_uv), _ptr(out), stream))
 
 
 def peak_mfma_bf16(iters: int = 4096, stream: Optional[int] = None) -> float:

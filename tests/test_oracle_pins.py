@@ -409,6 +409,68 @@ def test_mla_absorbed_equals_non_absorbed():
         assert_close(up[:, h], ref, rel=1e-12, atol=1e-12)
 
 
+def test_mla_projections_chain_equals_non_absorbed_attention():
+    """oracle.mla_absorb_q -> oracle.link_attn (latent rows) -> oracle.mla_up_v equals
+    torch SDPA over explicit per-head keys [W_UK c ; k_rope] and values W_UV c (the
+    non-absorbed MLA form), with the link mask; distinct widths (d_nope 4, rope 2, r 6,
+    d_val 5) so that a transposed or misplaced operand in either projection fails."""
+    rng = np.random.default_rng(21)
+    H, r_lat, d_rope, d_nope, d_val = 3, 6, 2, 4, 5
+    lens, ls, lq = [4, 3], 5, 3
+    ints = lambda shape, lo=-3, hi=4: rng.integers(lo, hi, size=shape).astype(np.float64) / 4
+    W_UK = ints((H, d_nope, r_lat))
+    W_UV = ints((H, d_val, r_lat))
+    lat_chunks = [ints((n, 1, r_lat + d_rope)) for n in lens]
+    lat_self = ints((ls, 1, r_lat + d_rope))
+    q = ints((lq, H, d_nope + d_rope))
+    q_abs = oracle.mla_absorb_q(q, W_UK.transpose(0, 2, 1).copy())
+    assert q_abs.shape == (lq, H, r_lat + d_rope)
+    assert np.array_equal(q_abs[:, :, r_lat:], q[:, :, d_nope:])     # rope passes through
+    tau = 0.125
+    # dyadic values: the absorbed query is exact in fp32
+    assert np.array_equal(q_abs.astype(np.float32).astype(np.float64), q_abs)
+    lat_out, _ = run_oracle([(c.astype(np.float32), None) for c in lat_chunks],
+                            q_abs.astype(np.float32), lat_self.astype(np.float32), None,
+                            dtype=W.F32, tau=tau, dv=r_lat, mla=True)
+    out = oracle.mla_up_v(lat_out, W_UV)
+    assert out.shape == (lq, H, d_val)
+    C = np.concatenate(lat_chunks + [lat_self])[:, 0]
+    ld = sum(lens)
+    mask = torch.zeros(lq, C.shape[0], dtype=torch.bool)
+    mask[:, :ld] = True
+    mask[:, ld:] = torch.arange(ls)[None, :] <= torch.arange(lq)[:, None] + ls - lq
+    for h in range(H):
+        K = np.concatenate([C[:, :r_lat] @ W_UK[h].T, C[:, r_lat:]], axis=1)
+        V = C[:, :r_lat] @ W_UV[h].T
+        ref = torch.nn.functional.scaled_dot_product_attention(
+            torch.from_numpy(q[:, h])[None], torch.from_numpy(K)[None], torch.from_numpy(V)[None],
+            attn_mask=mask[None], scale=tau)[0].numpy()
+        assert_close(out[:, h], ref, rel=1e-12, atol=1e-12)
+
+
+def test_mla_projections_special_weights():
+    """Identity-embedding W_UK^T puts q_nope in the first latent dims and zeros the
+    rest; one-hot rows of W_UV pick latent dims; bf16 bit patterns widen exactly."""
+    rng = np.random.default_rng(22)
+    T, H, d, rope, r = 4, 2, 3, 2, 5
+    q_bits = W.f32_to_bf16_bits(rng.standard_normal((T, H, d + rope), dtype=np.float32))
+    q = W.bf16_bits_to_f32(q_bits).astype(np.float64)
+    w = np.zeros((H, r, d))
+    for h in range(H):
+        w[h, :d, :] = np.eye(d)
+    out = oracle.mla_absorb_q(q_bits, W.f32_to_bf16_bits(w.astype(np.float32)))
+    assert np.array_equal(out[:, :, :d], q[:, :, :d])
+    assert np.all(out[:, :, d:r] == 0)
+    assert np.array_equal(out[:, :, r:], q[:, :, d:])
+    o = rng.standard_normal((T, H, r))
+    pick = [4, 0, 2]
+    wv = np.zeros((H, len(pick), r))
+    for h in range(H):
+        for i, j in enumerate(pick):
+            wv[h, i, j] = 1.0
+    assert np.array_equal(oracle.mla_up_v(o, wv), o[:, :, pick])
+
+
 # ---------------------------------------------------------------------------
 # degenerate cases
 
