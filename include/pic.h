@@ -68,8 +68,10 @@ enum { PIC_GQA = 0, PIC_MLA = 1 };      /* pic_store_desc.kind  */
  *   and 4.3, Fig. 3: 8 among 32 decoder layers; Eq. 12), and each reads its
  *   own K and V of every document; a chunk's caches of all layers are put
  *   together and each link call names its layer.
- * capacity_tokens: pool size in tokens per layer. Each chunk occupies its
- * length rounded up to a multiple of 64 tokens in every layer. */
+ * capacity_tokens: pool size in tokens per layer, in pages of 64 tokens.
+ * Each chunk occupies its length rounded up to whole pages in every layer,
+ * in one run of consecutive pages when a free run is long enough, else in
+ * several (removal leaves holes; no copy ever moves a chunk). */
 typedef struct pic_store_desc {
   int32_t kind;
   int32_t dtype;
@@ -103,12 +105,22 @@ pic_status pic_store_destroy(pic_store *store);
 pic_status pic_store_put(pic_store *store, uint64_t chunk_id, int64_t n_tokens, const void *k,
                          const void *v, void *stream);
 
+/* Removes a chunk from the store and frees its pages (the paper's allocator
+ * hands out free memory, Sec. 5.3, and says nothing of eviction; removal is
+ * the caller's policy). The pages are reused only after the work enqueued on
+ * `stream` up to this call has completed: pass the stream of the link calls
+ * that may still read the chunk. A removed id may be put again.
+ * Errors: INVALID (NULL store, or a live link plan links the chunk),
+ * NOT_FOUND, HIP. */
+pic_status pic_store_remove(pic_store *store, uint64_t chunk_id, void *stream);
+
 /* Hash-table lookup (Sec. 3 step 1): *n_tokens_out = the chunk's length.
  * Errors: INVALID, NOT_FOUND. */
 pic_status pic_store_lookup(const pic_store *store, uint64_t chunk_id, int64_t *n_tokens_out);
 
-/* Pool usage in (padded) tokens and the number of stored chunks. Any output
- * pointer may be NULL. */
+/* Pool usage in tokens of allocated 64-token pages (pages of removed chunks
+ * count until their readers have finished), the capacity, and the number of
+ * stored chunks. Any output pointer may be NULL. */
 pic_status pic_store_usage(const pic_store *store, int64_t *used_tokens,
                            int64_t *capacity_tokens, int64_t *n_chunks);
 

@@ -11,6 +11,7 @@
 #include <cstdio>
 #include <cstring>
 #include <functional>
+#include <map>
 #include <initializer_list>
 #include <mutex>
 #include <string>
@@ -63,10 +64,22 @@ struct DeviceGuard {
   }
 };
 
+// The pool is a sequence of 64-token pages (one attention tile each). A
+// chunk occupies runs of consecutive pages -- one run whenever a free run
+// is long enough -- and each run holds a piece of the chunk laid out like a
+// chunk of its own (K [H][run tokens][d_k], then V^T [H][d_v][run tokens]),
+// so a piece is one link-table entry and the kernels need no page table.
+struct Run {
+  int64_t page0;        // first page
+  int32_t pages;
+  int32_t tok0;         // first chunk token held by the run
+  int32_t ntok;         // chunk tokens held by the run
+};
+
 struct Slot {
-  int64_t off_tokens;   // first padded token of the slot in the pool
   int64_t len;
-  int32_t lp;
+  std::vector<Run> runs;
+  int64_t plan_refs = 0;   // live link plans that link this chunk
 };
 
 // Pinned host table + device copy + completion event. The planner writes a
@@ -103,7 +116,11 @@ struct pic_store {
   int esz = 2;
   char *pool = nullptr;
   int64_t capacity = 0;          // padded tokens
-  int64_t used = 0;
+  int64_t used = 0;              // tokens of allocated pages
+  std::map<int64_t, int64_t> free_runs;   // page0 -> pages, coalesced
+  // runs of removed chunks, reusable once the event (recorded on the
+  // remover's stream) has completed
+  std::vector<std::pair<hipEvent_t, std::vector<Run>>> pending;
   int32_t n_layers = 1;
   int64_t layer_bytes = 0;       // bytes of one layer's pool; layer l of a slot is l * layer_bytes on
   int64_t live_plans = 0;
@@ -160,6 +177,89 @@ pic_status ensure_work(pic_store *s, size_t bytes) {
   return PIC_OK;
 }
 
+// Returns a run of pages to the free map, merging it with free neighbours.
+void free_run(pic_store *s, int64_t page0, int64_t pages) {
+  auto next = s->free_runs.lower_bound(page0);
+  if (next != s->free_runs.end() && next->first == page0 + pages) {
+    pages += next->second;
+    next = s->free_runs.erase(next);
+  }
+  if (next != s->free_runs.begin()) {
+    auto prev = std::prev(next);
+    if (prev->first + prev->second == page0) {
+      prev->second += pages;
+      return;
+    }
+  }
+  s->free_runs.emplace(page0, pages);
+}
+
+// Moves the runs of removed chunks whose readers have finished into the
+// free map; with wait, first waits for all of them.
+pic_status reclaim(pic_store *s, bool wait) {
+  std::vector<std::pair<hipEvent_t, std::vector<Run>>> keep;
+  for (auto &pr : s->pending) {
+    hipError_t e = wait ? hipEventSynchronize(pr.first) : hipEventQuery(pr.first);
+    if (e == hipErrorNotReady) {
+      keep.push_back(std::move(pr));
+      continue;
+    }
+    if (e != hipSuccess) return hip_fail(e, "removed-chunk event");
+    (void)hipEventDestroy(pr.first);
+    for (const Run &r : pr.second) {
+      free_run(s, r.page0, r.pages);
+      s->used -= (int64_t)r.pages * kTile;
+    }
+  }
+  s->pending.swap(keep);
+  return PIC_OK;
+}
+
+// Allocates `pages` pages: the first free run that is long enough, else the
+// longest free runs until the request is met. false if the pool is short.
+bool alloc_pages(pic_store *s, int64_t pages, std::vector<Run> &out) {
+  out.clear();
+  for (auto it = s->free_runs.begin(); it != s->free_runs.end(); ++it) {
+    if (it->second < pages) continue;
+    out.push_back(Run{it->first, (int32_t)pages, 0, 0});
+    const int64_t rest = it->second - pages, start = it->first + pages;
+    s->free_runs.erase(it);
+    if (rest > 0) s->free_runs.emplace(start, rest);
+    return true;
+  }
+  int64_t total = 0;
+  for (auto &fr : s->free_runs) total += fr.second;
+  if (total < pages) return false;
+  std::vector<std::pair<int64_t, int64_t>> runs(s->free_runs.begin(), s->free_runs.end());
+  std::stable_sort(runs.begin(), runs.end(),
+                   [](const std::pair<int64_t, int64_t> &a, const std::pair<int64_t, int64_t> &b) {
+                     return a.second > b.second;
+                   });
+  int64_t need = pages;
+  for (auto &r : runs) {
+    const int64_t take = std::min(need, r.second);
+    out.push_back(Run{r.first, (int32_t)take, 0, 0});
+    s->free_runs.erase(r.first);
+    if (take < r.second) s->free_runs.emplace(r.first + take, r.second - take);
+    need -= take;
+    if (need == 0) break;
+  }
+  std::sort(out.begin(), out.end(), [](const Run &a, const Run &b) { return a.page0 < b.page0; });
+  return true;
+}
+
+// Link-table entry of one run of a chunk in `layer`.
+LinkEntry run_entry(const pic_store *s, const Run &r, int32_t layer) {
+  const int64_t slot_tok_bytes = (s->k_tok_elems + s->v_tok_elems) * s->esz;
+  const int32_t lp = r.pages * kTile;
+  LinkEntry E{};
+  E.k = s->pool + (int64_t)layer * s->layer_bytes + r.page0 * kTile * slot_tok_bytes;
+  E.v = s->desc.kind == PIC_GQA ? (const char *)E.k + (int64_t)lp * s->k_tok_elems * s->esz : E.k;
+  E.len = r.ntok;
+  E.lp = lp;
+  return E;
+}
+
 bool check_offsets(const int32_t *a, int32_t n) {
   if (!a || a[0] != 0) return false;
   for (int32_t i = 0; i < n; ++i)
@@ -180,6 +280,7 @@ struct Plan {
   int32_t max_tiles = 0;
   bool self = false;             // requests carry own KV
   int64_t total_self = 0;        // own tokens over the batch
+  std::vector<uint64_t> ids;     // every linked chunk id (with repeats)
 };
 
 // Tensor arguments of a call against its plan.
@@ -229,6 +330,7 @@ pic_status plan_call(pic_store *s, const pic_link_req *req, int32_t n_q_heads, f
   const int64_t slot_tok_bytes = (s->k_tok_elems + s->v_tok_elems) * s->esz;
   P.links.clear();
   P.links.reserve(n_links + B);
+  P.ids.clear();
   P.reqs.resize(B);
   std::vector<int64_t> weight(B);
   for (int32_t r = 0; r < B; ++r) {
@@ -253,16 +355,15 @@ pic_status plan_call(pic_store *s, const pic_link_req *req, int32_t n_q_heads, f
         return fail(PIC_ERR_NOT_FOUND, "request %d link %d: chunk id 0x%llx not in the store", r,
                     c, (unsigned long long)id);
       const Slot &sl = it->second;
-      LinkEntry E;
-      E.k = s->pool + (int64_t)layer * s->layer_bytes + sl.off_tokens * slot_tok_bytes;
-      E.v = d.kind == PIC_GQA ? (const char *)E.k + (int64_t)sl.lp * s->k_tok_elems * s->esz : E.k;
-      E.len = (int32_t)sl.len;
-      E.lp = sl.lp;
-      E.tile0 = (int32_t)tiles;
-      E.tok0 = (int32_t)toks;
-      P.links.push_back(E);
-      tiles += sl.lp / kTile;
-      toks += sl.len;
+      for (const Run &run : sl.runs) {
+        LinkEntry E = run_entry(s, run, layer);
+        E.tile0 = (int32_t)tiles;
+        E.tok0 = (int32_t)toks;
+        P.links.push_back(E);
+        tiles += run.pages;
+        toks += run.ntok;
+      }
+      P.ids.push_back(id);
     }
     if (toks + R.ls > INT32_MAX / 2) return fail(PIC_ERR_INVALID, "request %d too long", r);
     R.doc_tiles = (int32_t)tiles;
@@ -572,6 +673,7 @@ pic_status pic_store_create(const pic_store_desc *desc, pic_store **out) {
   s->v_tok_elems = d.kind == PIC_GQA ? (int64_t)d.n_kv_heads * d.d_v : 0;
   s->n_layers = d.n_layers > 1 ? d.n_layers : 1;
   s->layer_bytes = s->capacity * (s->k_tok_elems + s->v_tok_elems) * s->esz;
+  s->free_runs.emplace(0, s->capacity / kTile);
   hipError_t e = hipGetDevice(&s->device);
   if (e == hipSuccess) e = hipMalloc((void **)&s->pool, (size_t)s->layer_bytes * s->n_layers);
   if (e != hipSuccess) {
@@ -594,6 +696,7 @@ pic_status pic_store_destroy(pic_store *s) {
     if (st.dev) (void)hipFree(st.dev);
     if (st.done) (void)hipEventDestroy(st.done);
   }
+  for (auto &pr : s->pending) (void)hipEventDestroy(pr.first);
   if (s->work) (void)hipFree(s->work);
   if (s->pool) (void)hipFree(s->pool);
   delete s;
@@ -610,10 +713,7 @@ pic_status pic_store_put(pic_store *s, uint64_t chunk_id, int64_t n_tokens, cons
   if (!gqa && v) return fail(PIC_ERR_INVALID, "v must be NULL for MLA");
   if (s->map.count(chunk_id)) return fail(PIC_ERR_EXISTS, "chunk id 0x%llx already stored",
                                           (unsigned long long)chunk_id);
-  const int64_t lp = round_up(n_tokens, kTile);
-  if (s->used + lp > s->capacity)
-    return fail(PIC_ERR_OOM, "pool full: %lld of %lld tokens used, chunk needs %lld",
-                (long long)s->used, (long long)s->capacity, (long long)lp);
+  const int64_t pages = round_up(n_tokens, kTile) / kTile;
   DeviceGuard dg(s->device);
   if (!dg.ok) return fail(PIC_ERR_HIP, "cannot select the store's device");
   for (const void *ptr : {k, v}) {
@@ -625,29 +725,78 @@ pic_status pic_store_put(pic_store *s, uint64_t chunk_id, int64_t n_tokens, cons
       return fail(PIC_ERR_INVALID, "k and v must be device memory");
     }
   }
+  // pages: free ones, else those of removed chunks whose readers are done,
+  // else wait for the remaining readers
+  std::vector<Run> runs;
+  pic_status rc = reclaim(s, false);
+  if (rc != PIC_OK) return rc;
+  if (!alloc_pages(s, pages, runs) && !s->pending.empty()) {
+    rc = reclaim(s, true);
+    if (rc != PIC_OK) return rc;
+    (void)alloc_pages(s, pages, runs);
+  }
+  if (runs.empty())
+    return fail(PIC_ERR_OOM, "pool full: %lld of %lld tokens in use, chunk needs %lld",
+                (long long)s->used, (long long)s->capacity, (long long)pages * kTile);
+  int32_t tok = 0;
+  for (Run &r : runs) {
+    r.tok0 = tok;
+    r.ntok = (int32_t)std::min<int64_t>((int64_t)r.pages * kTile, n_tokens - tok);
+    tok += r.ntok;
+  }
   const hipStream_t st = (hipStream_t)stream;
   const pic_store_desc &d = s->desc;
-  // layer l of the caller's buffers -> layer l of the slot
+  // layer l of the caller's buffers -> layer l of each run
   const int64_t k_src_layer = n_tokens * s->k_tok_elems * s->esz;
   const int64_t v_src_layer = n_tokens * s->v_tok_elems * s->esz;
-  for (int32_t l = 0; l < s->n_layers; ++l) {
-    char *kdst = s->pool + (int64_t)l * s->layer_bytes +
-                 s->used * (s->k_tok_elems + s->v_tok_elems) * s->esz;
-    hipError_t e = launch_put_rows((const char *)k + l * k_src_layer, kdst, n_tokens, (int32_t)lp,
-                                   d.n_kv_heads, d.d_k, s->esz, st);
-    if (e != hipSuccess) return hip_fail(e, "put_rows_kernel");
-    if (gqa) {
-      char *vdst = kdst + (size_t)lp * s->k_tok_elems * s->esz;
-      e = launch_put_transposed((const char *)v + l * v_src_layer, vdst, n_tokens, (int32_t)lp,
-                                d.n_kv_heads, d.d_v, s->esz, st);
-      if (e != hipSuccess) return hip_fail(e, "put_transposed_kernel");
+  hipError_t e = hipSuccess;
+  for (int32_t l = 0; l < s->n_layers && e == hipSuccess; ++l) {
+    for (const Run &r : runs) {
+      const LinkEntry E = run_entry(s, r, l);
+      const char *ksrc = (const char *)k + l * k_src_layer + (int64_t)r.tok0 * s->k_tok_elems * s->esz;
+      e = launch_put_rows(ksrc, (void *)E.k, r.ntok, E.lp, d.n_kv_heads, d.d_k, s->esz, st);
+      if (e != hipSuccess) break;
+      if (gqa) {
+        const char *vsrc =
+            (const char *)v + l * v_src_layer + (int64_t)r.tok0 * s->v_tok_elems * s->esz;
+        e = launch_put_transposed(vsrc, (void *)E.v, r.ntok, E.lp, d.n_kv_heads, d.d_v, s->esz, st);
+        if (e != hipSuccess) break;
+      }
     }
   }
-  // A slot is its K block followed by its V block; slot offsets count padded
-  // tokens of (K + V) elements.
-  Slot sl{s->used, n_tokens, (int32_t)lp};
-  s->used += lp;
-  s->map.emplace(chunk_id, sl);
+  if (e != hipSuccess) {
+    for (const Run &r : runs) free_run(s, r.page0, r.pages);
+    return hip_fail(e, "put kernels");
+  }
+  Slot sl;
+  sl.len = n_tokens;
+  sl.runs = std::move(runs);
+  s->used += pages * kTile;
+  s->map.emplace(chunk_id, std::move(sl));
+  return PIC_OK;
+}
+
+pic_status pic_store_remove(pic_store *s, uint64_t chunk_id, void *stream) {
+  if (!s) return fail(PIC_ERR_INVALID, "store is NULL");
+  auto it = s->map.find(chunk_id);
+  if (it == s->map.end()) return fail(PIC_ERR_NOT_FOUND, "chunk id 0x%llx not in the store",
+                                      (unsigned long long)chunk_id);
+  if (it->second.plan_refs > 0)
+    return fail(PIC_ERR_INVALID, "chunk id 0x%llx is linked by %lld live link plans",
+                (unsigned long long)chunk_id, (long long)it->second.plan_refs);
+  DeviceGuard dg(s->device);
+  if (!dg.ok) return fail(PIC_ERR_HIP, "cannot select the store's device");
+  // the pages are reused only after the work enqueued so far on `stream`
+  // (the calls that may read them) has completed
+  hipEvent_t ev = nullptr;
+  HIP_TRY(hipEventCreateWithFlags(&ev, hipEventDisableTiming), "hipEventCreate(remove)");
+  hipError_t e = hipEventRecord(ev, (hipStream_t)stream);
+  if (e != hipSuccess) {
+    (void)hipEventDestroy(ev);
+    return hip_fail(e, "hipEventRecord(remove)");
+  }
+  s->pending.emplace_back(ev, std::move(it->second.runs));
+  s->map.erase(it);
   return PIC_OK;
 }
 
@@ -751,6 +900,7 @@ pic_status pic_link_plan_create(pic_store *s, const pic_link_req *req, int32_t n
       return hip_fail(e, "hipMemcpy(plan tables)");
     }
   }
+  for (uint64_t id : P.ids) ++s->map.at(id).plan_refs;
   ++s->live_plans;
   *out = pl;
   return PIC_OK;
@@ -787,6 +937,10 @@ pic_status pic_link_plan_destroy(pic_link_plan *pl) {
     (void)hipDeviceSynchronize();
     (void)hipFree(pl->dev);
   }
+  for (uint64_t id : pl->C.P.ids) {
+    auto it = pl->store->map.find(id);
+    if (it != pl->store->map.end()) --it->second.plan_refs;
+  }
   --pl->store->live_plans;
   delete pl;
   return PIC_OK;
@@ -799,23 +953,22 @@ pic_status pic_debug_gather(pic_store *s, const uint64_t *ids, int32_t n, int32_
   if (layer < 0 || layer >= s->n_layers)
     return fail(PIC_ERR_INVALID, "layer %d outside the store's %d layers", layer, s->n_layers);
   const bool gqa = s->desc.kind == PIC_GQA;
-  std::vector<LinkEntry> links(n);
+  std::vector<LinkEntry> links;
+  links.reserve(n);
   int64_t toks = 0;
   for (int32_t i = 0; i < n; ++i) {
     auto it = s->map.find(ids[i]);
     if (it == s->map.end()) return fail(PIC_ERR_NOT_FOUND, "chunk id 0x%llx not in the store",
                                         (unsigned long long)ids[i]);
-    const Slot &sl = it->second;
-    LinkEntry &E = links[i];
-    E.k = s->pool + (int64_t)layer * s->layer_bytes +
-          sl.off_tokens * (s->k_tok_elems + s->v_tok_elems) * s->esz;
-    E.v = gqa ? (const char *)E.k + (int64_t)sl.lp * s->k_tok_elems * s->esz : E.k;
-    E.len = (int32_t)sl.len;
-    E.lp = sl.lp;
-    E.tile0 = 0;
-    E.tok0 = (int32_t)toks;
-    toks += sl.len;
+    for (const Run &r : it->second.runs) {
+      LinkEntry E = run_entry(s, r, layer);
+      E.tile0 = 0;
+      E.tok0 = (int32_t)toks;
+      links.push_back(E);
+      toks += r.ntok;
+    }
   }
+  n = (int32_t)links.size();
   if (toks == 0) return PIC_OK;
   if (!k_out || (gqa && !v_out)) return fail(PIC_ERR_INVALID, "k_out/v_out is NULL");
   if (!gqa && v_out) return fail(PIC_ERR_INVALID, "v_out must be NULL for MLA");

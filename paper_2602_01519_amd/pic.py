@@ -71,6 +71,7 @@ def lib():
             "pic_store_destroy": [vp],
             "pic_store_put": [vp, u64, i64, vp, vp, vp],
             "pic_store_lookup": [vp, u64, vp],
+            "pic_store_remove": [vp, u64, vp],
             "pic_store_usage": [vp, vp, vp, vp],
             "pic_link_attn": [vp, vp, i32, vp, vp, vp, f32, vp, vp, vp],
             "pic_link_decode": [vp, vp, i32, vp, vp, vp, f32, i32, vp, vp, vp],
@@ -156,6 +157,10 @@ class Store:
 
     def put(self, chunk_id: int, n_tokens: int, k, v, stream: Optional[int] = None):
         _check(lib().pic_store_put(self.handle, int(chunk_id), int(n_tokens), _ptr(k), _ptr(v), stream))
+
+    def remove(self, chunk_id: int, stream: Optional[int] = None):
+        """pic_store_remove: frees the chunk's pages once `stream`'s earlier work is done."""
+        _check(lib().pic_store_remove(self.handle, int(chunk_id), stream))
 
     def lookup(self, chunk_id: int) -> int:
         n = ctypes.c_int64()

@@ -55,6 +55,7 @@ def test_null_arguments_are_rejected():
     assert L.pic_store_put(None, 1, 1, None, None, None) == pic.ERR_INVALID
     n = ctypes.c_int64()
     assert L.pic_store_lookup(None, 1, ctypes.byref(n)) == pic.ERR_INVALID
+    assert L.pic_store_remove(None, 1, None) == pic.ERR_INVALID
     assert L.pic_store_usage(None, None, None, None) == pic.ERR_INVALID
     assert L.pic_link_attn(None, None, 8, None, None, None, 1.0, None, None, None) == pic.ERR_INVALID
     assert L.pic_link_decode(None, None, 8, None, None, None, 1.0, 0, None, None, None) == pic.ERR_INVALID
