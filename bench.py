@@ -119,6 +119,55 @@ def copy_calibration(args):
     return 0
 
 
+def projections(args):
+    """--projections: times pic_mla_absorb_q and pic_mla_up_v at the mla
+    workload's size (all its query tokens x 16 heads) and prints one JSON line
+    per kernel with its HBM roofline (these projections move more bytes than
+    they compute). Inputs: seeded N(0,1) activations, N(0,1/K) weights, bf16."""
+    import torch
+    from paper_2602_01519_amd import pic, runner
+    from paper_2602_01519_amd import workloads as W
+    cfg = W.CONFIGS["mla"]
+    T = sum(cfg.q_length(r) for r in range(cfg.batch))
+    H = cfg.n_q_heads
+    rng = np.random.default_rng(cfg.seed + 17)
+    bf = lambda shape, std=1.0: runner.to_device(
+        W.f32_to_bf16_bits(rng.standard_normal(shape, dtype=np.float32) * np.float32(std)), "cuda")
+    q, w_uk_t = bf((T, H, 192)), bf((H, 512, 128), 1 / np.sqrt(128))
+    o_lat, w_uv = bf((T, H, 512)), bf((H, 128, 512), 1 / np.sqrt(512))
+    q_out = torch.empty((T, H, 576), dtype=torch.int16, device="cuda")
+    out = torch.empty((T, H, 128), dtype=torch.int16, device="cuda")
+    st = torch.cuda.current_stream()
+    flops = 2.0 * T * H * 128 * 512
+    cases = [("pic_mla_absorb_q", lambda: pic.mla_absorb_q(T, H, q, w_uk_t, q_out, st.cuda_stream),
+              (T * H * (192 + 576) + H * 512 * 128) * 2),
+             ("pic_mla_up_v", lambda: pic.mla_up_v(T, H, o_lat, w_uv, out, st.cuda_stream),
+              (T * H * (512 + 128) + H * 128 * 512) * 2)]
+    for name, fn, nbytes in cases:
+        t_w = time.perf_counter()
+        n_w = 0
+        while n_w < args.warmup or time.perf_counter() - t_w < args.min_warmup_s:
+            fn()
+            n_w += 1
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(st)
+        for _ in range(args.steps):
+            fn()
+        e1.record(st)
+        torch.cuda.synchronize()
+        us = e0.elapsed_time(e1) / args.steps * 1e3
+        gbs = nbytes / (us * 1e-6) / 1e9
+        print(json.dumps({
+            "metric": "MLA projection HBM GB/s (algorithmic bytes) at 1 GPU", "entry": name,
+            "value": round(gbs, 1), "unit": "GB/s", "us_per_call": round(us, 3), "steps": args.steps,
+            "dtype": "bf16", "data": "synthetic", "config": {"tokens": T, "heads": H},
+            "algorithmic_bytes": nbytes, "flops": flops,
+            "roofline": {"bound": "hbm", "achieved": round(gbs, 1), "peak": PEAK_HBM_GBS,
+                         "unit": "GB/s", "frac": round(gbs / PEAK_HBM_GBS, 4)}}), flush=True)
+    return 0
+
+
 def algorithmic(cfg, wl):
     from paper_2602_01519_amd import workloads as W
     pairs = W.visible_pairs(cfg, wl.plan)
@@ -199,6 +248,8 @@ def main(argv=None):
     ap.add_argument("--summarize-traffic", nargs=4, metavar="CSV",
                     help="kernel FETCH_SIZE csv, kernel WRITE_SIZE csv, copy FETCH csv, copy WRITE csv")
     ap.add_argument("--kernel", default="link_mfma_d128_kernel")
+    ap.add_argument("--projections", action="store_true",
+                    help="time the MLA absorption / up-projection kernels instead (one line each)")
     args = ap.parse_args(argv)
     if args.summarize_traffic:
         return summarize_traffic(args)
@@ -218,6 +269,8 @@ def main(argv=None):
     torch.cuda.set_device(0)
     if args.copy_mib:
         return copy_calibration(args)
+    if args.projections:
+        return projections(args)
     cfg = W.CONFIGS[args.config]
     wl = W.make_workload(cfg)
     keep = set(int(c) for c in wl.plan.chunk_index[wl.plan.chunk_offsets[0]:wl.plan.chunk_offsets[min(4, wl.plan.batch)]])
