@@ -14,7 +14,7 @@
 //   online softmax on S^T (each lane holds one row's 32 scores)
 //   O^T[128][32 rows]    += V^T . P^T      16 x v_mfma_f32_32x32x16_bf16
 // K and V^T tiles are copied global -> LDS by the load-to-LDS path
-// (global_load_lds_dwordx4, no register staging), double-buffered in four
+// (buffer_load_dwordx4 ... lds, no register staging), double-buffered in four
 // distinct LDS arrays; the tile loop is unrolled by two so every access names
 // its buffer statically, which lets the compiler see that a tile's reads and
 // the next tile's copy never alias (no wait on the copy before the reads).
@@ -159,15 +159,24 @@ __device__ __forceinline__ TileRef tile_ref(Ctx &c, int t) {
 // swizzled layout (uniform base address + per-lane 32-bit offset).
 // Copy i (0 .. 2 kCopySets - 1) of a tile: i < kCopySets is K chunk set i,
 // the rest V^T chunk set i - kCopySets.
+// The copies go through a buffer resource (MUBUF load-to-LDS) rather than a
+// global (FLAT-encoded) one: the compiler counts a FLAT load-to-LDS as a
+// possible LDS access in flight, which turns every wait for an LDS fragment
+// read into a wait for all of them; with buffer copies it keeps precise
+// counts and the fragment reads stay ahead of their MFMAs.
+__device__ __forceinline__ void lds_dma16(const void *base, uint32_t voff, uint4 *dst) {
+  const __amdgpu_buffer_rsrc_t rs =
+      __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(base), (short)0, -1, 0x00020000);
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (lds_ptr)dst, 16, voff, 0, 0, 0);
+}
+
 __device__ __forceinline__ void tile_copy(const Ctx &c, int i, const TileRef &r, uint4 *kdst,
                                           uint4 *vdst) {
   if (i < kCopySets) {
-    __builtin_amdgcn_global_load_lds(r.k + c.koff[i], (lds_ptr)(kdst + (i * kWaves + c.wave) * 64),
-                                     16, 0, 0);
+    lds_dma16(r.k, c.koff[i], kdst + (i * kWaves + c.wave) * 64);
   } else {
     const int u = i - kCopySets;
-    __builtin_amdgcn_global_load_lds(r.v + (c.vrow[u] * (uint32_t)r.lp * 2u + c.vcol[u]),
-                                     (lds_ptr)(vdst + (u * kWaves + c.wave) * 64), 16, 0, 0);
+    lds_dma16(r.v, c.vrow[u] * (uint32_t)r.lp * 2u + c.vcol[u], vdst + (u * kWaves + c.wave) * 64);
   }
 }
 __device__ __forceinline__ void issue_tile(const Ctx &c, const TileRef &r, uint4 *kdst,

@@ -140,17 +140,24 @@ __device__ __forceinline__ TileRef tile_ref(Cursor &c, int t, int doc_tiles) {
 // for u = 0 (u = 1 adds 32 rows). The tile base is uniform, so each copy is
 // a scalar base plus one 32-bit lane offset; dst is the LDS byte address of
 // the buffer.
+// Copies go through a buffer resource (MUBUF load-to-LDS, base = the tile,
+// uniform part of the offset in soffset) rather than a global (FLAT-encoded)
+// load-to-LDS: the compiler counts the latter as a possible LDS access in
+// flight, which turns every wait for a fragment read into a wait for all
+// of them.
 __device__ __forceinline__ void tile_copy(int i, const char *k, uint32_t dst, int wave,
                                           uint32_t lat_off, uint32_t rope_off) {
+  const __amdgpu_buffer_rsrc_t rs =
+      __builtin_amdgcn_make_buffer_rsrc(const_cast<char *>(k), (short)0, -1, 0x00020000);
   if (i < kTile / 4) {
     const int r = 4 * i + wave;
-    __builtin_amdgcn_global_load_lds(k + r * kRowBytes + (lat_off ^ (16u * (i & 3))),
-                                     (lds_ptr)(uintptr_t)(dst + r * kLatChunks * 16), 16, 0, 0);
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (lds_ptr)(uintptr_t)(dst + r * kLatChunks * 16),
+                                             16, lat_off ^ (16u * (i & 3)), r * kRowBytes, 0, 0);
   } else {
     const int u = i - kTile / 4;
-    __builtin_amdgcn_global_load_lds(k + u * 32 * kRowBytes + rope_off,
-                                     (lds_ptr)(uintptr_t)(dst + (kRopeBase + u * 256 + wave * 64) * 16),
-                                     16, 0, 0);
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(
+        rs, (lds_ptr)(uintptr_t)(dst + (kRopeBase + u * 256 + wave * 64) * 16), 16, rope_off,
+        u * 32 * kRowBytes, 0, 0);
   }
 }
 constexpr int kCopies = kTile / 4 + 2;   // 18 copies per lane per tile
