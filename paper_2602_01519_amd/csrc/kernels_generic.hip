@@ -125,11 +125,15 @@ __global__ void gather_kernel(const LinkEntry *__restrict__ links, int32_t n_lin
 // transpose 64x64 tiles of V.
 
 struct PrepParams {
-  const ReqEntry *reqs;
-  const LinkEntry *links;
+  const ReqEntry *reqs;       // the call's tables: in the host-mapped staging buffer
+  const LinkEntry *links;     // while the copy slice moves them, else on the device
   const void *k_self, *v_self;
   int32_t heads, d_k, d_v, mla, esz;
   int32_t rows_blocks;        // blocks per request doing K rows
+  int32_t prep_z;             // z slices preparing own KV (one per request, or 0)
+  const uint4 *copy_src;      // table copy (z slice prep_z), n16 = 0: none
+  uint4 *copy_dst;
+  int64_t copy_n16;
 };
 
 // One 64-token x 64-value tile of own V, transposed into the slot's V block.
@@ -171,7 +175,18 @@ __device__ __forceinline__ void prep_transposed_tile(const ReqEntry &R, const Li
   }
 }
 
+// The call's prologue. z slices 0 .. prep_z-1 lay out request z's own KV
+// like a chunk slot; the last slice, if any, copies the call's link and
+// request tables from the host-mapped staging buffer to the device (read
+// over PCIe, latency-bound). The prep slices read their two table entries
+// where they are, so neither part waits for the other.
 __global__ void prep_own_kernel(PrepParams pp) {
+  if ((int)blockIdx.z == pp.prep_z) {
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < pp.copy_n16;
+         i += (int64_t)gridDim.x * blockDim.x)
+      pp.copy_dst[i] = pp.copy_src[i];
+    return;
+  }
   const ReqEntry R = pp.reqs[blockIdx.z];
   if (R.ls == 0) return;
   const LinkEntry L = pp.links[R.link0 + R.nlinks - 1];
@@ -585,12 +600,17 @@ hipError_t launch_gather(const LinkEntry *links, int32_t n_links, int64_t total_
   return hipGetLastError();
 }
 
-hipError_t launch_prep_own(const LinkParams &p, int32_t mla, int32_t esz, int32_t max_own_lp,
-                           hipStream_t st) {
+hipError_t launch_prologue(const LinkParams &p, const LinkEntry *links, const ReqEntry *reqs,
+                           int32_t mla, int32_t esz, int32_t max_own_lp, const void *copy_src,
+                           void *copy_dst, int64_t copy_bytes, hipStream_t st) {
   if (p.batch == 0) return hipSuccess;
   PrepParams pp;
-  pp.reqs = p.reqs;
-  pp.links = p.links;
+  pp.reqs = reqs;
+  pp.links = links;
+  pp.copy_src = (const uint4 *)copy_src;
+  pp.copy_dst = (uint4 *)copy_dst;
+  pp.copy_n16 = copy_bytes / 16;
+  pp.prep_z = max_own_lp > 0 ? p.batch : 0;
   pp.k_self = p.k_self;
   pp.v_self = p.v_self;
   pp.heads = p.n_kv_heads;
@@ -601,8 +621,11 @@ hipError_t launch_prep_own(const LinkParams &p, int32_t mla, int32_t esz, int32_
   const int64_t rows_vec = (int64_t)p.n_kv_heads * max_own_lp * (p.d_k * esz / 16);
   pp.rows_blocks = (int32_t)std::max<int64_t>(1, std::min<int64_t>((rows_vec + 1023) / 1024, 256));
   const int64_t tblocks = mla ? 0 : (int64_t)p.n_kv_heads * (max_own_lp / 64) * ((p.d_v + 63) / 64);
-  dim3 grid((unsigned)(pp.rows_blocks + tblocks), 1, p.batch);
-  hipLaunchKernelGGL(prep_own_kernel, grid, dim3(256), 0, st, pp);
+  const int64_t copy_blocks = std::min<int64_t>((pp.copy_n16 + 255) / 256, 64);
+  const int64_t gx = std::max<int64_t>(pp.prep_z ? pp.rows_blocks + tblocks : 0, copy_blocks);
+  const int gz = pp.prep_z + (pp.copy_n16 > 0 ? 1 : 0);
+  if (gx == 0 || gz == 0) return hipSuccess;
+  hipLaunchKernelGGL(prep_own_kernel, dim3((unsigned)gx, 1, (unsigned)gz), dim3(256), 0, st, pp);
   return hipGetLastError();
 }
 

@@ -393,10 +393,20 @@ pic_status plan_call(pic_store *s, const pic_link_req *req, int32_t n_q_heads, f
   return PIC_OK;
 }
 
-// Writes the plan's tables into a staging slot; with copy, also enqueues
-// their copy to the device.
+// Writes the plan's tables into a staging slot (host-mapped pinned memory)
+// and points lp's tables at the slot's device copy; the call's prologue
+// kernel moves them there.
 struct TableLayout {
   size_t off_r, off_o, bytes;
+};
+
+// Where the prologue reads the tables, and what it copies first.
+struct Prologue {
+  const LinkEntry *links = nullptr;
+  const ReqEntry *reqs = nullptr;
+  const void *copy_src = nullptr;
+  void *copy_dst = nullptr;
+  int64_t copy_bytes = 0;
 };
 
 pic_status upload(pic_store *s, const Plan &P, hipStream_t st, Stage **stage, LinkParams &lp,
@@ -412,8 +422,7 @@ pic_status upload(pic_store *s, const Plan &P, hipStream_t st, Stage **stage, Li
   if (nl) memcpy(h, P.links.data(), sizeof(LinkEntry) * nl);
   memcpy(h + off_r, P.reqs.data(), sizeof(ReqEntry) * nr);
   memcpy(h + off_o, P.order.data(), sizeof(int32_t) * nr);
-  HIP_TRY(launch_table_copy((*stage)->host_dev, (*stage)->dev, (int64_t)bytes, st),
-          "table_copy_kernel");
+  (void)st;
   char *dv = (char *)(*stage)->dev;
   lp.links = (const LinkEntry *)dv;
   lp.reqs = (const ReqEntry *)(dv + off_r);
@@ -562,8 +571,8 @@ void place_own(const pic_store *s, const Plan &P, void *work, LinkEntry *links) 
 // Enqueues a call whose tables are already on the device (lp.links, reqs,
 // order set): own-KV staging, the attention kernel, the split combine.
 pic_status launch_call(const pic_store *s, const Setup &C, LinkParams lp, void *work,
-                       const void *q, const void *k_self, const void *v_self, float scale,
-                       void *out, float *lse, hipStream_t st) {
+                       const Prologue &pro, const void *q, const void *k_self,
+                       const void *v_self, float scale, void *out, float *lse, hipStream_t st) {
   const pic_store_desc &d = s->desc;
   const bool mla = d.kind == PIC_MLA;
   lp.q = q;
@@ -578,9 +587,10 @@ pic_status launch_call(const pic_store *s, const Setup &C, LinkParams lp, void *
     lp.part_m = lp.part_o + rows * C.splits * d.d_v;
     lp.part_l = lp.part_m + rows * C.splits;
   }
-  if (C.P.max_own_lp > 0) {
-    hipError_t e = launch_prep_own(lp, mla, s->esz, C.P.max_own_lp, st);
-    if (e != hipSuccess) return hip_fail(e, "prep_own kernels");
+  if (C.P.max_own_lp > 0 || pro.copy_bytes > 0) {
+    hipError_t e = launch_prologue(lp, pro.links, pro.reqs, mla, s->esz, C.P.max_own_lp,
+                                   pro.copy_src, pro.copy_dst, pro.copy_bytes, st);
+    if (e != hipSuccess) return hip_fail(e, "prep_own_kernel");
   }
   std::pair<hipEvent_t, hipEvent_t> ev;
   const char *name = "";
@@ -627,7 +637,14 @@ pic_status link_call(pic_store *s, const pic_link_req *req, int32_t n_q_heads, c
   LinkParams lp = C.lp;
   rc = upload(s, C.P, st, &stage, lp, tl);
   if (rc != PIC_OK) return rc;
-  rc = launch_call(s, C, lp, s->work, q, k_self, v_self, scale, out, lse, st);
+  Prologue pro;
+  const char *hd = (const char *)stage->host_dev;
+  pro.links = (const LinkEntry *)hd;
+  pro.reqs = (const ReqEntry *)(hd + tl.off_r);
+  pro.copy_src = hd;
+  pro.copy_dst = stage->dev;
+  pro.copy_bytes = (int64_t)tl.bytes;
+  rc = launch_call(s, C, lp, s->work, pro, q, k_self, v_self, scale, out, lse, st);
   if (rc != PIC_OK) return rc;
   HIP_TRY(hipEventRecord(stage->done, st), "hipEventRecord(stage)");
   stage->pending = true;
@@ -926,7 +943,10 @@ pic_status pic_link_plan_run(pic_link_plan *pl, int32_t layer, const void *q, co
   lp.links = (const LinkEntry *)t;
   lp.reqs = (const ReqEntry *)(t + pl->off_r);
   lp.order = (const int32_t *)(t + pl->off_o);
-  return launch_call(s, pl->C, lp, pl->work, q, k_self, v_self, softmax_scale, out, lse,
+  Prologue pro;
+  pro.links = lp.links;
+  pro.reqs = lp.reqs;
+  return launch_call(s, pl->C, lp, pl->work, pro, q, k_self, v_self, softmax_scale, out, lse,
                      (hipStream_t)stream);
 }
 

@@ -84,8 +84,12 @@ hipError_t launch_mla_absorb_q(const void *q, const void *w_uk_t, void *q_out, i
                                int32_t n_heads, hipStream_t st);
 hipError_t launch_mla_up_v(const void *o_lat, const void *w_uv, void *out, int32_t n_tokens,
                            int32_t n_heads, hipStream_t st);
-hipError_t launch_prep_own(const LinkParams &p, int32_t mla, int32_t esz, int32_t max_own_lp,
-                           hipStream_t st);
+// The call's prologue: lays out the own KV of every request (when
+// max_own_lp > 0; tables read from links / reqs) and copies copy_bytes of
+// tables from copy_src to copy_dst (when copy_bytes > 0).
+hipError_t launch_prologue(const LinkParams &p, const LinkEntry *links, const ReqEntry *reqs,
+                           int32_t mla, int32_t esz, int32_t max_own_lp, const void *copy_src,
+                           void *copy_dst, int64_t copy_bytes, hipStream_t st);
 
 // Generic vector-ALU link attention: any d_k <= 576, d_v <= 512, fp32 or bf16.
 hipError_t launch_link_valu(const LinkParams &p, int dtype, int mla, hipStream_t st,
