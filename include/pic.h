@@ -130,7 +130,14 @@ pic_status pic_store_usage(const pic_store *store, int64_t *used_tokens,
  *     chunk_ids[chunk_offsets[r] .. chunk_offsets[r+1]-1]; an id may repeat.
  *   q_offsets: the query tokens of request r are rows q_offsets[r].. of q.
  *   self_offsets: own-KV tokens of request r (L_s >= L_q), or NULL for
- *     cross-attention only (no own KV, every row sees only the documents). */
+ *     cross-attention only (no own KV, every row sees only the documents).
+ *   chunk_starts: NULL (every link reads its whole chunk), or per link (same
+ *     indexing as chunk_ids) the first token of the chunk the link reads: a
+ *     multiple of 64 below the chunk's length. Lets a request splice chunk
+ *     caches, e.g. the link of post-training PIC that recomputes the first
+ *     tokens of every document (Sec. 1 and 2.2; Sec. 6.1 runs EPIC with 64
+ *     per document): link [the recomputed tokens, put as a chunk of their
+ *     own ; the cached chunk from token 64] for every document. */
 typedef struct pic_link_req {
   int32_t batch;
   int32_t layer;             /* the store layer whose chunk caches are read (0 for one layer) */
@@ -138,6 +145,7 @@ typedef struct pic_link_req {
   const uint64_t *chunk_ids;
   const int32_t *q_offsets;
   const int32_t *self_offsets;
+  const int32_t *chunk_starts;
 } pic_link_req;
 
 /* Link-stage attention for prefill-shaped requests (Sec. 4.1-4.2).

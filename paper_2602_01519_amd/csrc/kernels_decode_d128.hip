@@ -88,7 +88,7 @@ __device__ __forceinline__ TileInfo tile_info(Cursor &c, int t) {
   for (;;) {
     const LinkEntry &e = c.links[c.li];
     const int tile0 = uni(e.tile0) * (kTile / kT), lp = uni(e.lp);
-    if (t < tile0 + lp / kT) {
+    if (t < tile0 + (uni(e.len) + kTile - 1) / kTile * (kTile / kT)) {
       const int tt = t - tile0;
       TileInfo r;
       r.lp = lp;

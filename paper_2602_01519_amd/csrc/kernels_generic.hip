@@ -294,7 +294,7 @@ __global__ __launch_bounds__(256) void link_valu_kernel(LinkParams p) {
   for (int t = t_begin; t < t_end; ++t) {
     const bool own = t >= R.doc_tiles;
     __syncthreads();
-    while (p.links[R.link0 + li].tile0 + p.links[R.link0 + li].lp / kTile <= t) ++li;
+    while (p.links[R.link0 + li].tile0 + (p.links[R.link0 + li].len + kTile - 1) / kTile <= t) ++li;
     const LinkEntry E = p.links[R.link0 + li];
     const int tt = t - E.tile0;
     const int nvalid = min(kTile, E.len - tt * kTile);

@@ -134,7 +134,7 @@ __device__ __forceinline__ void cursor_load(Ctx &c) {
   c.llen = c.links[c.li].len;
   c.llp = c.links[c.li].lp;
   c.ltile0 = c.links[c.li].tile0;
-  c.lend = c.ltile0 + c.llp / kTile;
+  c.lend = c.ltile0 + (c.llen + kTile - 1) / kTile;
 }
 
 // Tile t of the request (t only grows across calls).

@@ -114,7 +114,7 @@ __device__ __forceinline__ void cursor_load(Cursor &c) {
   c.k = (const char *)c.links[c.li].k;
   c.len = c.links[c.li].len;
   c.tile0 = c.links[c.li].tile0;
-  c.end = c.tile0 + c.links[c.li].lp / kTile;
+  c.end = c.tile0 + (c.len + kTile - 1) / kTile;
 }
 
 // Tile t of the request (tiles are visited in increasing order).

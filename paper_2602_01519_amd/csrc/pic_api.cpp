@@ -355,13 +355,25 @@ pic_status plan_call(pic_store *s, const pic_link_req *req, int32_t n_q_heads, f
         return fail(PIC_ERR_NOT_FOUND, "request %d link %d: chunk id 0x%llx not in the store", r,
                     c, (unsigned long long)id);
       const Slot &sl = it->second;
+      const int32_t start = req->chunk_starts ? req->chunk_starts[c0 + c] : 0;
+      if (start < 0 || start % kTile || start >= sl.len)
+        return fail(PIC_ERR_INVALID,
+                    "request %d link %d: start %d must be a multiple of %d below the chunk's %lld "
+                    "tokens", r, c, start, kTile, (long long)sl.len);
       for (const Run &run : sl.runs) {
+        if (run.tok0 + run.ntok <= start) continue;
         LinkEntry E = run_entry(s, run, layer);
+        // skip the run's pages before `start`: rows of K, columns of V^T
+        // (the row stride stays the run's)
+        const int32_t skip = std::max(0, start - run.tok0);
+        E.k = (const char *)E.k + (int64_t)skip * d.d_k * s->esz;
+        E.v = d.kind == PIC_MLA ? E.k : (const char *)E.v + (int64_t)skip * s->esz;
+        E.len -= skip;
         E.tile0 = (int32_t)tiles;
         E.tok0 = (int32_t)toks;
         P.links.push_back(E);
-        tiles += run.pages;
-        toks += run.ntok;
+        tiles += (E.len + kTile - 1) / kTile;
+        toks += E.len;
       }
       P.ids.push_back(id);
     }

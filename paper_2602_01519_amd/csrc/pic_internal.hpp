@@ -27,8 +27,8 @@ constexpr int kTile = 64;
 struct LinkEntry {        // one link of one request, in link order
   const void *k;          // K block of the slot
   const void *v;          // GQA: V block; MLA: same as k
-  int32_t len;            // tokens
-  int32_t lp;             // padded tokens (multiple of kTile)
+  int32_t len;            // tokens; the link spans ceil(len / kTile) tiles
+  int32_t lp;             // row stride of its K / V^T blocks in tokens (multiple of kTile)
   int32_t tile0;          // index of the link's first tile within the request
   int32_t tok0;           // index of the link's first token within the request
 };

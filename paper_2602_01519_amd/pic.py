@@ -51,7 +51,8 @@ class StoreDesc(ctypes.Structure):
 class LinkReq(ctypes.Structure):
     _fields_ = [("batch", ctypes.c_int32), ("layer", ctypes.c_int32),
                 ("chunk_offsets", ctypes.c_void_p), ("chunk_ids", ctypes.c_void_p),
-                ("q_offsets", ctypes.c_void_p), ("self_offsets", ctypes.c_void_p)]
+                ("q_offsets", ctypes.c_void_p), ("self_offsets", ctypes.c_void_p),
+                ("chunk_starts", ctypes.c_void_p)]
 
 
 def lib_path() -> str:
@@ -173,32 +174,35 @@ class Store:
         return u.value, c.value, n.value
 
 
-def _req(chunk_offsets, chunk_ids, q_offsets, self_offsets, keep: list, layer: int = 0):
+def _req(chunk_offsets, chunk_ids, q_offsets, self_offsets, keep: list, layer: int = 0,
+         chunk_starts=None):
     co = _host_i32(chunk_offsets)
     ids = np.ascontiguousarray(chunk_ids, dtype=np.uint64)
     qo = _host_i32(q_offsets)
     so = _host_i32(self_offsets)
-    keep += [co, ids, qo, so]
+    st = _host_i32(chunk_starts)
+    keep += [co, ids, qo, so, st]
     return LinkReq(len(qo) - 1, int(layer), co.ctypes.data, ids.ctypes.data if ids.size else None,
-                   qo.ctypes.data, None if so is None else so.ctypes.data)
+                   qo.ctypes.data, None if so is None else so.ctypes.data,
+                   None if st is None or not st.size else st.ctypes.data)
 
 
 def link_attn(store: Store, chunk_offsets, chunk_ids, q_offsets, self_offsets, n_q_heads: int, q,
               k_self, v_self, softmax_scale: float, out, lse=None, stream: Optional[int] = None,
-              layer: int = 0):
+              layer: int = 0, chunk_starts=None):
     """pic_link_attn: prefill-shaped link attention on store layer `layer`."""
     keep: list = []
-    req = _req(chunk_offsets, chunk_ids, q_offsets, self_offsets, keep, layer)
+    req = _req(chunk_offsets, chunk_ids, q_offsets, self_offsets, keep, layer, chunk_starts)
     _check(lib().pic_link_attn(store.handle, ctypes.byref(req), int(n_q_heads), _ptr(q), _ptr(k_self),
                                _ptr(v_self), float(softmax_scale), _ptr(out), _ptr(lse), stream))
 
 
 def link_decode(store: Store, chunk_offsets, chunk_ids, q_offsets, self_offsets, n_q_heads: int, q,
                 k_self, v_self, softmax_scale: float, out, lse=None, num_splits: int = 0,
-                stream: Optional[int] = None, layer: int = 0):
+                stream: Optional[int] = None, layer: int = 0, chunk_starts=None):
     """pic_link_decode: decode-shaped link attention with split-K on store layer `layer`."""
     keep: list = []
-    req = _req(chunk_offsets, chunk_ids, q_offsets, self_offsets, keep, layer)
+    req = _req(chunk_offsets, chunk_ids, q_offsets, self_offsets, keep, layer, chunk_starts)
     _check(lib().pic_link_decode(store.handle, ctypes.byref(req), int(n_q_heads), _ptr(q), _ptr(k_self),
                                  _ptr(v_self), float(softmax_scale), int(num_splits), _ptr(out),
                                  _ptr(lse), stream))
@@ -215,9 +219,9 @@ class LinkPlan:
     """pic_link_plan_*: a request batch resolved once, run per layer / decode step."""
 
     def __init__(self, store: Store, chunk_offsets, chunk_ids, q_offsets, self_offsets, n_q_heads: int,
-                 mode: int = PREFILL, num_splits: int = 0):
+                 mode: int = PREFILL, num_splits: int = 0, chunk_starts=None):
         keep: list = []
-        req = _req(chunk_offsets, chunk_ids, q_offsets, self_offsets, keep)
+        req = _req(chunk_offsets, chunk_ids, q_offsets, self_offsets, keep, chunk_starts=chunk_starts)
         h = ctypes.c_void_p()
         _check(lib().pic_link_plan_create(store.handle, ctypes.byref(req), int(n_q_heads), int(mode),
                                           int(num_splits), ctypes.byref(h)))
