@@ -48,7 +48,13 @@ template <int K, int N, bool kRope>
 __global__ __launch_bounds__(256, 1) void proj_kernel(ProjArgs p) {
   static_assert((K == 128 && N == 512) || (K == 512 && N == 128), "one 128 x 128 slice per wave");
   constexpr bool kSplitK = K > 128;
-  __shared__ float red[kSplitK ? 4 * 32 * 128 : 1];     // partial tiles of the k slices
+  // K = 512: the four waves' partial tiles, [wave][token][n] fp32 with rows
+  // padded to 132 floats.
+  // K = 128: each wave's bf16 output tile, [token][n] with rows padded to
+  // 272 bytes, so that the stores go out as whole 256-byte row pieces.
+  constexpr int kOutRow = 136;                          // bf16 per padded row
+  constexpr int kRedRow = 132;
+  __shared__ __attribute__((aligned(16))) float red[kSplitK ? 4 * 32 * kRedRow : 4 * 32 * kOutRow / 2];
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int parts = p.parts;
@@ -111,36 +117,42 @@ __global__ __launch_bounds__(256, 1) void proj_kernel(ProjArgs p) {
       for (int nt = 0; nt < 4; ++nt)
         acc[nt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(w[nt][s], b[s], acc[nt], 0, 0, 0);
 
-    // C^T tile: lane holds token t and n = nt*32 + jj*8 + g*4 + (0..3)
+    // C^T tile: lane holds token t and n = nt*32 + jj*8 + g*4 + (0..3).
+    // Stores: 16 bytes per lane.
     if (kSplitK) {
-      // partial tiles to LDS as [wave][n][token], then wave w adds the four
-      // partials of n tile w and stores it
-      float *mine = red + wave * 32 * 128;
+      // partial tiles to LDS as [wave][token][n]; then every thread adds the
+      // four partials of 8 consecutive n of one token (2 pieces per thread,
+      // consecutive lanes on consecutive tokens)
+      float *mine = red + wave * 32 * kRedRow;
 #pragma unroll
       for (int nt = 0; nt < 4; ++nt)
 #pragma unroll
-        for (int x = 0; x < 16; ++x)
-          mine[(nt * 32 + (x >> 2) * 8 + g * 4 + (x & 3)) * 32 + (lane & 31)] = acc[nt][x];
+        for (int jj = 0; jj < 4; ++jj)
+          *(float4 *)(mine + (lane & 31) * kRedRow + nt * 32 + jj * 8 + g * 4) =
+              make_float4(acc[nt][jj * 4], acc[nt][jj * 4 + 1], acc[nt][jj * 4 + 2],
+                          acc[nt][jj * 4 + 3]);
       __syncthreads();
-      if (tv) {
-        uint16_t *crow = ch + (int64_t)t * p.c_tok;
 #pragma unroll
-        for (int jj = 0; jj < 4; ++jj) {
-          __bf16 v4[4];
+      for (int j = 0; j < 2; ++j) {
+        const int piece = threadIdx.x + 256 * j, tok = piece & 31, nb = (piece >> 5) * 8;
+        float sum[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-          for (int x = 0; x < 4; ++x) {
-            const int n = wave * 32 + jj * 8 + g * 4 + x;
-            float sum = 0.f;
-#pragma unroll
-            for (int q = 0; q < 4; ++q) sum += red[q * 32 * 128 + n * 32 + (lane & 31)];
-            v4[x] = (__bf16)sum;
-          }
-          *(uint2 *)(crow + wave * 32 + jj * 8 + g * 4) = __builtin_bit_cast(uint2, v4);
+        for (int q = 0; q < 4; ++q) {
+          const float4 a = *(const float4 *)(red + (q * 32 + tok) * kRedRow + nb);
+          const float4 b = *(const float4 *)(red + (q * 32 + tok) * kRedRow + nb + 4);
+          sum[0] += a.x, sum[1] += a.y, sum[2] += a.z, sum[3] += a.w;
+          sum[4] += b.x, sum[5] += b.y, sum[6] += b.z, sum[7] += b.w;
         }
+        __bf16 v8[8];
+#pragma unroll
+        for (int x = 0; x < 8; ++x) v8[x] = (__bf16)sum[x];
+        if (tb * 32 + tok < p.n_tokens)
+          *(uint4 *)(ch + (int64_t)(tb * 32 + tok) * p.c_tok + nb) = __builtin_bit_cast(uint4, v8);
       }
       __syncthreads();      // before the next block overwrites the partials
-    } else if (tv) {
-      uint16_t *crow = ch + (int64_t)t * p.c_tok + n0;
+    } else {
+      // this wave's tile to LDS as bf16 [token][n], then row pieces out
+      uint16_t *mine = (uint16_t *)red + wave * 32 * kOutRow;
 #pragma unroll
       for (int nt = 0; nt < 4; ++nt)
 #pragma unroll
@@ -148,8 +160,18 @@ __global__ __launch_bounds__(256, 1) void proj_kernel(ProjArgs p) {
           __bf16 v4[4];
 #pragma unroll
           for (int x = 0; x < 4; ++x) v4[x] = (__bf16)acc[nt][jj * 4 + x];
-          *(uint2 *)(crow + nt * 32 + jj * 8 + g * 4) = __builtin_bit_cast(uint2, v4);
+          *(uint2 *)(mine + (lane & 31) * kOutRow + nt * 32 + jj * 8 + g * 4) =
+              __builtin_bit_cast(uint2, v4);
         }
+      // (a wave's LDS accesses complete in order: the reads see the writes)
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        const int piece = lane + 64 * j, tok = piece >> 4, nb = (piece & 15) * 8;
+        const uint4 v = *(const uint4 *)(mine + tok * kOutRow + nb);
+        if (tb * 32 + tok < p.n_tokens)
+          *(uint4 *)(ch + (int64_t)(tb * 32 + tok) * p.c_tok + n0 + nb) = v;
+      }
+      __builtin_amdgcn_wave_barrier();      // reads done before the next block's writes
     }
 #pragma unroll
     for (int st = 0; st < 8; ++st) b[st] = bn[st];
