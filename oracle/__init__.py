@@ -46,7 +46,7 @@ def _load():
         vp = ctypes.c_void_p
         lib.oracle_link_attn.restype = ctypes.c_int
         lib.oracle_link_attn.argtypes = [ctypes.c_int] * 7 + [vp] * 4 + [vp] * 2 + [vp] * 3 + \
-            [ctypes.c_double, vp, vp, vp]
+            [ctypes.c_double, vp, vp, vp, vp]
         lib.oracle_num_threads.restype = ctypes.c_int
         _lib = lib
     return _lib
@@ -64,12 +64,15 @@ def link_attn(*, dtype: int, mla: bool, n_q_heads: int, d_v: int,
               links: Sequence[Sequence[tuple]], q: np.ndarray, q_offsets: np.ndarray,
               k_self: Optional[np.ndarray] = None, v_self: Optional[np.ndarray] = None,
               self_offsets: Optional[np.ndarray] = None, tau: float,
+              q_doc_limits: Optional[np.ndarray] = None,
               row_select: Optional[np.ndarray] = None):
     """Reference output and log-sum-exp.
 
     links[r] is the ordered list of (k, v) chunk tensors request r links:
     k token-major [len, H_kv, d_k], v [len, H_kv, d_v] (None for MLA).
     q is [Tq, H_q, d_k]; own KV is [Ts, H_kv, d_*] with self_offsets, or absent.
+    q_doc_limits[t], if given, is the number of leading document rows of its
+    request that query token t sees (the rest of the documents are masked).
     bf16 tensors are passed as uint16 bit patterns, fp32 ones as float32.
     Returns (out float64 [Tq, H_q, d_v], lse float64 [Tq, H_q]).
     """
@@ -112,6 +115,9 @@ def link_attn(*, dtype: int, mla: bool, n_q_heads: int, d_v: int,
     so = None if self_offsets is None else np.ascontiguousarray(self_offsets, dtype=np.int32)
     out = np.zeros((tq, hq, d_v), np.float64)
     lse = np.zeros((tq, hq), np.float64)
+    lims = None if q_doc_limits is None else np.ascontiguousarray(q_doc_limits, dtype=np.int32)
+    if lims is not None:
+        assert lims.shape == (tq,)
     sel = None if row_select is None else np.ascontiguousarray(row_select, dtype=np.uint8)
     if sel is not None:
         assert sel.size == tq * hq
@@ -119,7 +125,7 @@ def link_attn(*, dtype: int, mla: bool, n_q_heads: int, d_v: int,
                               _ptr(offs), ctypes.cast(karr, ctypes.c_void_p),
                               ctypes.cast(varr, ctypes.c_void_p), _ptr(larr), _ptr(q_offsets),
                               _ptr(so), _ptr(q), _ptr(k_self), _ptr(v_self if not mla else None),
-                              float(tau), _ptr(sel), _ptr(out), _ptr(lse))
+                              float(tau), _ptr(lims), _ptr(sel), _ptr(out), _ptr(lse))
     if rc != 0:
         raise ValueError("oracle rejected its arguments")
     return out, lse

@@ -18,6 +18,11 @@
  *     masked self-attention (Sec. 4.1, Eq. 2). Queries are the last L_q of
  *     the L_s own tokens (during decoding new tokens are appended to the
  *     query sequence, Sec. 4), so row i sees own rows 0 .. i + L_s - L_q.
+ *   * Optionally, query token t sees only the first q_doc_limits[t] document
+ *     rows (the attention side of post-training PIC, Sec. 2 and 6.1:
+ *     recomputed tokens attend as in an ordinary prefill of the concatenated
+ *     prompt, i.e. causally by their position in it, and every other query
+ *     sees all document rows).
  *   * One softmax over the union of visible keys, scaled by tau (Eq. 2 and
  *     Eq. 7 use 1/sqrt(d); here tau is an argument), then H = A V (Eq. 3, 8).
  *   * Multi-head: query head h reads KV head h / (H_q / H_kv) (the paper
@@ -76,6 +81,9 @@ static void widen_rows(double *dst, const void *src, int64_t n, int heads, int w
  *   q_offsets    int32 [batch+1] query tokens per request (q is [Tq][H_q][d_k])
  *   self_offsets int32 [batch+1] own tokens per request, or NULL (no own KV)
  *   k_self       [Ts][H_kv][d_k];  v_self [Ts][H_kv][d_v] (ignored when mla)
+ *   q_doc_limits int32 [Tq]: document rows 0 .. q_doc_limits[t]-1 are visible to
+ *                query token t (0 <= limit <= the request's document rows), or
+ *                NULL = all
  *   row_select   uint8 [Tq*H_q] (1 = compute this (token, head)), or NULL = all
  *   out          double [Tq][H_q][d_v];  lse double [Tq][H_q]
  * Returns 0, or -1 on inconsistent arguments (nothing written then).
@@ -85,7 +93,8 @@ int oracle_link_attn(int dtype, int mla, int batch, int n_q_heads, int n_kv_head
                      const void *const *link_v, const int64_t *link_len,
                      const int32_t *q_offsets, const int32_t *self_offsets, const void *q,
                      const void *k_self, const void *v_self, double tau,
-                     const uint8_t *row_select, double *out, double *lse) {
+                     const int32_t *q_doc_limits, const uint8_t *row_select, double *out,
+                     double *lse) {
   if (batch < 0 || n_q_heads <= 0 || n_kv_heads <= 0 || n_q_heads % n_kv_heads) return -1;
   if (d_k <= 0 || d_v <= 0 || (mla && (n_kv_heads != 1 || d_v > d_k))) return -1;
   const int group = n_q_heads / n_kv_heads;
@@ -98,6 +107,11 @@ int oracle_link_attn(int dtype, int mla, int batch, int n_q_heads, int n_kv_head
     /* Materialise the request's linked document KV, in link order. */
     int64_t ld = 0;
     for (int c = link_offsets[r]; c < link_offsets[r + 1]; ++c) ld += link_len[c];
+    if (q_doc_limits)
+      for (int64_t i = 0; i < lq; ++i) {
+        const int64_t lim = q_doc_limits[q_offsets[r] + i];
+        if (lim < 0 || lim > ld) return -1;
+      }
     const int64_t nkeys = ld + ls;
     double *kc = malloc(sizeof(double) * (size_t)(nkeys > 0 ? nkeys : 1) * n_kv_heads * d_k);
     double *vc = malloc(sizeof(double) * (size_t)(nkeys > 0 ? nkeys : 1) * n_kv_heads * d_v);
@@ -142,20 +156,25 @@ int oracle_link_attn(int dtype, int mla, int batch, int n_q_heads, int n_kv_head
         if (row_select && !row_select[orow]) continue;
         const int kv = h / group;
         for (int e = 0; e < d_k; ++e) qi[e] = widen(q, orow * d_k + e, dtype);
-        /* Visible keys: all documents, then own rows 0 .. i + ls - lq. */
-        const int64_t nvis = ld + (self_offsets ? i + 1 + ls - lq : 0);
+        /* Visible keys, numbered u = 0 .. nvis-1: document rows 0 .. dvis-1
+         * (all of them unless limited), then own rows 0 .. i + ls - lq, which
+         * sit at ld .. in kc / vc. */
+        const int64_t dvis = q_doc_limits ? q_doc_limits[q0 + i] : ld;
+        const int64_t nvis = dvis + (self_offsets ? i + 1 + ls - lq : 0);
         double m = -INFINITY;
-        for (int64_t j = 0; j < nvis; ++j) {
+        for (int64_t u = 0; u < nvis; ++u) {
+          const int64_t j = u < dvis ? u : ld + (u - dvis);
           const double *kj = kc + (j * n_kv_heads + kv) * d_k;
           double dot = 0.0;
           for (int e = 0; e < d_k; ++e) dot += qi[e] * kj[e];
-          s[j] = tau * dot;
-          if (s[j] > m) m = s[j];
+          s[u] = tau * dot;
+          if (s[u] > m) m = s[u];
         }
         for (int e = 0; e < d_v; ++e) acc[e] = 0.0;
         double l = 0.0;
-        for (int64_t j = 0; j < nvis; ++j) {
-          const double p = exp(s[j] - m);
+        for (int64_t u = 0; u < nvis; ++u) {
+          const int64_t j = u < dvis ? u : ld + (u - dvis);
+          const double p = exp(s[u] - m);
           const double *vj = vc + (j * n_kv_heads + kv) * d_v;
           l += p;
           for (int e = 0; e < d_v; ++e) acc[e] += p * vj[e];

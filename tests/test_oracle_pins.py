@@ -15,7 +15,11 @@ special case:
   boundaries), GQA = MHA on repeated KV, log-sum-exp merge of the document
   and own parts;
 * MLA absorbed form = the non-absorbed form with explicit up-projections;
-* empty key sets.
+* empty key sets;
+* per-query document limits (the attention of tokens recomputed at link
+  time, Sec. 2 and 6.1): with limit = position + 1 the oracle's rows are the
+  rows of an ordinary causal prefill of the concatenated documents (torch
+  SDPA, is_causal), and with own KV they match an explicit mask.
 
 The paper prints no worked numeric example, so none of the pins is a
 printed value.
@@ -71,8 +75,9 @@ def run_oracle(chunks, q, ks, vs, *, dtype, tau, dv, mla=False):
                             self_offsets=so, tau=tau)
 
 
-def sdpa_reference(chunks, q, ks, vs, *, dtype, tau, dv, mla=False):
-    """torch fp64 SDPA over the explicitly concatenated KV with an explicit mask."""
+def sdpa_reference(chunks, q, ks, vs, *, dtype, tau, dv, mla=False, doc_limits=None):
+    """torch fp64 SDPA over the explicitly concatenated KV with an explicit mask
+    (query t sees document rows 0 .. doc_limits[t]-1 when limits are given)."""
     hq = q.shape[1]
     parts_k = [widen(k, dtype) for k, _ in chunks]
     parts_v = [widen(k, dtype)[:, :, :dv] if mla else widen(v, dtype) for k, v in chunks]
@@ -91,6 +96,8 @@ def sdpa_reference(chunks, q, ks, vs, *, dtype, tau, dv, mla=False):
     Q = torch.from_numpy(widen(q, dtype)).permute(1, 0, 2)   # [hq, lq, dk]
     mask = torch.zeros(lq, ld + ls, dtype=torch.bool)
     mask[:, :ld] = True
+    if doc_limits is not None:
+        mask[:, :ld] = torch.arange(ld)[None, :] < torch.as_tensor(doc_limits)[:, None]
     if ks is not None:
         i = torch.arange(lq)[:, None]
         j = torch.arange(ls)[None, :]
@@ -521,3 +528,79 @@ def test_multi_request_batch_equals_per_request_calls():
         o, l = run_oracle(links, wl.q[qs], wl.k_self[ss], wl.v_self[ss], dtype=W.BF16,
                           tau=float(np.float32(cfg.scale)), dv=16)
         assert np.array_equal(o, out[qs]) and np.array_equal(l, lse[qs])
+
+
+# ---------------------------------------------------------------------------
+# per-query document limits
+
+
+def causal_prefill_reference(chunks, q_all, *, dtype, tau, dv, mla=False):
+    """Every token of the concatenated documents attending causally to the
+    prompt before it (torch fp64 SDPA with is_causal): what an exact prefill
+    of [doc_1 ; ... ; doc_n] computes for each position."""
+    K = np.concatenate([widen(k, dtype) for k, _ in chunks])
+    V = np.concatenate([widen(k, dtype)[:, :, :dv] if mla else widen(v, dtype) for k, v in chunks])
+    g = q_all.shape[1] // K.shape[1]
+    K = torch.from_numpy(K).permute(1, 0, 2).repeat_interleave(g, dim=0)
+    V = torch.from_numpy(V).permute(1, 0, 2).repeat_interleave(g, dim=0)
+    Q = torch.from_numpy(widen(q_all, dtype)).permute(1, 0, 2)
+    out = torch.nn.functional.scaled_dot_product_attention(Q, K, V, is_causal=True, scale=tau)
+    n = K.shape[1]
+    scores = torch.matmul(Q, K.transpose(1, 2)) * tau
+    scores = scores.masked_fill(torch.ones(n, n, dtype=torch.bool).triu(1), -math.inf)
+    return out.permute(1, 0, 2).numpy(), torch.logsumexp(scores, dim=-1).permute(1, 0).numpy()
+
+
+@pytest.mark.parametrize("dtype,mla", [(W.F32, False), (W.BF16, False), (W.BF16, True)])
+def test_doc_limits_are_rows_of_a_causal_prefill(dtype, mla):
+    """Recomputed tokens at positions P see document rows 0..P: with limits
+    P + 1 and no own KV, the oracle's rows equal those rows of a causal
+    prefill of the concatenated documents."""
+    rng = np.random.default_rng(31 + dtype + 2 * mla)
+    dk, dv = (12, 8) if mla else (8, 8)
+    chunks, _, _, _ = make_case(rng, dtype=dtype, n_chunks=3, lens=[7, 12, 5], hq=4, hkv=2, dk=dk,
+                                dv=dv, lq=1, ls=None, mla=mla)
+    ld = 24
+    q_all = rand(rng, (ld, 4, dk), dtype)
+    tau = 0.4
+    ref, ref_lse = causal_prefill_reference(chunks, q_all, dtype=dtype, tau=tau, dv=dv, mla=mla)
+    sel = np.unique(np.concatenate([[0, 6, 7, ld - 1], rng.choice(ld, 6, replace=False)]))
+    out, lse = oracle.link_attn(dtype=dtype, mla=mla, n_q_heads=4, d_v=dv, links=[chunks],
+                                q=q_all[sel], q_offsets=np.array([0, sel.size], np.int32), tau=tau,
+                                q_doc_limits=(sel + 1).astype(np.int32))
+    assert_close(out, ref[sel])
+    assert_close(lse, ref_lse[sel])
+
+
+def test_doc_limits_with_own_kv_match_explicit_mask():
+    rng = np.random.default_rng(33)
+    chunks, q, ks, vs = make_case(rng, dtype=W.BF16, n_chunks=2, lens=[9, 6], hq=4, hkv=2, dk=8, dv=6,
+                                  lq=5, ls=7)
+    lims = np.array([0, 15, 3, 9, 14], np.int32)
+    ref, ref_lse, _ = sdpa_reference(chunks, q, ks, vs, dtype=W.BF16, tau=0.3, dv=6, doc_limits=lims)
+    out, lse = oracle.link_attn(dtype=W.BF16, mla=False, n_q_heads=4, d_v=6, links=[chunks], q=q,
+                                q_offsets=np.array([0, 5], np.int32), k_self=ks, v_self=vs,
+                                self_offsets=np.array([0, 7], np.int32), tau=0.3, q_doc_limits=lims)
+    assert_close(out, ref)
+    assert_close(lse, ref_lse)
+    # full limits are no limits
+    full, full_lse = oracle.link_attn(dtype=W.BF16, mla=False, n_q_heads=4, d_v=6, links=[chunks], q=q,
+                                      q_offsets=np.array([0, 5], np.int32), k_self=ks, v_self=vs,
+                                      self_offsets=np.array([0, 7], np.int32), tau=0.3,
+                                      q_doc_limits=np.full(5, 15, np.int32))
+    plain, plain_lse = run_oracle(chunks, q, ks, vs, dtype=W.BF16, tau=0.3, dv=6)
+    assert np.array_equal(full, plain) and np.array_equal(full_lse, plain_lse)
+
+
+def test_doc_limits_zero_and_out_of_range():
+    rng = np.random.default_rng(35)
+    chunks, q, _, _ = make_case(rng, dtype=W.F32, n_chunks=2, lens=[4, 4], hq=2, hkv=2, dk=4, dv=4,
+                                lq=2, ls=None)
+    kw = dict(dtype=W.F32, mla=False, n_q_heads=2, d_v=4, links=[chunks], q=q,
+              q_offsets=np.array([0, 2], np.int32), tau=1.0)
+    out, lse = oracle.link_attn(**kw, q_doc_limits=np.array([0, 1], np.int32))
+    assert np.all(out[0] == 0) and np.all(np.isneginf(lse[0]))
+    assert np.array_equal(out[1], widen(chunks[0][1], W.F32)[0])   # one key: its value
+    for bad in ([9, 1], [-1, 1]):
+        with pytest.raises(ValueError):
+            oracle.link_attn(**kw, q_doc_limits=np.array(bad, np.int32))
