@@ -114,6 +114,32 @@ pic_status pic_store_put(pic_store *store, uint64_t chunk_id, int64_t n_tokens, 
  * NOT_FOUND, HIP. */
 pic_status pic_store_remove(pic_store *store, uint64_t chunk_id, void *stream);
 
+/* A chunk that differs from a stored one in a few rows, for the link stage
+ * of post-training PIC, which recomputes selected tokens of each document
+ * and attends over the cached KV with those rows replaced (Sec. 2: EPIC
+ * recomputes the first tokens of every chunk, CacheBlend the tokens whose
+ * cached KV deviates most; Sec. 6.1 runs CacheBlend at 20%).
+ * pic_store_derive: new_id becomes a chunk with base_id's length and
+ *   content. The 64-token pages that hold `rows` (host int32 [n_rows],
+ *   strictly increasing, each below the base's length) are private copies
+ *   made on `stream`; every other page is shared with the base (no copy).
+ *   The base may be removed first: shared pages live while a chunk holds
+ *   them. Errors: INVALID, NOT_FOUND (base), EXISTS (new_id), OOM, HIP.
+ * pic_store_write_rows: writes token-major K / V rows of one layer into a
+ *   derived chunk: k device [n_rows][n_kv_heads][d_k], v device
+ *   [n_rows][n_kv_heads][d_v] (GQA) or NULL (MLA); rows as above, each on a
+ *   page the chunk holds alone (a page named at pic_store_derive and not
+ *   shared since by a later derive). Ordered on `stream`; k and v are read
+ *   before the stream passes the call. Link calls already enqueued on
+ *   another stream may see either content.
+ *   Errors: INVALID (not a derived chunk, a row on a shared page, bad
+ *   arguments), NOT_FOUND, HIP. */
+pic_status pic_store_derive(pic_store *store, uint64_t new_id, uint64_t base_id, int32_t n_rows,
+                            const int32_t *rows, void *stream);
+pic_status pic_store_write_rows(pic_store *store, uint64_t chunk_id, int32_t layer,
+                                int32_t n_rows, const int32_t *rows, const void *k,
+                                const void *v, void *stream);
+
 /* Hash-table lookup (Sec. 3 step 1): *n_tokens_out = the chunk's length.
  * Errors: INVALID, NOT_FOUND. */
 pic_status pic_store_lookup(const pic_store *store, uint64_t chunk_id, int64_t *n_tokens_out);
@@ -137,7 +163,14 @@ pic_status pic_store_usage(const pic_store *store, int64_t *used_tokens,
  *     caches, e.g. the link of post-training PIC that recomputes the first
  *     tokens of every document (Sec. 1 and 2.2; Sec. 6.1 runs EPIC with 64
  *     per document): link [the recomputed tokens, put as a chunk of their
- *     own ; the cached chunk from token 64] for every document. */
+ *     own ; the cached chunk from token 64] for every document.
+ *   q_doc_limits: NULL (every query token sees all of its request's linked
+ *     rows), or per query token t (indexing as q) the number of leading
+ *     linked rows it sees, 0 .. the request's linked rows. Recomputed
+ *     tokens attend as in a prefill of the concatenated prompt (Sec. 2,
+ *     post-training PIC): a token at position P of the linked rows passes
+ *     P + 1 (and the call passes self_offsets = NULL). The own KV, if any,
+ *     is not affected. */
 typedef struct pic_link_req {
   int32_t batch;
   int32_t layer;             /* the store layer whose chunk caches are read (0 for one layer) */
@@ -146,6 +179,7 @@ typedef struct pic_link_req {
   const int32_t *q_offsets;
   const int32_t *self_offsets;
   const int32_t *chunk_starts;
+  const int32_t *q_doc_limits;
 } pic_link_req;
 
 /* Link-stage attention for prefill-shaped requests (Sec. 4.1-4.2).

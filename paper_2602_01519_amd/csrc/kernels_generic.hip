@@ -118,6 +118,27 @@ __global__ void gather_kernel(const LinkEntry *__restrict__ links, int32_t n_lin
   }
 }
 
+// Rows written into chunk slots (rows recomputed at link time): row i of the
+// token-major sources goes to dst[i], K into its head-major row, V into its
+// transposed column. Off the link path.
+template <typename E>
+__global__ void write_rows_kernel(const RowDst *__restrict__ dst, int32_t n,
+                                  const E *__restrict__ src_k, const E *__restrict__ src_v,
+                                  int32_t heads, int32_t d_k, int32_t d_v, int32_t mla) {
+  const int i = blockIdx.x;
+  if (i >= n) return;
+  const RowDst d = dst[i];
+  for (int x = threadIdx.x; x < heads * d_k; x += blockDim.x) {
+    const int h = x / d_k, c = x - h * d_k;
+    ((E *)d.k)[(int64_t)h * d.lp * d_k + c] = src_k[(int64_t)i * heads * d_k + x];
+  }
+  if (!mla)
+    for (int x = threadIdx.x; x < heads * d_v; x += blockDim.x) {
+      const int h = x / d_v, e = x - h * d_v;
+      ((E *)d.v)[((int64_t)h * d_v + e) * d.lp] = src_v[(int64_t)i * heads * d_v + x];
+    }
+}
+
 // ---------------------------------------------------------------------------
 // Own KV of a request laid out like a chunk slot (at its last link): K rows
 // head-major, V transposed, zero padding up to lp. One launch per call:
@@ -273,12 +294,14 @@ __global__ __launch_bounds__(256) void link_valu_kernel(LinkParams p) {
   }
 
   int lim[4];          // last visible own key per row (-1: none)
+  int dl[4];           // linked rows visible to the row
   bool rvalid[4];
 #pragma unroll
   for (int r = 0; r < 4; ++r) {
     const int row = row0 + wave * 4 + r;
     rvalid[r] = row < nrows;
     lim[r] = rvalid[r] ? row / group + R.ls - R.lq : -1;
+    dl[r] = p.doc_lim && rvalid[r] ? p.doc_lim[R.q0 + row / group] : kNoLimit;
   }
   float m[4], l[4], acc[4][8];
 #pragma unroll
@@ -299,6 +322,7 @@ __global__ __launch_bounds__(256) void link_valu_kernel(LinkParams p) {
     const int tt = t - E.tile0;
     const int nvalid = min(kTile, E.len - tt * kTile);
     const int j0 = tt * kTile;          // key index within the link (own: within the own KV)
+    const int tok = E.tok0 + j0;        // ... within the request's linked rows
     // 64 consecutive key rows (the slot's padding rows are zeros)
     const uint32_t *src = (const uint32_t *)key_row<T>(E, MLA ? 0 : kvh, tt * kTile, d_k);
     for (int w = threadIdx.x; w < kTile * kwords; w += blockDim.x) {
@@ -333,7 +357,7 @@ __global__ __launch_bounds__(256) void link_valu_kernel(LinkParams p) {
     float pr[4], alpha[4];
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
-      bool vis = rvalid[r] && lane < nvalid && (!own || j0 + lane <= lim[r]);
+      bool vis = rvalid[r] && lane < nvalid && (own ? j0 + lane <= lim[r] : tok + lane < dl[r]);
       float sv = vis ? s[r] : -INFINITY;
       float mx = sv;
 #pragma unroll
@@ -582,6 +606,19 @@ hipError_t launch_put_transposed(const void *src, void *dst, int64_t n_tokens, i
   else
     hipLaunchKernelGGL(put_transposed_kernel<uint32_t>, grid, dim3(256), 0, st,
                        (const uint32_t *)src, (uint32_t *)dst, n_tokens, lp, heads, width);
+  return hipGetLastError();
+}
+
+hipError_t launch_write_rows(const RowDst *dst, int32_t n, const void *src_k, const void *src_v,
+                             int32_t heads, int32_t d_k, int32_t d_v, int32_t mla, int32_t esz,
+                             hipStream_t st) {
+  if (n <= 0) return hipSuccess;
+  if (esz == 2)
+    hipLaunchKernelGGL(write_rows_kernel<uint16_t>, dim3(n), dim3(256), 0, st, dst, n,
+                       (const uint16_t *)src_k, (const uint16_t *)src_v, heads, d_k, d_v, mla);
+  else
+    hipLaunchKernelGGL(write_rows_kernel<uint32_t>, dim3(n), dim3(256), 0, st, dst, n,
+                       (const uint32_t *)src_k, (const uint32_t *)src_v, heads, d_k, d_v, mla);
   return hipGetLastError();
 }
 

@@ -107,6 +107,7 @@ struct TileRef {
   int lp;            // V^T row stride in elements
   int nvalid;        // valid keys in the tile
   int j0;            // key index of the tile's first key within its link
+  int tok;           // ... within the request's linked rows (document tiles)
   int own;           // the tile belongs to the request's own KV (causal mask)
 };
 
@@ -124,6 +125,7 @@ struct Ctx {
   int li;                      // cursor: current link
   const char *lk, *lv;         // its K / V^T blocks
   int llen, llp, ltile0, lend; // its tokens, padded tokens, first tile, tile after its last
+  int ltok0;                   // its first row within the request's linked rows
   uint32_t koff[kCopySets];    // byte offsets of this lane's K chunks within a tile
   uint32_t vrow[kCopySets], vcol[kCopySets];   // row / byte column of its V^T chunks
 };
@@ -134,6 +136,7 @@ __device__ __forceinline__ void cursor_load(Ctx &c) {
   c.llen = c.links[c.li].len;
   c.llp = c.links[c.li].lp;
   c.ltile0 = c.links[c.li].tile0;
+  c.ltok0 = c.links[c.li].tok0;
   c.lend = c.ltile0 + (c.llen + kTile - 1) / kTile;
 }
 
@@ -148,6 +151,7 @@ __device__ __forceinline__ TileRef tile_ref(Ctx &c, int t) {
   r.lp = c.llp;
   r.nvalid = min(kTile, c.llen - tt * kTile);
   r.j0 = tt * kTile;
+  r.tok = c.ltok0 + tt * kTile;
   r.own = t >= c.R.doc_tiles;
   r.k = c.lk + ((int64_t)c.kvh * c.llp + tt * kTile) * kD * 2;
   r.v = c.lv + ((int64_t)c.kvh * kD * c.llp + tt * kTile) * 2;
@@ -190,14 +194,23 @@ struct Acc {
   float m_used, lsum;
 };
 
-// Masks keys past the tile's valid end and, in own tiles, keys after the
-// row's causal limit. s0[x] / s1[x] hold key (x>>3)*16 + g*8 + (x&7) (+32).
-__device__ __forceinline__ void mask_tile(const Ctx &c, f32x16 &s0, f32x16 &s1, int nvalid,
-                                          int j0, int own, int lim) {
-  if (own || nvalid < kTile) {
+// Per-row limit on the visible linked rows: dl for this lane's row, wmin
+// its minimum over the wave (both far above any row count without limits).
+struct DocLim {
+  int dl, wmin;
+};
+
+// Masks keys past the tile's valid end, in own tiles keys after the row's
+// causal limit, and in document tiles rows at or past the row's limit.
+// s0[x] / s1[x] hold key (x>>3)*16 + g*8 + (x&7) (+32).
+__device__ __forceinline__ void mask_tile(const Ctx &c, f32x16 &s0, f32x16 &s1, const TileRef &r,
+                                          int lim, const DocLim &dlm) {
+  const int nvalid = r.nvalid;
+  if (r.own || nvalid < kTile || r.tok + kTile > dlm.wmin) {
     // visible iff key <= kl; compared as (key - g*8) against kl - g*8 so the
     // left side is a compile-time constant per element
-    const int kl = (own ? min(lim - j0, nvalid - 1) : nvalid - 1) - c.g * 8;
+    const int kl = (r.own ? min(lim - r.j0, nvalid - 1) : min(dlm.dl - r.tok, nvalid) - 1) -
+                   c.g * 8;
 #pragma unroll
     for (int x = 0; x < 16; ++x) {
       const int key = (x >> 3) * 16 + (x & 7);
@@ -212,9 +225,9 @@ __device__ __forceinline__ void mask_tile(const Ctx &c, f32x16 &s0, f32x16 &s1, 
 // reads are issued a few MFMAs ahead of their use (scheduling groups), so an
 // MFMA does not wait on the read issued right before it.
 __device__ __forceinline__ void compute_tile(const Ctx &c, const uint4 *kt, const uint4 *vt,
-                                             const bf16x8 (&qf)[8], Acc &a, int nvalid, int j0,
-                                             int own, int lim, float sc, const TileRef &nref,
-                                             uint4 *nk, uint4 *nv) {
+                                             const bf16x8 (&qf)[8], Acc &a, const TileRef &ref,
+                                             int lim, const DocLim &dlm, float sc,
+                                             const TileRef &nref, uint4 *nk, uint4 *nv) {
   const int krow0 = key_of_m(c.n);
   f32x16 s0, s1;
 #pragma unroll
@@ -242,7 +255,7 @@ __device__ __forceinline__ void compute_tile(const Ctx &c, const uint4 *kt, cons
     s1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kb[st], qf[st], s1, 0, 0, 0);
     __builtin_amdgcn_sched_barrier(0);
   }
-  mask_tile(c, s0, s1, nvalid, j0, own, lim);
+  mask_tile(c, s0, s1, ref, lim, dlm);
 
   float tmax = -INFINITY;
 #pragma unroll
@@ -345,6 +358,14 @@ __global__ __launch_bounds__(kWaves * 64, 8 / kWaves) void link_mfma_d128_kernel
   const int qh = c.kvh * group + (rvalid ? row % group : 0);
   const int lim = rvalid ? qi + R.ls - R.lq : -1;     // last visible own key
   const int64_t orow = (int64_t)(R.q0 + qi) * p.n_q_heads + qh;
+  DocLim dlm{kNoLimit, kNoLimit};
+  if (p.doc_lim) {
+    if (rvalid) dlm.dl = p.doc_lim[R.q0 + qi];
+    int w = dlm.dl;
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) w = min(w, __shfl_xor(w, o));
+    dlm.wmin = uni(w);
+  }
 
   // Per-lane load-to-LDS offsets (see issue_k / issue_v).
 #pragma unroll
@@ -402,7 +423,7 @@ __global__ __launch_bounds__(kWaves * 64, 8 / kWaves) void link_mfma_d128_kernel
     // tile t in buffers 0; copy tile t+1 into buffers 1
     ref1 = t + 1 < t_end ? tile_ref(c, t + 1) : ref0;
     if (active)
-      compute_tile(c, sk0, sv0, qf, a, ref0.nvalid, ref0.j0, ref0.own, lim, sc, ref1, sk1, sv1);
+      compute_tile(c, sk0, sv0, qf, a, ref0, lim, dlm, sc, ref1, sk1, sv1);
     else
       issue_tile(c, ref1, sk1, sv1);
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
@@ -411,7 +432,7 @@ __global__ __launch_bounds__(kWaves * 64, 8 / kWaves) void link_mfma_d128_kernel
     // tile t+1 in buffers 1; copy tile t+2 into buffers 0
     ref0 = t + 2 < t_end ? tile_ref(c, t + 2) : ref1;
     if (active)
-      compute_tile(c, sk1, sv1, qf, a, ref1.nvalid, ref1.j0, ref1.own, lim, sc, ref0, sk0, sv0);
+      compute_tile(c, sk1, sv1, qf, a, ref1, lim, dlm, sc, ref0, sk0, sv0);
     else
       issue_tile(c, ref0, sk0, sv0);
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");

@@ -94,6 +94,7 @@ struct MlaSmem {
 struct TileRef {
   const char *k;    // first latent row of the tile (bytes)
   int nvalid, j0, own;
+  int tok;          // first key's row within the request's linked rows (document tiles)
 };
 
 // Walks a request's links in order. The tables are read through the
@@ -108,12 +109,14 @@ struct Cursor {
   int li;                // current link
   const char *k;         // its first latent row
   int len, tile0, end;   // its tokens, first tile and the tile after its last
+  int tok0;              // its first row within the request's linked rows
 };
 
 __device__ __forceinline__ void cursor_load(Cursor &c) {
   c.k = (const char *)c.links[c.li].k;
   c.len = c.links[c.li].len;
   c.tile0 = c.links[c.li].tile0;
+  c.tok0 = c.links[c.li].tok0;
   c.end = c.tile0 + (c.len + kTile - 1) / kTile;
 }
 
@@ -127,6 +130,7 @@ __device__ __forceinline__ TileRef tile_ref(Cursor &c, int t, int doc_tiles) {
   TileRef r;
   r.nvalid = min(kTile, c.len - tt * kTile);
   r.j0 = tt * kTile;
+  r.tok = c.tok0 + tt * kTile;
   r.own = t >= doc_tiles;
   r.k = c.k + (int64_t)tt * kTile * kRowBytes;
   return r;
@@ -209,6 +213,16 @@ __global__ __launch_bounds__(256, 1) void link_mla_kernel(LinkParams p) {
     const int qh = rvalid[rb] ? row % group : 0;
     lim[rb] = rvalid[rb] ? qi + R.ls - R.lq : -1;
     orow[rb] = (int64_t)(R.q0 + qi) * p.n_q_heads + qh;
+  }
+  // Limit on the visible linked rows of this lane's score row (dl_s) and its
+  // minimum over the wave (wmin_s).
+  int dl_s = kNoLimit, wmin_s = kNoLimit;
+  if (p.doc_lim) {
+    if (rvalid[rb_s]) dl_s = p.doc_lim[R.q0 + (row0 + 32 * rb_s + n) / group];
+    int w = dl_s;
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) w = min(w, __shfl_xor(w, o));
+    wmin_s = uni(w);
   }
 
   const uint32_t lat_off = 16u * (uint32_t)(lane ^ (wave << 2));
@@ -355,8 +369,9 @@ __global__ __launch_bounds__(256, 1) void link_mla_kernel(LinkParams p) {
       __builtin_amdgcn_sched_barrier(0);
     }
     // s[x]: key 32 kb_s + (x>>3)*16 + g*8 + (x&7) of row 32 rb_s + n
-    if (ref.own || ref.nvalid < kTile) {
-      const int kl = (ref.own ? min(lim[rb_s] - ref.j0, ref.nvalid - 1) : ref.nvalid - 1) -
+    if (ref.own || ref.nvalid < kTile || ref.tok + kTile > wmin_s) {
+      const int kl = (ref.own ? min(lim[rb_s] - ref.j0, ref.nvalid - 1)
+                              : min(dl_s - ref.tok, ref.nvalid) - 1) -
                      32 * kb_s - g * 8;
 #pragma unroll
       for (int x = 0; x < 16; ++x)

@@ -96,8 +96,6 @@ __global__ __launch_bounds__(256, 1) void proj_kernel(ProjArgs p) {
   bf16x8 b[8], bn[8];
   load_a(part, b);
   for (int tb = part; tb < n_blocks; tb += parts) {
-    const int t = tb * 32 + (lane & 31);
-    const bool tv = t < p.n_tokens;
     load_a(tb + parts, bn);         // the next block's fragments load during this one
     if (kRope) {
       // 32 tokens x 128 bytes of rope, one 16-byte piece per thread

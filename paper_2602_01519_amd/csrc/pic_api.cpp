@@ -69,17 +69,23 @@ struct DeviceGuard {
 // is long enough -- and each run holds a piece of the chunk laid out like a
 // chunk of its own (K [H][run tokens][d_k], then V^T [H][d_v][run tokens]),
 // so a piece is one link-table entry and the kernels need no page table.
+// Such a run of pages is a block; a chunk is a list of views of blocks
+// (pages skip .. of the block), in token order. A chunk made by
+// pic_store_derive views its base's blocks for the pages it shares with
+// it, so blocks are reference-counted by the chunks that view them.
 struct Run {
-  int64_t page0;        // first page
-  int32_t pages;
-  int32_t tok0;         // first chunk token held by the run
-  int32_t ntok;         // chunk tokens held by the run
+  int64_t page0;        // the block's first page
+  int32_t pages;        // the block's pages (its row stride is pages * 64 tokens)
+  int32_t tok0;         // first chunk token held by the view
+  int32_t ntok;         // chunk tokens held by the view
+  int32_t skip = 0;     // pages of the block before the view's first page
 };
 
 struct Slot {
   int64_t len;
   std::vector<Run> runs;
   int64_t plan_refs = 0;   // live link plans that link this chunk
+  bool derived = false;    // made by pic_store_derive (rows may be written)
 };
 
 // Pinned host table + device copy + completion event. The planner writes a
@@ -118,6 +124,8 @@ struct pic_store {
   int64_t capacity = 0;          // padded tokens
   int64_t used = 0;              // tokens of allocated pages
   std::map<int64_t, int64_t> free_runs;   // page0 -> pages, coalesced
+  std::unordered_map<int64_t, int32_t> block_refs;   // block page0 -> chunks viewing it
+  std::vector<int32_t> page_refs;                     // page -> chunks viewing it
   // runs of removed chunks, reusable once the event (recorded on the
   // remover's stream) has completed
   std::vector<std::pair<hipEvent_t, std::vector<Run>>> pending;
@@ -252,12 +260,59 @@ bool alloc_pages(pic_store *s, int64_t pages, std::vector<Run> &out) {
 LinkEntry run_entry(const pic_store *s, const Run &r, int32_t layer) {
   const int64_t slot_tok_bytes = (s->k_tok_elems + s->v_tok_elems) * s->esz;
   const int32_t lp = r.pages * kTile;
+  const int64_t skip_tok = (int64_t)r.skip * kTile;
+  const char *block = s->pool + (int64_t)layer * s->layer_bytes + r.page0 * kTile * slot_tok_bytes;
   LinkEntry E{};
-  E.k = s->pool + (int64_t)layer * s->layer_bytes + r.page0 * kTile * slot_tok_bytes;
-  E.v = s->desc.kind == PIC_GQA ? (const char *)E.k + (int64_t)lp * s->k_tok_elems * s->esz : E.k;
+  // K rows and V^T columns of the view start skip_tok tokens into the block
+  E.k = block + skip_tok * s->desc.d_k * s->esz;
+  E.v = s->desc.kind == PIC_GQA
+            ? block + (int64_t)lp * s->k_tok_elems * s->esz + skip_tok * s->esz
+            : E.k;
   E.len = r.ntok;
   E.lp = lp;
   return E;
+}
+
+// Pages for a new chunk: free ones, else those of removed chunks whose
+// readers are done, else after waiting for the remaining readers.
+pic_status take_pages(pic_store *s, int64_t pages, std::vector<Run> &runs) {
+  runs.clear();
+  if (pages == 0) return PIC_OK;
+  pic_status rc = reclaim(s, false);
+  if (rc != PIC_OK) return rc;
+  if (!alloc_pages(s, pages, runs) && !s->pending.empty()) {
+    rc = reclaim(s, true);
+    if (rc != PIC_OK) return rc;
+    (void)alloc_pages(s, pages, runs);
+  }
+  if (runs.empty())
+    return fail(PIC_ERR_OOM, "pool full: %lld of %lld tokens in use, %lld needed",
+                (long long)s->used, (long long)s->capacity, (long long)pages * kTile);
+  return PIC_OK;
+}
+
+// Host row list of pic_store_derive / pic_store_write_rows: strictly
+// increasing, each below len.
+bool check_rows(const int32_t *rows, int32_t n, int64_t len) {
+  if (n < 0 || (n > 0 && !rows)) return false;
+  for (int32_t i = 0; i < n; ++i)
+    if (rows[i] < 0 || rows[i] >= len || (i > 0 && rows[i] <= rows[i - 1])) return false;
+  return true;
+}
+
+// Adds d to the reference count of every page a chunk's views cover.
+void ref_pages(pic_store *s, const std::vector<Run> &views, int32_t d) {
+  for (const Run &v : views) {
+    const int64_t first = v.page0 + v.skip, n = (v.ntok + kTile - 1) / kTile;
+    for (int64_t p = first; p < first + n; ++p) s->page_refs[p] += d;
+  }
+}
+
+// The view of a chunk holding token t.
+const Run &view_of(const Slot &sl, int64_t t) {
+  size_t i = 0;
+  while (i + 1 < sl.runs.size() && sl.runs[i].tok0 + sl.runs[i].ntok <= t) ++i;
+  return sl.runs[i];
 }
 
 bool check_offsets(const int32_t *a, int32_t n) {
@@ -281,6 +336,9 @@ struct Plan {
   bool self = false;             // requests carry own KV
   int64_t total_self = 0;        // own tokens over the batch
   std::vector<uint64_t> ids;     // every linked chunk id (with repeats)
+  // per query token: linked rows visible to it; empty unless the rows of
+  // some request see different numbers of them (the kernels mask per row)
+  std::vector<int32_t> doc_lim;
 };
 
 // Tensor arguments of a call against its plan.
@@ -332,6 +390,8 @@ pic_status plan_call(pic_store *s, const pic_link_req *req, int32_t n_q_heads, f
   P.links.reserve(n_links + B);
   P.ids.clear();
   P.reqs.resize(B);
+  P.doc_lim.clear();
+  bool mixed_limits = false;
   std::vector<int64_t> weight(B);
   for (int32_t r = 0; r < B; ++r) {
     ReqEntry &R = P.reqs[r];
@@ -377,6 +437,31 @@ pic_status plan_call(pic_store *s, const pic_link_req *req, int32_t n_q_heads, f
       }
       P.ids.push_back(id);
     }
+    if (req->q_doc_limits && R.lq > 0) {
+      int32_t lo = INT32_MAX, hi = 0;
+      for (int32_t i = 0; i < R.lq; ++i) {
+        const int32_t lim = req->q_doc_limits[R.q0 + i];
+        if (lim < 0 || lim > toks)
+          return fail(PIC_ERR_INVALID, "request %d query %d: limit %d outside 0..%lld linked rows",
+                      r, i, lim, (long long)toks);
+        lo = std::min(lo, lim);
+        hi = std::max(hi, lim);
+      }
+      // rows past every query's limit are never read: cut the links there;
+      // limits that differ between rows are applied by the kernels
+      if (hi < toks) {
+        size_t keep = R.link0;
+        tiles = 0;
+        while (keep < P.links.size() && P.links[keep].tok0 < hi) {
+          LinkEntry &E = P.links[keep++];
+          E.len = std::min(E.len, hi - E.tok0);
+          tiles += (E.len + kTile - 1) / kTile;
+        }
+        P.links.resize(keep);
+        toks = hi;
+      }
+      if (lo < hi) mixed_limits = true;
+    }
     if (toks + R.ls > INT32_MAX / 2) return fail(PIC_ERR_INVALID, "request %d too long", r);
     R.doc_tiles = (int32_t)tiles;
     if (R.ls > 0) {             // own KV: a slot in the call's workspace, filled on the device
@@ -402,6 +487,7 @@ pic_status plan_call(pic_store *s, const pic_link_req *req, int32_t n_q_heads, f
   std::stable_sort(P.order.begin(), P.order.end(),
                    [&](int32_t a, int32_t b) { return weight[a] > weight[b]; });
   P.total_q = (int32_t)tq;
+  if (mixed_limits) P.doc_lim.assign(req->q_doc_limits, req->q_doc_limits + tq);
   return PIC_OK;
 }
 
@@ -409,7 +495,7 @@ pic_status plan_call(pic_store *s, const pic_link_req *req, int32_t n_q_heads, f
 // and points lp's tables at the slot's device copy; the call's prologue
 // kernel moves them there.
 struct TableLayout {
-  size_t off_r, off_o, bytes;
+  size_t off_r, off_o, off_d, bytes;
 };
 
 // Where the prologue reads the tables, and what it copies first.
@@ -426,7 +512,8 @@ pic_status upload(pic_store *s, const Plan &P, hipStream_t st, Stage **stage, Li
   const size_t nl = P.links.size(), nr = P.reqs.size();
   tl.off_r = round_up(sizeof(LinkEntry) * nl, 256);
   tl.off_o = tl.off_r + round_up(sizeof(ReqEntry) * nr, 256);
-  tl.bytes = tl.off_o + round_up(sizeof(int32_t) * nr, 256);
+  tl.off_d = tl.off_o + round_up(sizeof(int32_t) * nr, 256);
+  tl.bytes = tl.off_d + round_up(sizeof(int32_t) * P.doc_lim.size(), 256);
   const size_t off_r = tl.off_r, off_o = tl.off_o, bytes = tl.bytes;
   pic_status rc = stage_acquire(s, bytes, stage);
   if (rc != PIC_OK) return rc;
@@ -434,11 +521,13 @@ pic_status upload(pic_store *s, const Plan &P, hipStream_t st, Stage **stage, Li
   if (nl) memcpy(h, P.links.data(), sizeof(LinkEntry) * nl);
   memcpy(h + off_r, P.reqs.data(), sizeof(ReqEntry) * nr);
   memcpy(h + off_o, P.order.data(), sizeof(int32_t) * nr);
+  if (!P.doc_lim.empty()) memcpy(h + tl.off_d, P.doc_lim.data(), sizeof(int32_t) * P.doc_lim.size());
   (void)st;
   char *dv = (char *)(*stage)->dev;
   lp.links = (const LinkEntry *)dv;
   lp.reqs = (const ReqEntry *)(dv + off_r);
   lp.order = (const int32_t *)(dv + off_o);
+  lp.doc_lim = P.doc_lim.empty() ? nullptr : (const int32_t *)(dv + tl.off_d);
   return PIC_OK;
 }
 
@@ -514,6 +603,9 @@ pic_status setup_call(pic_store *s, const pic_link_req *req, int32_t n_q_heads, 
   if (bf16_128)
     kern = mode == Mode::Decode && P.max_rows <= decode_d128_max_rows() ? Kern::Decode128
                                                                          : Kern::Mfma128;
+  // rows of one request that see different numbers of linked rows need the
+  // per-row masks of the flash kernel
+  if (kern == Kern::Decode128 && !P.doc_lim.empty()) kern = Kern::Mfma128;
   if (d.dtype == PIC_BF16 && mla && d.d_k == 576 && d.d_v == 512) kern = Kern::Mla;
   if (kern == Kern::Valu && valu_lds_bytes_for(s->esz, mla, d.d_k, d.d_v) > 160 * 1024)
     return fail(PIC_ERR_UNSUPPORTED, "head widths d_k=%d d_v=%d exceed the generic kernel's LDS",
@@ -674,6 +766,7 @@ struct pic_link_plan {
   void *dev = nullptr;           // [layer tables][workspace]
   size_t table_bytes = 0;        // one layer's tables, 256-byte aligned
   size_t off_r = 0, off_o = 0;   // request / order tables within a layer's tables
+  size_t off_d = 0;              // per-query limits (if any) within a layer's tables
   void *work = nullptr;          // inside dev
 };
 
@@ -708,6 +801,13 @@ pic_status pic_store_create(const pic_store_desc *desc, pic_store **out) {
   if (e != hipSuccess) {
     delete s;
     return hip_fail(e, "hipMalloc(pool)");
+  }
+  try {
+    s->page_refs.assign((size_t)(s->capacity / kTile), 0);
+  } catch (...) {
+    (void)hipFree(s->pool);
+    delete s;
+    return fail(PIC_ERR_OOM, "host allocation failed");
   }
   *out = s;
   return PIC_OK;
@@ -754,19 +854,9 @@ pic_status pic_store_put(pic_store *s, uint64_t chunk_id, int64_t n_tokens, cons
       return fail(PIC_ERR_INVALID, "k and v must be device memory");
     }
   }
-  // pages: free ones, else those of removed chunks whose readers are done,
-  // else wait for the remaining readers
   std::vector<Run> runs;
-  pic_status rc = reclaim(s, false);
+  pic_status rc = take_pages(s, pages, runs);
   if (rc != PIC_OK) return rc;
-  if (!alloc_pages(s, pages, runs) && !s->pending.empty()) {
-    rc = reclaim(s, true);
-    if (rc != PIC_OK) return rc;
-    (void)alloc_pages(s, pages, runs);
-  }
-  if (runs.empty())
-    return fail(PIC_ERR_OOM, "pool full: %lld of %lld tokens in use, chunk needs %lld",
-                (long long)s->used, (long long)s->capacity, (long long)pages * kTile);
   int32_t tok = 0;
   for (Run &r : runs) {
     r.tok0 = tok;
@@ -799,9 +889,156 @@ pic_status pic_store_put(pic_store *s, uint64_t chunk_id, int64_t n_tokens, cons
   }
   Slot sl;
   sl.len = n_tokens;
+  for (const Run &r : runs) s->block_refs[r.page0] = 1;
+  ref_pages(s, runs, 1);
   sl.runs = std::move(runs);
   s->used += pages * kTile;
   s->map.emplace(chunk_id, std::move(sl));
+  return PIC_OK;
+}
+
+pic_status pic_store_derive(pic_store *s, uint64_t new_id, uint64_t base_id, int32_t n_rows,
+                            const int32_t *rows, void *stream) {
+  if (!s) return fail(PIC_ERR_INVALID, "store is NULL");
+  auto bit = s->map.find(base_id);
+  if (bit == s->map.end()) return fail(PIC_ERR_NOT_FOUND, "base chunk id 0x%llx not in the store",
+                                       (unsigned long long)base_id);
+  if (s->map.count(new_id)) return fail(PIC_ERR_EXISTS, "chunk id 0x%llx already stored",
+                                        (unsigned long long)new_id);
+  const int64_t len = bit->second.len;
+  if (!check_rows(rows, n_rows, len))
+    return fail(PIC_ERR_INVALID, "rows must be strictly increasing and below the chunk's %lld tokens",
+                (long long)len);
+  const int64_t npages = round_up(len, kTile) / kTile;
+  std::vector<char> own(npages, 0);
+  int64_t n_own = 0;
+  for (int32_t i = 0; i < n_rows; ++i) {
+    char &o = own[rows[i] / kTile];
+    n_own += !o;
+    o = 1;
+  }
+  DeviceGuard dg(s->device);
+  if (!dg.ok) return fail(PIC_ERR_HIP, "cannot select the store's device");
+  std::vector<Run> fresh;
+  pic_status rc = take_pages(s, n_own, fresh);
+  if (rc != PIC_OK) return rc;
+  const Slot &B = s->map.at(base_id);   // take_pages does not touch the map
+  // One view per chunk page, merged where consecutive pages are consecutive
+  // pages of one block; private pages take the fresh blocks' pages in order.
+  std::vector<Run> views;
+  std::vector<std::pair<Run, Run>> copies;     // (source page view, destination page view)
+  size_t fb = 0;
+  int32_t fq = 0;
+  for (int64_t p = 0; p < npages; ++p) {
+    const int32_t t0 = (int32_t)(p * kTile);
+    const int32_t nt = (int32_t)std::min<int64_t>(kTile, len - t0);
+    const Run &src = view_of(B, t0);
+    Run pv{src.page0, src.pages, t0, nt, src.skip + (t0 - src.tok0) / kTile};
+    if (own[p]) {
+      Run dst{fresh[fb].page0, fresh[fb].pages, t0, nt, fq};
+      copies.emplace_back(pv, dst);
+      pv = dst;
+      if (++fq == fresh[fb].pages) {
+        ++fb;
+        fq = 0;
+      }
+    }
+    if (!views.empty()) {
+      Run &last = views.back();
+      if (last.page0 == pv.page0 && last.skip + last.ntok / kTile == pv.skip && last.ntok % kTile == 0) {
+        last.ntok += nt;
+        continue;
+      }
+    }
+    views.push_back(pv);
+  }
+  // copy the private pages' base content, every layer (K rows of each head,
+  // V^T columns of each head and dim)
+  const hipStream_t st = (hipStream_t)stream;
+  const pic_store_desc &d = s->desc;
+  hipError_t e = hipSuccess;
+  for (int32_t l = 0; l < s->n_layers && e == hipSuccess; ++l)
+    for (const auto &c : copies) {
+      const LinkEntry S = run_entry(s, c.first, l), D = run_entry(s, c.second, l);
+      const size_t kw = (size_t)kTile * d.d_k * s->esz;
+      e = hipMemcpy2DAsync((void *)D.k, (size_t)D.lp * d.d_k * s->esz, S.k,
+                           (size_t)S.lp * d.d_k * s->esz, kw, (size_t)d.n_kv_heads,
+                           hipMemcpyDeviceToDevice, st);
+      if (e != hipSuccess) break;
+      if (d.kind == PIC_GQA) {
+        e = hipMemcpy2DAsync((void *)D.v, (size_t)D.lp * s->esz, S.v, (size_t)S.lp * s->esz,
+                             (size_t)kTile * s->esz, (size_t)d.n_kv_heads * d.d_v,
+                             hipMemcpyDeviceToDevice, st);
+        if (e != hipSuccess) break;
+      }
+    }
+  if (e != hipSuccess) {
+    for (const Run &r : fresh) free_run(s, r.page0, r.pages);
+    return hip_fail(e, "derive page copies");
+  }
+  for (const Run &r : fresh) s->block_refs[r.page0] = 0;
+  std::vector<int64_t> blocks;
+  for (const Run &v : views) blocks.push_back(v.page0);
+  std::sort(blocks.begin(), blocks.end());
+  blocks.erase(std::unique(blocks.begin(), blocks.end()), blocks.end());
+  for (int64_t b : blocks) ++s->block_refs.at(b);
+  ref_pages(s, views, 1);
+  s->used += n_own * kTile;
+  Slot sl;
+  sl.len = len;
+  sl.runs = std::move(views);
+  sl.derived = true;
+  s->map.emplace(new_id, std::move(sl));
+  return PIC_OK;
+}
+
+pic_status pic_store_write_rows(pic_store *s, uint64_t chunk_id, int32_t layer, int32_t n_rows,
+                                const int32_t *rows, const void *k, const void *v, void *stream) {
+  if (!s) return fail(PIC_ERR_INVALID, "store is NULL");
+  auto it = s->map.find(chunk_id);
+  if (it == s->map.end()) return fail(PIC_ERR_NOT_FOUND, "chunk id 0x%llx not in the store",
+                                      (unsigned long long)chunk_id);
+  const Slot &sl = it->second;
+  if (!sl.derived)
+    return fail(PIC_ERR_INVALID, "chunk id 0x%llx was not made by pic_store_derive",
+                (unsigned long long)chunk_id);
+  if (layer < 0 || layer >= s->n_layers)
+    return fail(PIC_ERR_INVALID, "layer %d outside the store's %d layers", layer, s->n_layers);
+  if (!check_rows(rows, n_rows, sl.len))
+    return fail(PIC_ERR_INVALID, "rows must be strictly increasing and below the chunk's %lld tokens",
+                (long long)sl.len);
+  if (n_rows == 0) return PIC_OK;
+  const bool gqa = s->desc.kind == PIC_GQA;
+  if (!k || (gqa && !v)) return fail(PIC_ERR_INVALID, "k/v is NULL");
+  if (!gqa && v) return fail(PIC_ERR_INVALID, "v must be NULL for MLA");
+  std::vector<RowDst> dst(n_rows);
+  for (int32_t i = 0; i < n_rows; ++i) {
+    const Run &r = view_of(sl, rows[i]);
+    if (s->page_refs[r.page0 + r.skip + (rows[i] - r.tok0) / kTile] != 1)
+      return fail(PIC_ERR_INVALID, "row %d of chunk 0x%llx is on a page shared with another chunk",
+                  rows[i], (unsigned long long)chunk_id);
+    const LinkEntry E = run_entry(s, r, layer);
+    const int64_t t = rows[i] - r.tok0;
+    dst[i].k = (char *)E.k + t * s->desc.d_k * s->esz;
+    dst[i].v = gqa ? (char *)E.v + t * s->esz : nullptr;
+    dst[i].lp = E.lp;
+  }
+  DeviceGuard dg(s->device);
+  if (!dg.ok) return fail(PIC_ERR_HIP, "cannot select the store's device");
+  const hipStream_t st = (hipStream_t)stream;
+  const size_t bytes = sizeof(RowDst) * (size_t)n_rows;
+  Stage *stage = nullptr;
+  pic_status rc = stage_acquire(s, bytes, &stage);
+  if (rc != PIC_OK) return rc;
+  memcpy(stage->host, dst.data(), bytes);
+  HIP_TRY(launch_table_copy(stage->host_dev, stage->dev, (int64_t)round_up(bytes, 16), st),
+          "table_copy_kernel");
+  const pic_store_desc &d = s->desc;
+  HIP_TRY(launch_write_rows((const RowDst *)stage->dev, n_rows, k, v, d.n_kv_heads, d.d_k, d.d_v,
+                            !gqa, s->esz, st),
+          "write_rows_kernel");
+  HIP_TRY(hipEventRecord(stage->done, st), "hipEventRecord(stage)");
+  stage->pending = true;
   return PIC_OK;
 }
 
@@ -824,7 +1061,25 @@ pic_status pic_store_remove(pic_store *s, uint64_t chunk_id, void *stream) {
     (void)hipEventDestroy(ev);
     return hip_fail(e, "hipEventRecord(remove)");
   }
-  s->pending.emplace_back(ev, std::move(it->second.runs));
+  // blocks no other chunk views are freed once the event has completed
+  ref_pages(s, it->second.runs, -1);
+  std::vector<Run> freed;
+  std::vector<int64_t> blocks;
+  for (const Run &r : it->second.runs) blocks.push_back(r.page0);
+  std::sort(blocks.begin(), blocks.end());
+  blocks.erase(std::unique(blocks.begin(), blocks.end()), blocks.end());
+  for (int64_t b : blocks) {
+    auto ref = s->block_refs.find(b);
+    if (--ref->second > 0) continue;
+    const Run &r = *std::find_if(it->second.runs.begin(), it->second.runs.end(),
+                                 [b](const Run &x) { return x.page0 == b; });
+    freed.push_back(Run{r.page0, r.pages, 0, 0});
+    s->block_refs.erase(ref);
+  }
+  if (freed.empty())
+    (void)hipEventDestroy(ev);
+  else
+    s->pending.emplace_back(ev, std::move(freed));
   s->map.erase(it);
   return PIC_OK;
 }
@@ -886,7 +1141,8 @@ pic_status pic_link_plan_create(pic_store *s, const pic_link_req *req, int32_t n
   const size_t nl = P.links.size(), nr = P.reqs.size();
   pl->off_r = round_up(sizeof(LinkEntry) * nl, 256);
   pl->off_o = pl->off_r + round_up(sizeof(ReqEntry) * nr, 256);
-  pl->table_bytes = round_up(pl->off_o + sizeof(int32_t) * nr, 256);
+  pl->off_d = pl->off_o + round_up(sizeof(int32_t) * nr, 256);
+  pl->table_bytes = round_up(pl->off_d + sizeof(int32_t) * P.doc_lim.size(), 256);
   const size_t tables = pl->table_bytes * s->n_layers;
   const size_t bytes = tables + pl->C.work_bytes();
   if (bytes > 0) {
@@ -921,6 +1177,8 @@ pic_status pic_link_plan_create(pic_store *s, const pic_link_req *req, int32_t n
       }
       if (nr) memcpy(h + pl->off_r, P.reqs.data(), sizeof(ReqEntry) * nr);
       if (nr) memcpy(h + pl->off_o, P.order.data(), sizeof(int32_t) * nr);
+      if (!P.doc_lim.empty())
+        memcpy(h + pl->off_d, P.doc_lim.data(), sizeof(int32_t) * P.doc_lim.size());
     }
     e = hipMemcpy(pl->dev, host.data(), tables, hipMemcpyHostToDevice);
     if (e != hipSuccess) {
@@ -955,6 +1213,7 @@ pic_status pic_link_plan_run(pic_link_plan *pl, int32_t layer, const void *q, co
   lp.links = (const LinkEntry *)t;
   lp.reqs = (const ReqEntry *)(t + pl->off_r);
   lp.order = (const int32_t *)(t + pl->off_o);
+  lp.doc_lim = pl->C.P.doc_lim.empty() ? nullptr : (const int32_t *)(t + pl->off_d);
   Prologue pro;
   pro.links = lp.links;
   pro.reqs = lp.reqs;

@@ -24,6 +24,9 @@ constexpr int kTile = 64;
 // the same way (in the call's workspace) before the attention kernel runs,
 // so every key tile of a request -- document or own -- is read alike.
 
+// A per-row limit on the visible linked rows that no request reaches.
+constexpr int kNoLimit = 1 << 30;
+
 struct LinkEntry {        // one link of one request, in link order
   const void *k;          // K block of the slot
   const void *v;          // GQA: V block; MLA: same as k
@@ -53,6 +56,7 @@ struct LinkParams {
   float *part_o;          // split partials: [split][Tq*H_q][d_v] unnormalised
   float *part_m;          // [split][Tq*H_q] running max (log2 domain)
   float *part_l;          // [split][Tq*H_q] running sum
+  const int32_t *doc_lim; // per query token: linked rows it sees (NULL: all of them)
   int32_t batch;
   int32_t n_q_heads;
   int32_t n_kv_heads;
@@ -74,6 +78,20 @@ hipError_t launch_put_transposed(const void *src, void *dst, int64_t n_tokens, i
 hipError_t launch_gather(const LinkEntry *links, int32_t n_links, int64_t total_tokens,
                          int32_t heads, int32_t d_k, int32_t d_v, int32_t mla, int32_t esz,
                          void *k_out, void *v_out, hipStream_t st);
+
+// Destination of one row written into a chunk slot: its K row of head 0
+// (head h at + h * lp * d_k elements) and its V^T column of head 0, dim 0
+// (head h, dim e at + (h * d_v + e) * lp; unused for MLA).
+struct RowDst {
+  void *k;
+  void *v;
+  int64_t lp;
+};
+// Scatters token-major rows src_k [n][heads][d_k] (and src_v [n][heads][d_v]
+// unless mla) to the slot rows dst[0 .. n).
+hipError_t launch_write_rows(const RowDst *dst, int32_t n, const void *src_k, const void *src_v,
+                             int32_t heads, int32_t d_k, int32_t d_v, int32_t mla, int32_t esz,
+                             hipStream_t st);
 
 // Copies bytes (a multiple of 16) from a host-mapped buffer to the device.
 hipError_t launch_table_copy(const void *src, void *dst, int64_t bytes, hipStream_t st);

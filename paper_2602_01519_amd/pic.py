@@ -52,7 +52,7 @@ class LinkReq(ctypes.Structure):
     _fields_ = [("batch", ctypes.c_int32), ("layer", ctypes.c_int32),
                 ("chunk_offsets", ctypes.c_void_p), ("chunk_ids", ctypes.c_void_p),
                 ("q_offsets", ctypes.c_void_p), ("self_offsets", ctypes.c_void_p),
-                ("chunk_starts", ctypes.c_void_p)]
+                ("chunk_starts", ctypes.c_void_p), ("q_doc_limits", ctypes.c_void_p)]
 
 
 def lib_path() -> str:
@@ -73,6 +73,8 @@ def lib():
             "pic_store_put": [vp, u64, i64, vp, vp, vp],
             "pic_store_lookup": [vp, u64, vp],
             "pic_store_remove": [vp, u64, vp],
+            "pic_store_derive": [vp, u64, u64, i32, vp, vp],
+            "pic_store_write_rows": [vp, u64, i32, i32, vp, vp, vp, vp],
             "pic_store_usage": [vp, vp, vp, vp],
             "pic_link_attn": [vp, vp, i32, vp, vp, vp, f32, vp, vp, vp],
             "pic_link_decode": [vp, vp, i32, vp, vp, vp, f32, i32, vp, vp, vp],
@@ -163,6 +165,18 @@ class Store:
         """pic_store_remove: frees the chunk's pages once `stream`'s earlier work is done."""
         _check(lib().pic_store_remove(self.handle, int(chunk_id), stream))
 
+    def derive(self, new_id: int, base_id: int, rows, stream: Optional[int] = None):
+        """pic_store_derive: new_id = base_id with private copies of the pages holding `rows`."""
+        r = np.ascontiguousarray(rows, dtype=np.int32)
+        _check(lib().pic_store_derive(self.handle, int(new_id), int(base_id), int(r.size),
+                                      r.ctypes.data if r.size else None, stream))
+
+    def write_rows(self, chunk_id: int, layer: int, rows, k, v, stream: Optional[int] = None):
+        """pic_store_write_rows: token-major K / V rows of one layer into a derived chunk."""
+        r = np.ascontiguousarray(rows, dtype=np.int32)
+        _check(lib().pic_store_write_rows(self.handle, int(chunk_id), int(layer), int(r.size),
+                                          r.ctypes.data if r.size else None, _ptr(k), _ptr(v), stream))
+
     def lookup(self, chunk_id: int) -> int:
         n = ctypes.c_int64()
         _check(lib().pic_store_lookup(self.handle, int(chunk_id), ctypes.byref(n)))
@@ -175,34 +189,38 @@ class Store:
 
 
 def _req(chunk_offsets, chunk_ids, q_offsets, self_offsets, keep: list, layer: int = 0,
-         chunk_starts=None):
+         chunk_starts=None, q_doc_limits=None):
     co = _host_i32(chunk_offsets)
     ids = np.ascontiguousarray(chunk_ids, dtype=np.uint64)
     qo = _host_i32(q_offsets)
     so = _host_i32(self_offsets)
     st = _host_i32(chunk_starts)
-    keep += [co, ids, qo, so, st]
+    dl = _host_i32(q_doc_limits)
+    keep += [co, ids, qo, so, st, dl]
     return LinkReq(len(qo) - 1, int(layer), co.ctypes.data, ids.ctypes.data if ids.size else None,
                    qo.ctypes.data, None if so is None else so.ctypes.data,
-                   None if st is None or not st.size else st.ctypes.data)
+                   None if st is None or not st.size else st.ctypes.data,
+                   None if dl is None or not dl.size else dl.ctypes.data)
 
 
 def link_attn(store: Store, chunk_offsets, chunk_ids, q_offsets, self_offsets, n_q_heads: int, q,
               k_self, v_self, softmax_scale: float, out, lse=None, stream: Optional[int] = None,
-              layer: int = 0, chunk_starts=None):
+              layer: int = 0, chunk_starts=None, q_doc_limits=None):
     """pic_link_attn: prefill-shaped link attention on store layer `layer`."""
     keep: list = []
-    req = _req(chunk_offsets, chunk_ids, q_offsets, self_offsets, keep, layer, chunk_starts)
+    req = _req(chunk_offsets, chunk_ids, q_offsets, self_offsets, keep, layer, chunk_starts,
+               q_doc_limits)
     _check(lib().pic_link_attn(store.handle, ctypes.byref(req), int(n_q_heads), _ptr(q), _ptr(k_self),
                                _ptr(v_self), float(softmax_scale), _ptr(out), _ptr(lse), stream))
 
 
 def link_decode(store: Store, chunk_offsets, chunk_ids, q_offsets, self_offsets, n_q_heads: int, q,
                 k_self, v_self, softmax_scale: float, out, lse=None, num_splits: int = 0,
-                stream: Optional[int] = None, layer: int = 0, chunk_starts=None):
+                stream: Optional[int] = None, layer: int = 0, chunk_starts=None, q_doc_limits=None):
     """pic_link_decode: decode-shaped link attention with split-K on store layer `layer`."""
     keep: list = []
-    req = _req(chunk_offsets, chunk_ids, q_offsets, self_offsets, keep, layer, chunk_starts)
+    req = _req(chunk_offsets, chunk_ids, q_offsets, self_offsets, keep, layer, chunk_starts,
+               q_doc_limits)
     _check(lib().pic_link_decode(store.handle, ctypes.byref(req), int(n_q_heads), _ptr(q), _ptr(k_self),
                                  _ptr(v_self), float(softmax_scale), int(num_splits), _ptr(out),
                                  _ptr(lse), stream))
@@ -219,9 +237,10 @@ class LinkPlan:
     """pic_link_plan_*: a request batch resolved once, run per layer / decode step."""
 
     def __init__(self, store: Store, chunk_offsets, chunk_ids, q_offsets, self_offsets, n_q_heads: int,
-                 mode: int = PREFILL, num_splits: int = 0, chunk_starts=None):
+                 mode: int = PREFILL, num_splits: int = 0, chunk_starts=None, q_doc_limits=None):
         keep: list = []
-        req = _req(chunk_offsets, chunk_ids, q_offsets, self_offsets, keep, chunk_starts=chunk_starts)
+        req = _req(chunk_offsets, chunk_ids, q_offsets, self_offsets, keep, chunk_starts=chunk_starts,
+                   q_doc_limits=q_doc_limits)
         h = ctypes.c_void_p()
         _check(lib().pic_link_plan_create(store.handle, ctypes.byref(req), int(n_q_heads), int(mode),
                                           int(num_splits), ctypes.byref(h)))
