@@ -203,13 +203,18 @@ struct DocLim {
 // Masks keys past the tile's valid end, in own tiles keys after the row's
 // causal limit, and in document tiles rows at or past the row's limit.
 // s0[x] / s1[x] hold key (x>>3)*16 + g*8 + (x&7) (+32).
+// kLim: the call carries per-row limits (a separate instantiation, so that
+// calls without them run no limit code).
+template <bool kLim>
 __device__ __forceinline__ void mask_tile(const Ctx &c, f32x16 &s0, f32x16 &s1, const TileRef &r,
                                           int lim, const DocLim &dlm) {
   const int nvalid = r.nvalid;
-  if (r.own || nvalid < kTile || r.tok + kTile > dlm.wmin) {
+  if (r.own || nvalid < kTile || (kLim && r.tok + kTile > dlm.wmin)) {
     // visible iff key <= kl; compared as (key - g*8) against kl - g*8 so the
     // left side is a compile-time constant per element
-    const int kl = (r.own ? min(lim - r.j0, nvalid - 1) : min(dlm.dl - r.tok, nvalid) - 1) -
+    const int kl = (r.own   ? min(lim - r.j0, nvalid - 1)
+                    : kLim ? min(dlm.dl - r.tok, nvalid) - 1
+                           : nvalid - 1) -
                    c.g * 8;
 #pragma unroll
     for (int x = 0; x < 16; ++x) {
@@ -224,6 +229,7 @@ __device__ __forceinline__ void mask_tile(const Ctx &c, f32x16 &s0, f32x16 &s1, 
 // rescale), O += V^T P^T from vt. In both matrix sections the LDS fragment
 // reads are issued a few MFMAs ahead of their use (scheduling groups), so an
 // MFMA does not wait on the read issued right before it.
+template <bool kLim>
 __device__ __forceinline__ void compute_tile(const Ctx &c, const uint4 *kt, const uint4 *vt,
                                              const bf16x8 (&qf)[8], Acc &a, const TileRef &ref,
                                              int lim, const DocLim &dlm, float sc,
@@ -255,7 +261,7 @@ __device__ __forceinline__ void compute_tile(const Ctx &c, const uint4 *kt, cons
     s1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kb[st], qf[st], s1, 0, 0, 0);
     __builtin_amdgcn_sched_barrier(0);
   }
-  mask_tile(c, s0, s1, ref, lim, dlm);
+  mask_tile<kLim>(c, s0, s1, ref, lim, dlm);
 
   float tmax = -INFINITY;
 #pragma unroll
@@ -308,6 +314,7 @@ __device__ __forceinline__ void compute_tile(const Ctx &c, const uint4 *kt, cons
   }
 }
 
+template <bool kLim>
 __global__ __launch_bounds__(kWaves * 64, 8 / kWaves) void link_mfma_d128_kernel(LinkParams p) {
   __shared__ uint4 sk0[kTile * 16], sk1[kTile * 16];
   __shared__ uint4 sv0[kD * 8], sv1[kD * 8];
@@ -359,7 +366,7 @@ __global__ __launch_bounds__(kWaves * 64, 8 / kWaves) void link_mfma_d128_kernel
   const int lim = rvalid ? qi + R.ls - R.lq : -1;     // last visible own key
   const int64_t orow = (int64_t)(R.q0 + qi) * p.n_q_heads + qh;
   DocLim dlm{kNoLimit, kNoLimit};
-  if (p.doc_lim) {
+  if (kLim) {
     if (rvalid) dlm.dl = p.doc_lim[R.q0 + qi];
     int w = dlm.dl;
 #pragma unroll
@@ -423,7 +430,7 @@ __global__ __launch_bounds__(kWaves * 64, 8 / kWaves) void link_mfma_d128_kernel
     // tile t in buffers 0; copy tile t+1 into buffers 1
     ref1 = t + 1 < t_end ? tile_ref(c, t + 1) : ref0;
     if (active)
-      compute_tile(c, sk0, sv0, qf, a, ref0, lim, dlm, sc, ref1, sk1, sv1);
+      compute_tile<kLim>(c, sk0, sv0, qf, a, ref0, lim, dlm, sc, ref1, sk1, sv1);
     else
       issue_tile(c, ref1, sk1, sv1);
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
@@ -432,7 +439,7 @@ __global__ __launch_bounds__(kWaves * 64, 8 / kWaves) void link_mfma_d128_kernel
     // tile t+1 in buffers 1; copy tile t+2 into buffers 0
     ref0 = t + 2 < t_end ? tile_ref(c, t + 2) : ref1;
     if (active)
-      compute_tile(c, sk1, sv1, qf, a, ref1, lim, dlm, sc, ref0, sk0, sv0);
+      compute_tile<kLim>(c, sk1, sv1, qf, a, ref1, lim, dlm, sc, ref0, sk0, sv0);
     else
       issue_tile(c, ref0, sk0, sv0);
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
@@ -484,7 +491,10 @@ int mfma_d128_blocks_per_cu() { return 8 / kWaves; }
 hipError_t launch_link_mfma_d128(const LinkParams &p, hipStream_t st, const char **name) {
   *name = "link_mfma_d128_kernel";
   dim3 grid(p.n_groups * p.nrb, p.num_splits);
-  hipLaunchKernelGGL(link_mfma_d128_kernel, grid, dim3(kWaves * 64), 0, st, p);
+  if (p.doc_lim)
+    hipLaunchKernelGGL(link_mfma_d128_kernel<true>, grid, dim3(kWaves * 64), 0, st, p);
+  else
+    hipLaunchKernelGGL(link_mfma_d128_kernel<false>, grid, dim3(kWaves * 64), 0, st, p);
   return hipGetLastError();
 }
 

@@ -166,6 +166,9 @@ __device__ __forceinline__ void tile_copy(int i, const char *k, uint32_t dst, in
 }
 constexpr int kCopies = kTile / 4 + 2;   // 18 copies per lane per tile
 
+// kLim: the call carries per-row limits on the linked rows (a separate
+// instantiation, so that calls without them run no limit code).
+template <bool kLim>
 __global__ __launch_bounds__(256, 1) void link_mla_kernel(LinkParams p) {
   __shared__ MlaSmem sm;
   __shared__ uint4 sk0[kTileChunks], sk1[kTileChunks];
@@ -217,7 +220,7 @@ __global__ __launch_bounds__(256, 1) void link_mla_kernel(LinkParams p) {
   // Limit on the visible linked rows of this lane's score row (dl_s) and its
   // minimum over the wave (wmin_s).
   int dl_s = kNoLimit, wmin_s = kNoLimit;
-  if (p.doc_lim) {
+  if (kLim) {
     if (rvalid[rb_s]) dl_s = p.doc_lim[R.q0 + (row0 + 32 * rb_s + n) / group];
     int w = dl_s;
 #pragma unroll
@@ -369,9 +372,10 @@ __global__ __launch_bounds__(256, 1) void link_mla_kernel(LinkParams p) {
       __builtin_amdgcn_sched_barrier(0);
     }
     // s[x]: key 32 kb_s + (x>>3)*16 + g*8 + (x&7) of row 32 rb_s + n
-    if (ref.own || ref.nvalid < kTile || ref.tok + kTile > wmin_s) {
+    if (ref.own || ref.nvalid < kTile || (kLim && ref.tok + kTile > wmin_s)) {
       const int kl = (ref.own ? min(lim[rb_s] - ref.j0, ref.nvalid - 1)
-                              : min(dl_s - ref.tok, ref.nvalid) - 1) -
+                      : kLim  ? min(dl_s - ref.tok, ref.nvalid) - 1
+                              : ref.nvalid - 1) -
                      32 * kb_s - g * 8;
 #pragma unroll
       for (int x = 0; x < 16; ++x)
@@ -513,7 +517,10 @@ int mla_rows_per_block() { return kRowsMla; }
 hipError_t launch_link_mla(const LinkParams &p, hipStream_t st, const char **name) {
   *name = "link_mla_kernel";
   dim3 grid(p.batch * p.nrb, p.num_splits);
-  hipLaunchKernelGGL(link_mla_kernel, grid, dim3(256), 0, st, p);
+  if (p.doc_lim)
+    hipLaunchKernelGGL(link_mla_kernel<true>, grid, dim3(256), 0, st, p);
+  else
+    hipLaunchKernelGGL(link_mla_kernel<false>, grid, dim3(256), 0, st, p);
   return hipGetLastError();
 }
 
