@@ -616,6 +616,7 @@ pic_status setup_call(pic_store *s, const pic_link_req *req, int32_t n_q_heads, 
                              : kern == Kern::Mla   ? mla_rows_per_block()
                                                    : decode_d128_max_rows();
   lp.nrb = std::max(1, (P.max_rows + rows_per_block - 1) / rows_per_block);
+  lp.max_rows = P.max_rows;
   lp.n_groups = req->batch * d.n_kv_heads;
   if (kern == Kern::Mfma128) lp.n_groups = (int32_t)round_up(lp.n_groups, 8);
 

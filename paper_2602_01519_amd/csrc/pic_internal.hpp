@@ -66,6 +66,7 @@ struct LinkParams {
   int32_t total_q;        // Tq
   int32_t num_splits;     // 1: write out/lse directly; >1: write partials
   int32_t nrb;            // row blocks per (request, kv head)
+  int32_t max_rows;       // most rows of one (request, kv head)
   int32_t n_groups;       // batch * n_kv_heads, padded as the kernel requires
   float scale_log2;       // softmax_scale * log2(e)
 };
