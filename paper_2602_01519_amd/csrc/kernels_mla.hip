@@ -58,6 +58,17 @@ constexpr float kJumpSum = 18446744073709551616.0f;  // 2^64: redo a tile past i
 constexpr int kAhead = 6;                // K fragment read lead in the score loop
 constexpr int kVLead = 3;                // value fragment read lead in the value loop
 
+// Workgroup barrier for exchanges through LDS only (probabilities, flags,
+// maxima inside a tile): it waits for this wave's LDS accesses but not for
+// the next tile's copies in flight, which the memory fence of __syncthreads
+// would wait for (forcing them to land before the value product). The empty
+// asm statements keep the compiler from moving memory accesses across it.
+__device__ __forceinline__ void lds_barrier() {
+  asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
+
 __device__ __forceinline__ int swz(int r) { return ((r & 3) << 2) | ((r >> 2) & 3); }
 __device__ __forceinline__ int swr(int r) { return (r >> 1) & 7; }
 
@@ -392,7 +403,7 @@ __global__ __launch_bounds__(256, 1) void link_mla_kernel(LinkParams p) {
     const bool jump = !(ts <= kJumpSum) || (mu == -INFINITY && ts > 0.f);
     const bool wjump = __any(jump);
     if (lane == 0) ((int *)&sm.jump)[wave] = wjump;
-    __syncthreads();
+    lds_barrier();
     // 3. O^T += V^T P^T for this wave's 128 value dims
     // Fragment f = 4 ks + db: two transposing reads (key rows 16 ks ..,
     // value block db), issued kVLead fragments ahead of its two MFMAs; the
@@ -424,7 +435,7 @@ __global__ __launch_bounds__(256, 1) void link_mla_kernel(LinkParams p) {
       for (int x = 0; x < 16; x += 2) tmax = fmaxf(fmaxf(tmax, s[x]), s[x + 1]);
       tmax = half_swap_max(tmax) * sc;
       if (g == 0) sm.xm[wave][n] = tmax;
-      __syncthreads();
+      lds_barrier();
       float mnew[2];
 #pragma unroll
       for (int rb = 0; rb < 2; ++rb)
@@ -432,7 +443,7 @@ __global__ __launch_bounds__(256, 1) void link_mla_kernel(LinkParams p) {
       lsum = lsum0;
       rescale(mnew);
       lsum += publish(s, rb_s ? m_used[1] : m_used[0]);
-      __syncthreads();
+      lds_barrier();
     }
 #pragma unroll
     for (int f = 0; f < kVLead; ++f) read_frag(f);
