@@ -3,6 +3,7 @@
 #include "pic_internal.hpp"
 
 #include <cmath>
+#include <type_traits>
 
 namespace pic {
 namespace {
@@ -155,6 +156,9 @@ struct PrepParams {
   const uint4 *copy_src;      // table copy (z slice prep_z), n16 = 0: none
   uint4 *copy_dst;
   int64_t copy_n16;
+  int32_t has_own;            // own[] holds every request's own rows and slot
+  char *work;                 // workspace the slots are in
+  OwnArg own[kOwnArgs];
 };
 
 // One 64-token x 64-value tile of own V, transposed into the slot's V block.
@@ -208,9 +212,20 @@ __global__ void prep_own_kernel(PrepParams pp) {
       pp.copy_dst[i] = pp.copy_src[i];
     return;
   }
-  const ReqEntry R = pp.reqs[blockIdx.z];
+  ReqEntry R;
+  LinkEntry L;
+  if (pp.has_own) {     // from the kernel arguments: no table read
+    const OwnArg o = pp.own[blockIdx.z];
+    R.s0 = o.s0;
+    R.ls = o.ls;
+    L.lp = (o.ls + kTile - 1) / kTile * kTile;
+    L.k = pp.work + o.off;
+    L.v = pp.work + o.off + (int64_t)L.lp * pp.heads * pp.d_k * pp.esz;
+  } else {
+    R = pp.reqs[blockIdx.z];
+    if (R.ls > 0) L = pp.links[R.link0 + R.nlinks - 1];
+  }
   if (R.ls == 0) return;
-  const LinkEntry L = pp.links[R.link0 + R.nlinks - 1];
   if ((int)blockIdx.x < pp.rows_blocks) {
     const int vpr = pp.d_k * pp.esz / 16;
     const uint4 *src = (const uint4 *)pp.k_self;
@@ -438,88 +453,92 @@ __global__ __launch_bounds__(256) void link_valu_kernel(LinkParams p) {
 }
 
 // ---------------------------------------------------------------------------
-// Split-K combine: one wave per output row. Lane j covers value dims
-// 2j, 2j+1 of every 128-wide chunk (8-byte loads, a row's partials of one
-// split are one coalesced 512-byte read per chunk). The partial outputs of
-// the first kPre splits are loaded before the split maxima are reduced, so
-// a row costs one memory round trip rather than two; each split's weight
-// exp2(m_s - M) is computed once (lane s) and broadcast with readlane.
-// Every (split, row) partial is written by the attention kernels (zeros with
-// m = -inf for an empty split), so the loads need no guard.
+// Split-K combine: one wave per output row, lane j covering value dims
+// 2j, 2j+1 of each of the row's kChunks 128-wide chunks (8-byte loads: a
+// row's partial of one split is one coalesced 512-byte read per chunk).
+// One pass over the splits, kB at a time: their maxima and sums (wave-
+// uniform, read through the scalar cache) and partial outputs are loaded
+// together, and the running merge is rescaled when the maximum grows, as in
+// the online softmax -- a row with up to kB splits costs one memory round
+// trip and no cross-lane reduction. Every (split, row) partial is written by
+// the attention kernels (zeros with m = -inf for an empty split).
 template <typename T>
+__device__ __forceinline__ void store_pair(T *out, int e, float x, float y);
+template <>
+__device__ __forceinline__ void store_pair<float>(float *out, int e, float x, float y) {
+  *(float2 *)(out + e) = make_float2(x, y);
+}
+template <>
+__device__ __forceinline__ void store_pair<uint16_t>(uint16_t *out, int e, float x, float y) {
+  *(uint32_t *)(out + e) = (uint32_t)bf16_rne(x) | ((uint32_t)bf16_rne(y) << 16);
+}
+
+template <typename T, int kChunks>
 __global__ __launch_bounds__(256) void combine_kernel(LinkParams p) {
-  constexpr int kPre = 8;
-  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  typedef __attribute__((address_space(4))) const float *const_floats;
+  constexpr int kB = 4;
+  // the wave index read as a uniform value, so the row's split loads are
+  // scalar loads
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
   const int64_t rows = (int64_t)p.total_q * p.n_q_heads;
   const int64_t orow = (int64_t)blockIdx.x * 4 + wave;
   if (orow >= rows) return;
   const int S = p.num_splits, dv = p.d_v;
-  const int nchunk = (dv + 127) / 128;
-  auto po = [&](int s, int e) {
-    return *(const float2 *)(p.part_o + (s * rows + orow) * dv + e);
-  };
-  // prefetch: chunk 0 of the first kPre splits
   const int e0 = 2 * lane;
-  float2 pre[kPre];
+  const const_floats pm = (const_floats)p.part_m + orow;
+  const const_floats pl = (const_floats)p.part_l + orow;
+  float M = -INFINITY, L = 0.f;
+  float2 acc[kChunks];
 #pragma unroll
-  for (int s = 0; s < kPre; ++s)
-    pre[s] = (s < S && e0 < dv) ? po(s, e0) : make_float2(0.f, 0.f);
-  // split maxima and weights: lane l holds splits l, l + 64, l + 128, l + 192
-  float ms[4], ls[4], M = -INFINITY;
+  for (int c = 0; c < kChunks; ++c) acc[c] = make_float2(0.f, 0.f);
+  for (int s0 = 0; s0 < S; s0 += kB) {
+    float mb[kB], lb[kB];
+    float2 vb[kB][kChunks];
 #pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    const int sj = lane + 64 * j;
-    ms[j] = sj < S ? p.part_m[sj * rows + orow] : -INFINITY;
-    ls[j] = sj < S ? p.part_l[sj * rows + orow] : 0.f;
-    M = fmaxf(M, ms[j]);
-  }
+    for (int i = 0; i < kB; ++i) {
+      const int sc = min(s0 + i, S - 1);      // past the last split: reread it, weight 0
+      mb[i] = pm[(int64_t)sc * rows];
+      lb[i] = pl[(int64_t)sc * rows];
+      const float *po = p.part_o + ((int64_t)sc * rows + orow) * dv;
 #pragma unroll
-  for (int o = 32; o > 0; o >>= 1) M = fmaxf(M, __shfl_xor(M, o));
-  T *out = (T *)p.out + orow * dv;
-  if (M == -INFINITY) {
-    for (int e = lane; e < dv; e += 64) out[e] = from_f32<T>(0.f);
-    if (p.lse && lane == 0) p.lse[orow] = -INFINITY;
-    return;
-  }
-  float w[4], L = 0.f;
-#pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    const int sj = lane + 64 * j;
-    w[j] = ms[j] == -INFINITY ? 0.f : exp2f(ms[j] - M);
-    if (sj < S) L += w[j] * ls[j];
-  }
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) L += __shfl_xor(L, o);
-  const float inv = 1.f / L;
-  auto weight = [&](int s) {   // s is uniform
-    const float wj = s < 64 ? w[0] : s < 128 ? w[1] : s < 192 ? w[2] : w[3];
-    return __builtin_amdgcn_readlane(__float_as_int(wj), s & 63);
-  };
-  for (int c = 0; c < nchunk; ++c) {
-    const int e = 128 * c + e0;
-    float ax = 0.f, ay = 0.f;
-#pragma unroll
-    for (int s = 0; s < kPre; ++s) {
-      if (s >= S) break;
-      const float ws = __int_as_float(weight(s));
-      const float2 v = c == 0 ? pre[s] : (e < dv ? po(s, e) : make_float2(0.f, 0.f));
-      ax += ws * v.x;
-      ay += ws * v.y;
+      for (int c = 0; c < kChunks; ++c) {
+        const int e = 128 * c + e0;
+        vb[i][c] = e < dv ? *(const float2 *)(po + e) : make_float2(0.f, 0.f);
+      }
+      if (s0 + i >= S) mb[i] = -INFINITY;
     }
-    for (int s = kPre; s < S; ++s) {
-      const float ws = __int_as_float(weight(s));
-      if (e < dv) {
-        const float2 v = po(s, e);
-        ax += ws * v.x;
-        ay += ws * v.y;
+    float bm = M;
+#pragma unroll
+    for (int i = 0; i < kB; ++i) bm = fmaxf(bm, mb[i]);
+    if (bm == -INFINITY) continue;
+    const float r = M == -INFINITY ? 0.f : exp2f(M - bm);
+    L *= r;
+#pragma unroll
+    for (int c = 0; c < kChunks; ++c) {
+      acc[c].x *= r;
+      acc[c].y *= r;
+    }
+#pragma unroll
+    for (int i = 0; i < kB; ++i) {
+      const float w = mb[i] == -INFINITY ? 0.f : exp2f(mb[i] - bm);
+      L += w * lb[i];
+#pragma unroll
+      for (int c = 0; c < kChunks; ++c) {
+        acc[c].x += w * vb[i][c].x;
+        acc[c].y += w * vb[i][c].y;
       }
     }
-    if (e < dv) {
-      out[e] = from_f32<T>(ax * inv);
-      out[e + 1] = from_f32<T>(ay * inv);
-    }
+    M = bm;
   }
-  if (p.lse && lane == 0) p.lse[orow] = (M + log2f(L)) * 0.69314718055994531f;
+  T *out = (T *)p.out + orow * dv;
+  const float inv = M == -INFINITY ? 0.f : 1.f / L;
+#pragma unroll
+  for (int c = 0; c < kChunks; ++c) {
+    const int e = 128 * c + e0;
+    if (e < dv) store_pair<T>(out, e, acc[c].x * inv, acc[c].y * inv);
+  }
+  if (p.lse && lane == 0)
+    p.lse[orow] = M == -INFINITY ? -INFINITY : (M + log2f(L)) * 0.69314718055994531f;
 }
 
 size_t valu_lds_bytes(int esz, int mla, int d_k, int d_v) {
@@ -562,10 +581,20 @@ hipError_t launch_combine(const LinkParams &p, int dtype, hipStream_t st) {
   const int64_t rows = (int64_t)p.total_q * p.n_q_heads;
   if (rows == 0) return hipSuccess;
   dim3 grid((unsigned)((rows + 3) / 4));
-  if (dtype == 0)
-    hipLaunchKernelGGL(combine_kernel<float>, grid, dim3(256), 0, st, p);
+  const int chunks = (p.d_v + 127) / 128;     // 1 .. 8 (d_v <= 1024)
+  auto go = [&](auto kc) {
+    constexpr int kC = decltype(kc)::value;
+    if (dtype == 0)
+      hipLaunchKernelGGL((combine_kernel<float, kC>), grid, dim3(256), 0, st, p);
+    else
+      hipLaunchKernelGGL((combine_kernel<uint16_t, kC>), grid, dim3(256), 0, st, p);
+  };
+  if (chunks == 1)
+    go(std::integral_constant<int, 1>());
+  else if (chunks <= 4)
+    go(std::integral_constant<int, 4>());
   else
-    hipLaunchKernelGGL(combine_kernel<uint16_t>, grid, dim3(256), 0, st, p);
+    go(std::integral_constant<int, 8>());
   return hipGetLastError();
 }
 
@@ -638,10 +667,15 @@ hipError_t launch_gather(const LinkEntry *links, int32_t n_links, int64_t total_
 }
 
 hipError_t launch_prologue(const LinkParams &p, const LinkEntry *links, const ReqEntry *reqs,
-                           int32_t mla, int32_t esz, int32_t max_own_lp, const void *copy_src,
-                           void *copy_dst, int64_t copy_bytes, hipStream_t st) {
+                           int32_t mla, int32_t esz, int32_t max_own_lp, const OwnArg *own,
+                           const void *work, const void *copy_src, void *copy_dst,
+                           int64_t copy_bytes, hipStream_t st) {
   if (p.batch == 0) return hipSuccess;
   PrepParams pp;
+  pp.has_own = own != nullptr && p.batch <= kOwnArgs;
+  pp.work = (char *)work;
+  if (pp.has_own)
+    for (int32_t r = 0; r < p.batch; ++r) pp.own[r] = own[r];
   pp.reqs = reqs;
   pp.links = links;
   pp.copy_src = (const uint4 *)copy_src;

@@ -567,6 +567,7 @@ struct Setup {
   Kern kern = Kern::Valu;
   int32_t splits = 1;
   LinkParams lp{};               // shapes only: no tables, tensors or scale yet
+  std::vector<OwnArg> own_args;  // per request, for the prologue (batch <= kOwnArgs)
   size_t part_off = 0, part_bytes = 0;
   size_t work_bytes() const { return part_off + part_bytes; }
 };
@@ -590,6 +591,15 @@ pic_status setup_call(pic_store *s, const pic_link_req *req, int32_t n_q_heads, 
   lp.d_v = d.d_v;
   lp.total_q = P.total_q;
   if (req->batch == 0 || P.total_q == 0) return PIC_OK;
+  if (P.max_own_lp > 0 && req->batch <= kOwnArgs) {
+    C.own_args.assign(req->batch, OwnArg{0, 0, 0});
+    size_t k = 0;
+    for (int32_t r = 0; r < req->batch; ++r) {
+      const ReqEntry &R = P.reqs[r];
+      if (R.ls == 0) continue;
+      C.own_args[r] = OwnArg{R.s0, R.ls, P.own[k++].second};
+    }
+  }
 
   // Kernel choice.
   //   bf16 GQA d=128: decode-shaped calls with at most 16 rows per (request,
@@ -694,6 +704,7 @@ pic_status launch_call(const pic_store *s, const Setup &C, LinkParams lp, void *
   }
   if (C.P.max_own_lp > 0 || pro.copy_bytes > 0) {
     hipError_t e = launch_prologue(lp, pro.links, pro.reqs, mla, s->esz, C.P.max_own_lp,
+                                   C.own_args.empty() ? nullptr : C.own_args.data(), work,
                                    pro.copy_src, pro.copy_dst, pro.copy_bytes, st);
     if (e != hipSuccess) return hip_fail(e, "prep_own_kernel");
   }

@@ -106,9 +106,18 @@ hipError_t launch_mla_up_v(const void *o_lat, const void *w_uv, void *out, int32
 // The call's prologue: lays out the own KV of every request (when
 // max_own_lp > 0; tables read from links / reqs) and copies copy_bytes of
 // tables from copy_src to copy_dst (when copy_bytes > 0).
+// own, if not NULL: per request (batch <= kOwnArgs) its own rows and slot,
+// passed as kernel arguments so that the own-KV layout does not wait for a
+// read of the tables (over PCIe from the staging buffer).
+struct OwnArg {
+  int32_t s0, ls;     // own rows s0 .. s0+ls of k_self / v_self
+  int64_t off;        // slot offset in the workspace (K block, then V^T block)
+};
+constexpr int kOwnArgs = 128;
 hipError_t launch_prologue(const LinkParams &p, const LinkEntry *links, const ReqEntry *reqs,
-                           int32_t mla, int32_t esz, int32_t max_own_lp, const void *copy_src,
-                           void *copy_dst, int64_t copy_bytes, hipStream_t st);
+                           int32_t mla, int32_t esz, int32_t max_own_lp, const OwnArg *own,
+                           const void *work, const void *copy_src, void *copy_dst,
+                           int64_t copy_bytes, hipStream_t st);
 
 // Generic vector-ALU link attention: any d_k <= 576, d_v <= 512, fp32 or bf16.
 hipError_t launch_link_valu(const LinkParams &p, int dtype, int mla, hipStream_t st,
