@@ -180,6 +180,56 @@ def test_blend_recompute_and_link(case):
 
 
 @pytest.mark.parametrize("case", ["gqa_bf16", "mla_bf16"])
+def test_limits_with_starts_over_derived_chunks(case):
+    """Per-query limits, page-aligned starts and derived chunks in one call:
+    the links read [derived doc 3 from token 128 ; base doc 1 ; derived doc 0
+    from token 64], queries see different numbers of those rows."""
+    kind, dtype, d_k = CASES[case]
+    cfg = case_cfg(kind, dtype, d_k, seed=87)
+    n_docs = len(cfg.chunk_len)
+    rng = np.random.default_rng(88)
+    docs = [W.make_chunk(cfg, c) for c in range(n_docs)]
+    fresh = [W.make_chunk(cfg, c, layer=1) for c in range(n_docs)]
+    rows = [pick_rows(rng, cfg.chunk_length(c)) for c in range(n_docs)]
+    new_kv = [(fresh[c][0][rows[c]], None if kind == W.MLA else fresh[c][1][rows[c]])
+              for c in range(n_docs)]
+    spliced = [patched(*docs[c], rows[c], *new_kv[c]) for c in range(n_docs)]
+    print(f"case {case} limits + starts + derived", flush=True)
+    store = pic.Store(kind, dtype, cfg.n_kv_heads, cfg.d_k, cfg.d_v,
+                      2 * sum(runner.padded(cfg.chunk_length(c)) for c in range(n_docs)))
+    try:
+        base = [int(W.chunk_id_of(c)) for c in range(n_docs)]
+        blend = [int(W.chunk_id_of(600 + c)) for c in range(n_docs)]
+        for c in range(n_docs):
+            store.put(base[c], cfg.chunk_length(c), dev(docs[c][0]), dev(docs[c][1]), stream())
+            store.derive(blend[c], base[c], rows[c], stream())
+            store.write_rows(blend[c], 0, rows[c], dev(new_kv[c][0]), dev(new_kv[c][1]), stream())
+        ids = [blend[3], base[1], blend[0]]
+        starts = np.array([128, 0, 64], np.int32)
+        links = [tuple(None if x is None else x[st:] for x in kv)
+                 for kv, st in zip([spliced[3], docs[1], spliced[0]], starts)]
+        ld = sum(k.shape[0] for k, _ in links)
+        nq = 70
+        q = rand_q(cfg, rng, nq)
+        lims = rng.integers(0, ld + 1, nq).astype(np.int32)
+        lims[:3] = (0, ld, 1)
+        qo = np.array([0, nq], np.int32)
+        tq = q.shape[0]
+        et = torch.float32 if cfg.dtype == W.F32 else torch.int16
+        out = torch.empty((tq, cfg.n_q_heads, cfg.d_v), dtype=et, device="cuda")
+        lse = torch.empty((tq, cfg.n_q_heads), dtype=torch.float32, device="cuda")
+        pic.link_attn(store, np.array([0, 3], np.int32), np.asarray(ids, np.uint64), qo, None,
+                      cfg.n_q_heads, dev(q), None, None, float(np.float32(cfg.scale)), out, lse,
+                      stream=stream(), chunk_starts=starts, q_doc_limits=lims)
+        torch.cuda.synchronize()
+        ref, ref_lse = ref_link(cfg, [links], q, qo, lims=lims)
+        compare(cfg, runner.to_host(out, cfg.dtype), lse.cpu().numpy().astype(np.float64), ref,
+                ref_lse, label=f"{case} limits + starts + derived")
+    finally:
+        store.close()
+
+
+@pytest.mark.parametrize("case", ["gqa_bf16", "mla_bf16"])
 def test_limits_in_decode_calls(case):
     """Decode-shaped calls with limits: one token per request (the links are
     cut on the host), and several tokens of one request with different

@@ -196,6 +196,29 @@ def test_degenerate_requests(case):
     run_and_check(cfg, links=DEGENERATE_LINKS)
 
 
+def _big_batch(kind, dtype=W.BF16):
+    """150 requests: more than the prologue takes as kernel arguments, so the
+    own-KV layout reads the request and link tables instead."""
+    n = 150
+    common = dict(chunk_lens=(70, 64, 130, 9), batch=n, links=(0, 2), seed=17,
+                  q_len=tuple((3, 1, 5)[r % 3] for r in range(n)),
+                  self_len=tuple((4, 1, 9)[r % 3] for r in range(n)))
+    if kind == W.MLA:
+        return W.small_config("big_batch_mla", kind=W.MLA, n_q_heads=16, d_k=576, d_v=512,
+                              q_std=1.0, scale=1 / math.sqrt(192), **common)
+    if dtype == W.F32:
+        return W.small_config("big_batch_f32", dtype=W.F32, d_k=64, **common)
+    return W.small_config("big_batch_gqa", d_k=128, **common)
+
+
+@pytest.mark.parametrize("case", ["gqa", "mla", "f32"])
+def test_batch_beyond_prologue_arguments(case):
+    cfg = _big_batch(W.MLA if case == "mla" else W.GQA, W.F32 if case == "f32" else W.BF16)
+    run_and_check(cfg)
+    if case == "gqa":
+        run_and_check(cfg, decode=True, num_splits=3)
+
+
 @pytest.mark.parametrize("case", ["gqa", "mla"])
 def test_empty_key_sets(case):
     """Cross-only attention with a request that links nothing: its rows see no
