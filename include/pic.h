@@ -124,7 +124,9 @@ pic_status pic_store_remove(pic_store *store, uint64_t chunk_id, void *stream);
  *   strictly increasing, each below the base's length) are private copies
  *   made on `stream`; every other page is shared with the base (no copy).
  *   The base may be removed first: shared pages live while a chunk holds
- *   them. Errors: INVALID, NOT_FOUND (base), EXISTS (new_id), OOM, HIP.
+ *   them (a run of pages allocated together is freed once no chunk holds
+ *   any of its pages). Errors: INVALID, NOT_FOUND (base), EXISTS (new_id),
+ *   OOM, HIP.
  * pic_store_write_rows: writes token-major K / V rows of one layer into a
  *   derived chunk: k device [n_rows][n_kv_heads][d_k], v device
  *   [n_rows][n_kv_heads][d_v] (GQA) or NULL (MLA); rows as above, each on a
@@ -145,8 +147,9 @@ pic_status pic_store_write_rows(pic_store *store, uint64_t chunk_id, int32_t lay
 pic_status pic_store_lookup(const pic_store *store, uint64_t chunk_id, int64_t *n_tokens_out);
 
 /* Pool usage in tokens of allocated 64-token pages (pages of removed chunks
- * count until their readers have finished), the capacity, and the number of
- * stored chunks. Any output pointer may be NULL. */
+ * count until their readers have finished; pages shared by derived chunks
+ * count once), the capacity, and the number of stored chunks (derived ones
+ * included). Any output pointer may be NULL. */
 pic_status pic_store_usage(const pic_store *store, int64_t *used_tokens,
                            int64_t *capacity_tokens, int64_t *n_chunks);
 
