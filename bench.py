@@ -37,6 +37,7 @@ sys.path.insert(0, ROOT)
 PEAK_BF16_TFLOPS = 2500.0     # MI355X dense bf16 matrix peak
 PEAK_HBM_GBS = 8000.0         # MI355X HBM3E
 PEAK_FP32_VALU_TFLOPS = 157.3
+PROF_EVERY = 5                # timed steps per kernel-timing event pair
 
 # Source file of each attention kernel: a traffic record measured with
 # rocprofv3 counters is used only while the kernel source is unchanged.
@@ -285,7 +286,10 @@ def main(argv=None):
         torch.cuda.synchronize()
 
     ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    pic.prof_begin()
+    # HIP events around one attention launch in PROF_EVERY (the event pair
+    # adds a few microseconds between kernels), on the launch stream, inside
+    # the timed region
+    pic.prof_begin(PROF_EVERY)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     ev0.record(stream)
@@ -376,6 +380,7 @@ def main(argv=None):
             "traffic": traffic_record(kname, cfg.name),
             "kernel_avg_us": round(kern_avg_ms * 1e3, 3),
             "launches": launches,
+            "launches_timed_every": PROF_EVERY,
         },
         "cpu_baseline": cpu,
     }

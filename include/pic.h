@@ -279,10 +279,14 @@ pic_status pic_mla_up_v(int32_t n_tokens, int32_t n_heads, const void *o_lat, co
 
 /* Kernel timing for measurement. pic_prof_begin() clears and enables
  * recording of HIP events around every launch of the main attention kernel;
- * pic_prof_end() waits for them, disables recording and returns the summed
- * kernel time in milliseconds, the launch count and the kernel's name
- * (name_buf may be NULL). */
+ * pic_prof_begin_sampled(every) around one launch in `every` (1..1000000;
+ * the event pair adds a few microseconds between kernels, so sampling keeps
+ * the timed steps close to an uninstrumented run); pic_prof_end() waits for
+ * them, disables recording and returns the summed kernel time in
+ * milliseconds, the number of timed launches and the kernel's name
+ * (name_buf may be NULL). Errors: INVALID (every out of range), HIP. */
 pic_status pic_prof_begin(void);
+pic_status pic_prof_begin_sampled(int32_t every);
 pic_status pic_prof_end(double *kernel_ms, int64_t *launches, char *name_buf, int32_t name_len);
 
 /* Achievable peaks of this GPU, a second roofline denominator next to the

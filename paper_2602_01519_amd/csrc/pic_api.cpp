@@ -106,6 +106,8 @@ constexpr int kRing = 8;
 struct ProfState {
   std::mutex mu;
   bool on = false;
+  int32_t every = 1;       // time one launch in `every`
+  int64_t seen = 0;        // launches since the last begin
   std::vector<std::pair<hipEvent_t, hipEvent_t>> events;
   std::vector<std::pair<hipEvent_t, hipEvent_t>> spare;
   std::string name;
@@ -535,6 +537,7 @@ void prof_start(hipStream_t st, std::pair<hipEvent_t, hipEvent_t> *ev) {
   ev->first = ev->second = nullptr;
   std::lock_guard<std::mutex> g(g_prof.mu);
   if (!g_prof.on) return;
+  if (g_prof.seen++ % g_prof.every) return;
   if (!g_prof.spare.empty()) {
     *ev = g_prof.spare.back();
     g_prof.spare.pop_back();
@@ -1329,13 +1332,18 @@ pic_status pic_mla_up_v(int32_t n_tokens, int32_t n_heads, const void *o_lat, co
   return PIC_OK;
 }
 
-pic_status pic_prof_begin(void) {
+pic_status pic_prof_begin_sampled(int32_t every) {
+  if (every < 1 || every > 1000000) return fail(PIC_ERR_INVALID, "every must be 1..1000000");
   std::lock_guard<std::mutex> g(g_prof.mu);
   for (auto &ev : g_prof.events) g_prof.spare.push_back(ev);
   g_prof.events.clear();
+  g_prof.every = every;
+  g_prof.seen = 0;
   g_prof.on = true;
   return PIC_OK;
 }
+
+pic_status pic_prof_begin(void) { return pic_prof_begin_sampled(1); }
 
 pic_status pic_prof_end(double *kernel_ms, int64_t *launches, char *name_buf, int32_t name_len) {
   std::lock_guard<std::mutex> g(g_prof.mu);

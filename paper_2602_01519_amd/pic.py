@@ -85,6 +85,7 @@ def lib():
             "pic_mla_absorb_q": [i32, i32, vp, vp, vp, vp],
             "pic_mla_up_v": [i32, i32, vp, vp, vp, vp],
             "pic_prof_begin": [],
+            "pic_prof_begin_sampled": [i32],
             "pic_prof_end": [vp, vp, vp, i32],
             "pic_peak_mfma_bf16": [i32, vp, vp],
             "pic_peak_hbm_read": [vp, i64, vp, vp],
@@ -294,8 +295,9 @@ def peak_hbm_read(buf, nbytes: int, stream: Optional[int] = None) -> float:
     return out.value
 
 
-def prof_begin():
-    _check(lib().pic_prof_begin())
+def prof_begin(every: int = 1):
+    """pic_prof_begin_sampled: time one launch of the attention kernel in `every`."""
+    _check(lib().pic_prof_begin_sampled(int(every)))
 
 
 def prof_end():
