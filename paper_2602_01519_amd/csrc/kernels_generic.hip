@@ -266,6 +266,37 @@ __global__ void prep_own_kernel(PrepParams pp) {
 
 constexpr int kValuRows = 16;
 
+// Copies rows of 16-byte units from global memory into LDS rows of 4-byte
+// words (row r, unit c at dst[r * stride + 4 c ..]): each thread issues 4
+// loads before storing any, so the loads' latencies overlap (a plain loop
+// waits for each load before its store). Past the end a thread reloads the
+// last unit and stores nothing, which keeps the loads free of branches.
+__device__ __forceinline__ void copy_rows_lds(const char *src, int64_t src_row_bytes, int rows,
+                                              int units, uint32_t *dst, int stride) {
+  const int n = rows * units;
+  for (int base = threadIdx.x; base < n; base += 4 * blockDim.x) {
+    uint4 v[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int i = min(base + u * (int)blockDim.x, n - 1);
+      const int r = i / units, c = i - r * units;
+      v[u] = *(const uint4 *)(src + r * src_row_bytes + 16 * c);
+    }
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int i = base + u * blockDim.x;
+      if (i < n) {
+        const int r = i / units, c = i - r * units;
+        uint32_t *d = dst + r * stride + 4 * c;
+        d[0] = v[u].x;
+        d[1] = v[u].y;
+        d[2] = v[u].z;
+        d[3] = v[u].w;
+      }
+    }
+  }
+}
+
 template <typename T, bool MLA>
 __global__ __launch_bounds__(256) void link_valu_kernel(LinkParams p) {
   extern __shared__ float smem[];
@@ -297,15 +328,23 @@ __global__ __launch_bounds__(256) void link_valu_kernel(LinkParams p) {
   const T *ks_e = (const T *)ks;
   const T *vts_e = (const T *)vts;
 
-  for (int x = threadIdx.x; x < kValuRows * d_k; x += blockDim.x) {
-    const int rl = x / d_k, c = x - rl * d_k;
-    const int row = row0 + rl;
-    float v = 0.f;
-    if (row < nrows) {
+  // the block's query rows, scaled; 4 loads per thread in flight at once
+  for (int base = threadIdx.x; base < kValuRows * d_k; base += 4 * blockDim.x) {
+    float v[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      // rows past the request read its last row (stored as zero below)
+      const int x = min(base + u * (int)blockDim.x, kValuRows * d_k - 1);
+      const int rl = x / d_k, c = x - rl * d_k;
+      const int row = min(row0 + rl, nrows - 1);
       const int i = row / group, h = kvh * group + row % group;
-      v = to_f32(q[((int64_t)(R.q0 + i) * p.n_q_heads + h) * d_k + c]) * p.scale_log2;
+      v[u] = to_f32(q[((int64_t)(R.q0 + i) * p.n_q_heads + h) * d_k + c]);
     }
-    qs[x] = v;
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int x = base + u * blockDim.x;
+      if (x < kValuRows * d_k) qs[x] = row0 + x / d_k < nrows ? v[u] * p.scale_log2 : 0.f;
+    }
   }
 
   int lim[4];          // last visible own key per row (-1: none)
@@ -339,18 +378,12 @@ __global__ __launch_bounds__(256) void link_valu_kernel(LinkParams p) {
     const int j0 = tt * kTile;          // key index within the link (own: within the own KV)
     const int tok = E.tok0 + j0;        // ... within the request's linked rows
     // 64 consecutive key rows (the slot's padding rows are zeros)
-    const uint32_t *src = (const uint32_t *)key_row<T>(E, MLA ? 0 : kvh, tt * kTile, d_k);
-    for (int w = threadIdx.x; w < kTile * kwords; w += blockDim.x) {
-      const int r = w / kwords, c = w - r * kwords;
-      ks[r * kstride + c] = src[w];
-    }
-    if (!MLA) {
-      const T *vsrc = value_at<T>(E, kvh, 0, tt * kTile, d_v);
-      for (int w = threadIdx.x; w < d_v * vwords; w += blockDim.x) {
-        const int e = w / vwords, c = w - e * vwords;
-        vts[e * vstride + c] = ((const uint32_t *)(vsrc + (int64_t)e * E.lp))[c];
-      }
-    }
+    // K rows (d_k elements, whole 16-byte units) and V^T rows (64 keys)
+    copy_rows_lds((const char *)key_row<T>(E, MLA ? 0 : kvh, tt * kTile, d_k),
+                  (int64_t)d_k * sizeof(T), kTile, kwords / 4, ks, kstride);
+    if (!MLA)
+      copy_rows_lds((const char *)value_at<T>(E, kvh, 0, tt * kTile, d_v),
+                    (int64_t)E.lp * sizeof(T), d_v, vwords / 4, vts, vstride);
     __syncthreads();
 
     // scores: lane = key
