@@ -203,8 +203,10 @@ __device__ __forceinline__ void prep_transposed_tile(const ReqEntry &R, const Li
 // The call's prologue. z slices 0 .. prep_z-1 lay out request z's own KV
 // like a chunk slot; the last slice, if any, copies the call's link and
 // request tables from the host-mapped staging buffer to the device (read
-// over PCIe, latency-bound). The prep slices read their two table entries
-// where they are, so neither part waits for the other.
+// over PCIe, latency-bound). The prep slices take their request's own rows
+// and slot from the kernel arguments (batches of up to kOwnArgs requests),
+// else read their two table entries where they are (the staging buffer, or
+// a plan's device tables), so neither part waits for the other.
 __global__ void prep_own_kernel(PrepParams pp) {
   if ((int)blockIdx.z == pp.prep_z) {
     for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < pp.copy_n16;

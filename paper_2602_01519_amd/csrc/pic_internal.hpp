@@ -103,12 +103,13 @@ hipError_t launch_mla_absorb_q(const void *q, const void *w_uk_t, void *q_out, i
                                int32_t n_heads, hipStream_t st);
 hipError_t launch_mla_up_v(const void *o_lat, const void *w_uv, void *out, int32_t n_tokens,
                            int32_t n_heads, hipStream_t st);
-// The call's prologue: lays out the own KV of every request (when
-// max_own_lp > 0; tables read from links / reqs) and copies copy_bytes of
-// tables from copy_src to copy_dst (when copy_bytes > 0).
-// own, if not NULL: per request (batch <= kOwnArgs) its own rows and slot,
-// passed as kernel arguments so that the own-KV layout does not wait for a
-// read of the tables (over PCIe from the staging buffer).
+// The call's prologue: lays out the own KV of every request in its slot
+// in `work` (when max_own_lp > 0) and copies copy_bytes of tables from
+// copy_src to copy_dst (when copy_bytes > 0). The layout takes each
+// request's own rows and slot from `own` (host, batch entries, batch <=
+// kOwnArgs: passed as kernel arguments, so it does not wait for a read of
+// the tables over PCIe from the staging buffer), or, when own is NULL,
+// from the tables at links / reqs.
 struct OwnArg {
   int32_t s0, ls;     // own rows s0 .. s0+ls of k_self / v_self
   int64_t off;        // slot offset in the workspace (K block, then V^T block)
