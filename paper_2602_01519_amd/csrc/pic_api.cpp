@@ -744,13 +744,14 @@ pic_status link_call(pic_store *s, const pic_link_req *req, int32_t n_q_heads, c
   if (rc != PIC_OK) return rc;
   if (C.P.total_q == 0) return PIC_OK;
   const hipStream_t st = (hipStream_t)stream;
+  // the workspace is allocated on the store's device
+  DeviceGuard dg(s->device);
+  if (!dg.ok) return fail(PIC_ERR_HIP, "cannot select the store's device");
   if (C.work_bytes() > 0) {
     rc = ensure_work(s, C.work_bytes());
     if (rc != PIC_OK) return rc;
   }
   place_own(s, C.P, s->work, C.P.links.data());
-  DeviceGuard dg(s->device);
-  if (!dg.ok) return fail(PIC_ERR_HIP, "cannot select the store's device");
   Stage *stage = nullptr;
   TableLayout tl;
   LinkParams lp = C.lp;
