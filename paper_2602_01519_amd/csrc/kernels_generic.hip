@@ -433,24 +433,48 @@ __global__ __launch_bounds__(256) void link_valu_kernel(LinkParams p) {
     for (int r = 0; r < 4; ++r)
 #pragma unroll
       for (int j = 0; j < 8; ++j) acc[r][j] *= alpha[r];
+    // O += P V: per 64-dim value chunk j, keys four at a time with their
+    // probability and value reads issued together (one load at a time per
+    // key made every step wait for the LDS round trip). A lane past d_v
+    // reads a valid column; its sums are not stored.
     const int kmax = nvalid;
-    for (int k = 0; k < kmax; ++k) {
-      const float4 p4 = pb[wave * 64 + k];
+    const float4 *pw = pb + wave * 64;
 #pragma unroll
-      for (int j = 0; j < 8; ++j) {
-        if (j < nvj) {
-          const int e = lane + 64 * j;
-          if (e < d_v) {
-            float v;
-            if (MLA) v = to_f32(ks_e[k * kstride * EPW + e]);
-            else v = to_f32(vts_e[e * vstride * EPW + k]);
-            acc[0][j] += p4.x * v;
-            acc[1][j] += p4.y * v;
-            acc[2][j] += p4.z * v;
-            acc[3][j] += p4.w * v;
-          }
+    for (int j = 0; j < 8; ++j) {
+      if (j >= nvj) break;
+      const int e = min(lane + 64 * j, d_v - 1);
+      const T *vc = MLA ? ks_e + e : vts_e + e * vstride * EPW;
+      const int kst = MLA ? kstride * EPW : 1;
+      float a0 = acc[0][j], a1 = acc[1][j], a2 = acc[2][j], a3 = acc[3][j];
+      int k = 0;
+      for (; k + 4 <= kmax; k += 4) {
+        float4 pp[4];
+        float vv[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          pp[u] = pw[k + u];
+          vv[u] = to_f32(vc[(k + u) * kst]);
+        }
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          a0 += pp[u].x * vv[u];
+          a1 += pp[u].y * vv[u];
+          a2 += pp[u].z * vv[u];
+          a3 += pp[u].w * vv[u];
         }
       }
+      for (; k < kmax; ++k) {
+        const float4 p4 = pw[k];
+        const float v = to_f32(vc[k * kst]);
+        a0 += p4.x * v;
+        a1 += p4.y * v;
+        a2 += p4.z * v;
+        a3 += p4.w * v;
+      }
+      acc[0][j] = a0;
+      acc[1][j] = a1;
+      acc[2][j] = a2;
+      acc[3][j] = a3;
     }
   }
 
