@@ -7,9 +7,10 @@ attention kernel, and the split-K combine when used. The chunk store is
 filled (compile side, not timed) before the timed region, so every input is
 resident in HBM when timing starts.
 
-Default workload: the Llama-3-8B-shaped prefill link (H_q 32, H_kv 8, d 128,
-8 requests x 10 linked chunks of 512 tokens + 256 query tokens with causal own
-KV, bf16). Prints one JSON line.
+Default workload: the long-RAG link, the largest single-GPU configuration
+(Llama-3-8B head shape H_q 32, H_kv 8, d 128; 16 requests, each linking 8-20
+chunks of 1024 tokens from a 256-chunk store, then 512 query tokens with
+causal own KV; bf16). Prints one JSON line.
 
 Warm-up: the W untimed steps are extended, if needed, to at least
 --min-warmup-s seconds of work. The GPU's core clock ramps up over the first
@@ -183,6 +184,57 @@ def algorithmic(cfg, wl):
     return flops, nbytes
 
 
+def host_cpu_info():
+    """nproc, the affinity mask and the CPU model of the host the oracle ran on."""
+    import re
+    import subprocess
+    aff = sorted(os.sched_getaffinity(0))
+    ranges, start = [], None
+    for i, c in enumerate(aff):
+        if start is None:
+            start = c
+        if i + 1 == len(aff) or aff[i + 1] != c + 1:
+            ranges.append(f"{start}-{c}" if c != start else f"{c}")
+            start = None
+    model = None
+    try:
+        txt = subprocess.run(["lscpu"], capture_output=True, text=True, timeout=10).stdout
+        m = re.search(r"^Model name:\s*(.+)$", txt, re.M)
+        model = m.group(1).strip() if m else None
+    except (OSError, subprocess.SubprocessError):
+        pass
+    if model is None and os.path.exists("/proc/cpuinfo"):
+        m = re.search(r"^model name\s*:\s*(.+)$", open("/proc/cpuinfo").read(), re.M)
+        model = m.group(1).strip() if m else None
+    return {"nproc": os.cpu_count(), "affinity": ",".join(ranges), "affinity_cpus": len(aff),
+            "model": model}
+
+
+def single_core_tiny():
+    """The oracle on the whole tiny fp32 workload with one OpenMP thread (ms)."""
+    import ctypes
+    import oracle
+    from paper_2602_01519_amd import workloads as W
+    cfg = W.CONFIGS["tiny_f32"]
+    wl = W.make_workload(cfg)
+    chunks = {int(c): W.make_chunk(cfg, int(c)) for c in wl.used_chunks()}
+    oracle.num_threads()                      # loads the oracle (and its OpenMP runtime)
+    gomp = ctypes.CDLL("libgomp.so.1")
+    prev = gomp.omp_get_max_threads()
+    gomp.omp_set_num_threads(1)
+    try:
+        best = None
+        for _ in range(3):
+            t0 = time.perf_counter()
+            oracle.run_workload(wl, chunks)
+            dt = (time.perf_counter() - t0) * 1e3
+            best = dt if best is None else min(best, dt)
+    finally:
+        gomp.omp_set_num_threads(prev)
+    flops = W.visible_pairs(cfg, wl.plan) * cfg.n_q_heads * (2 * cfg.d_k + 2 * cfg.d_v)
+    return {"ms": round(best, 3), "cores": 1, "tflops": flops / (best * 1e-3) / 1e12}
+
+
 def cpu_baseline(cfg, wl, dw, budget_s: float):
     """Times the fp64 oracle on a bounded sample of whole requests (host cores),
     and checks the GPU output of the sampled requests against it."""
@@ -225,6 +277,8 @@ def cpu_baseline(cfg, wl, dw, budget_s: float):
         "value": flops_done / t_used / 1e12,
         "unit": "TFLOP/s",
         "cores": oracle.num_threads(),
+        "host": host_cpu_info(),
+        "single_core_tiny_f32": single_core_tiny(),
         "kind": "oracle",
         "sample": f"requests {done} of {p.batch} (all query rows and heads), fp64, {t_used:.1f} s",
         "gpu_max_abs_err_on_sample": max_err,
@@ -240,8 +294,9 @@ def main(argv=None):
                     help="skip the achievable-peak microbenchmarks (second roofline denominator)")
     ap.add_argument("--min-warmup-s", type=float, default=0.5,
                     help="run untimed warm-up steps for at least this long (clock ramp-up)")
-    ap.add_argument("--config", default="llama_prefill",
-                    help="workload: tiny_f32, llama_prefill, long_rag, decode, mla")
+    ap.add_argument("--config", default="long_rag",
+                    help="workload: long_rag (default), tiny_f32, llama_prefill, decode, mla, "
+                         "skinny_rag")
     ap.add_argument("--cpu-budget", type=float, default=15.0,
                     help="seconds of oracle time for the CPU baseline (0 = skip)")
     ap.add_argument("--copy-mib", type=int, default=0,
@@ -302,6 +357,22 @@ def main(argv=None):
     step_ms = ev0.elapsed_time(ev1) / args.steps
     kern_avg_ms = kern_ms / max(launches, 1)
 
+    # Spread of single steps: a second pass of K steps (after the timed
+    # region) with an event at every step boundary; each step's time then
+    # also holds one event record.
+    evs = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
+    evs[0].record(stream)
+    for i in range(args.steps):
+        dw.run()
+        evs[i + 1].record(stream)
+    torch.cuda.synchronize()
+    per_step = np.array([evs[i].elapsed_time(evs[i + 1]) for i in range(args.steps)])
+    step_dist = {"p10": round(float(np.percentile(per_step, 10)), 5),
+                 "median": round(float(np.median(per_step)), 5),
+                 "p90": round(float(np.percentile(per_step, 90)), 5),
+                 "steps": args.steps,
+                 "how": "second pass of K steps, one event per step boundary"}
+
     flops, nbytes = algorithmic(cfg, wl)
     tflops = flops / (step_ms * 1e-3) / 1e12
     gbs = nbytes / (step_ms * 1e-3) / 1e9
@@ -343,6 +414,7 @@ def main(argv=None):
         "warmup": args.warmup,
         "warmup_steps_run": warm_run,
         "ms_per_step": round(step_ms, 5),
+        "step_ms_dist": step_dist,
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,

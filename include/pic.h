@@ -37,6 +37,13 @@
  *     (fp32, or bf16 as raw 16-bit patterns) unless stated; lse is fp32.
  *   - One host thread uses a store at a time. Outputs of calls that are in
  *     flight on different streams must not alias.
+ *   - Each pic_link_attn / pic_link_decode call gets a device workspace of
+ *     its own (the request's own KV laid out for the kernels, and partial
+ *     results of split key ranges): a store keeps eight, handed out in turn,
+ *     and one is reused only once the call that last used it has completed,
+ *     so calls may be in flight on different streams at once; a ninth call
+ *     waits on the host for the oldest of the eight. Runs of one link plan
+ *     share the plan's workspace instead (see pic_link_plan_run).
  */
 #ifndef PIC_H
 #define PIC_H

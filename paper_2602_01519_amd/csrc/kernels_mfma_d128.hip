@@ -50,22 +50,13 @@ typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef __attribute__((address_space(3))) void *lds_ptr;
 
 constexpr int kD = 128;
-#ifndef PIC_D128_WAVES
-#define PIC_D128_WAVES 8
-#endif
-constexpr int kWaves = PIC_D128_WAVES;          // waves (32 rows each) per workgroup
+constexpr int kWaves = 8;                       // waves (32 rows each) per workgroup
 constexpr int kCopySets = 16 / kWaves;          // 64-chunk copies per lane per K (or V) tile
 constexpr int kRowsPerWave = 32;
 constexpr int kRows = kWaves * kRowsPerWave;
 constexpr float kLazy = 8.0f;
-#ifndef PIC_QK_AHEAD
-#define PIC_QK_AHEAD 5
-#endif
-#ifndef PIC_PV_AHEAD
-#define PIC_PV_AHEAD 8
-#endif
-constexpr int kQkAhead = PIC_QK_AHEAD;   // K-fragment read lead, in QK steps
-constexpr int kPvAhead = PIC_PV_AHEAD;   // V-fragment read lead, in PV MFMAs
+constexpr int kQkAhead = 5;    // K-fragment read lead, in QK steps
+constexpr int kPvAhead = 8;    // V-fragment read lead, in PV MFMAs
 
 // LDS tiles, 16-byte chunks XOR-swizzled within each row. The swizzles keep
 // every fragment read conflict-free whether a 16-byte-per-lane read is served
@@ -344,12 +335,12 @@ __global__ __launch_bounds__(kWaves * 64, 8 / kWaves) void link_mfma_d128_kernel
   c.n = c.lane & 31;
   c.g = c.lane >> 5;
 
-  // XCD-aware work mapping: consecutive blocks go round-robin to the 8 XCDs;
+  // XCD-aware work mapping: consecutive blocks go round-robin to the XCDs;
   // all row blocks of one (request, kv head) land on the same XCD (same L2)
   // and are dispatched back to back. Heaviest requests first.
   const int lin = blockIdx.x;
-  const int xcd = lin & 7, j = lin >> 3;
-  const int grp = xcd + 8 * (j / p.nrb);
+  const int xcd = lin % p.n_xcd, j = lin / p.n_xcd;
+  const int grp = xcd + p.n_xcd * (j / p.nrb);
   const int rb = j % p.nrb;
   const int split = blockIdx.y;
   if (grp >= p.batch * p.n_kv_heads) return;

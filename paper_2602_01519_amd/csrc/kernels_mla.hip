@@ -188,10 +188,11 @@ __global__ __launch_bounds__(256, 1) void link_mla_kernel(LinkParams p) {
   const int n = lane & 31, g = lane >> 5;
   const int rb_s = wave >> 1, kb_s = wave & 1;      // this wave's score tile
 
-  // Blocks are dealt to the 8 XCDs round-robin; give each XCD a contiguous
+  // Blocks are dealt to the XCDs round-robin; give each XCD a contiguous
   // run of row blocks so the row blocks of one request share an L2.
   int b = blockIdx.x;
-  if ((gridDim.x & 7) == 0) b = (b & 7) * (gridDim.x >> 3) + (b >> 3);
+  if (gridDim.x % p.n_xcd == 0)
+    b = (b % p.n_xcd) * (gridDim.x / p.n_xcd) + b / p.n_xcd;
   const int nrb = p.nrb;
   const int grp = b / nrb, rblk = b % nrb;
   const int split = blockIdx.y;

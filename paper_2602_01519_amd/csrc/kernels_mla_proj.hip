@@ -37,11 +37,12 @@ struct ProjArgs {
   int64_t a_tok, a_head, c_tok, c_head;
   int32_t n_tokens, n_heads;
   int32_t parts;          // workgroups per head
+  int32_t n_xcd;          // XCDs of the device
 };
 
 // kRope: also copy a[.., 128:192] to c[.., 512:576] (the absorb projection).
 // Workgroup (head h, part j) of `parts` per head walks token blocks j,
-// j + parts, ... Consecutive workgroup ids go round-robin to the 8 XCDs;
+// j + parts, ... Consecutive workgroup ids go round-robin to the XCDs;
 // when the head count allows, all parts of a head go to one XCD, so that
 // its weights are fetched into one L2 only.
 template <int K, int N, bool kRope>
@@ -59,9 +60,9 @@ __global__ __launch_bounds__(256, 1) void proj_kernel(ProjArgs p) {
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int parts = p.parts;
   int h, part;
-  if (p.n_heads % 8 == 0) {
-    const int xcd = blockIdx.x & 7, j = blockIdx.x >> 3;
-    h = xcd + 8 * (j / parts);
+  if (p.n_heads % p.n_xcd == 0) {
+    const int xcd = blockIdx.x % p.n_xcd, j = blockIdx.x / p.n_xcd;
+    h = xcd + p.n_xcd * (j / parts);
     part = j % parts;
   } else {
     h = blockIdx.x / parts;
@@ -178,27 +179,27 @@ __global__ __launch_bounds__(256, 1) void proj_kernel(ProjArgs p) {
 
 // Workgroups per head: about one per CU over all heads, never more than
 // the head's token blocks.
-int proj_parts(int32_t n_tokens, int32_t n_heads) {
+int proj_parts(int32_t n_tokens, int32_t n_heads, int32_t cus) {
   const int blocks = (n_tokens + 31) / 32;
-  return std::max(1, std::min(blocks, (256 + n_heads - 1) / n_heads));
+  return std::max(1, std::min(blocks, (cus + n_heads - 1) / n_heads));
 }
 
 }  // namespace
 
 hipError_t launch_mla_absorb_q(const void *q, const void *w_uk_t, void *q_out, int32_t n_tokens,
-                               int32_t n_heads, hipStream_t st) {
+                               int32_t n_heads, const DevShape &ds, hipStream_t st) {
   ProjArgs p{(const uint16_t *)q, (const uint16_t *)w_uk_t, (uint16_t *)q_out,
              (int64_t)n_heads * 192, 192, (int64_t)n_heads * 576, 576, n_tokens, n_heads,
-             proj_parts(n_tokens, n_heads)};
+             proj_parts(n_tokens, n_heads, ds.cus), ds.xcds};
   hipLaunchKernelGGL((proj_kernel<128, 512, true>), dim3(p.parts * n_heads), dim3(256), 0, st, p);
   return hipGetLastError();
 }
 
 hipError_t launch_mla_up_v(const void *o_lat, const void *w_uv, void *out, int32_t n_tokens,
-                           int32_t n_heads, hipStream_t st) {
+                           int32_t n_heads, const DevShape &ds, hipStream_t st) {
   ProjArgs p{(const uint16_t *)o_lat, (const uint16_t *)w_uv, (uint16_t *)out,
              (int64_t)n_heads * 512, 512, (int64_t)n_heads * 128, 128, n_tokens, n_heads,
-             proj_parts(n_tokens, n_heads)};
+             proj_parts(n_tokens, n_heads, ds.cus), ds.xcds};
   hipLaunchKernelGGL((proj_kernel<512, 128, false>), dim3(p.parts * n_heads), dim3(256), 0, st, p);
   return hipGetLastError();
 }

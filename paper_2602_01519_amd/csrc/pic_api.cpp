@@ -92,11 +92,15 @@ struct Slot {
 // call's chunk/request tables into one slot, copies them to the device on
 // the call's stream, and records the event after the call's last kernel; a
 // slot is reused only after its event has completed.
+// A call's workspace (own-KV slots, split partials) belongs to its slot
+// too, so calls in flight on different streams never share one.
 struct Stage {
   void *host = nullptr;
   void *host_dev = nullptr;     // device-visible address of host
   void *dev = nullptr;
   size_t cap = 0;
+  void *work = nullptr;
+  size_t work_cap = 0;
   hipEvent_t done = nullptr;
   bool pending = false;
 };
@@ -117,6 +121,30 @@ ProfState g_prof;
 inline int64_t round_up(int64_t x, int64_t m) { return (x + m - 1) / m * m; }
 
 }  // namespace
+
+namespace pic {
+// Queried once per device: compute units, and XCDs (one when the runtime
+// does not report them, e.g. a partition that exposes a single die).
+DevShape device_shape() {
+  static std::mutex mu;
+  static std::unordered_map<int, DevShape> cache;
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return DevShape{256, 8};
+  std::lock_guard<std::mutex> g(mu);
+  auto it = cache.find(dev);
+  if (it != cache.end()) return it->second;
+  int cus = 0, xcds = 0;
+  if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+      cus <= 0)
+    cus = 256;
+  if (hipDeviceGetAttribute(&xcds, hipDeviceAttributeNumberOfXccs, dev) != hipSuccess || xcds <= 0)
+    xcds = 1;
+  (void)hipGetLastError();
+  const DevShape ds{cus, xcds};
+  cache.emplace(dev, ds);
+  return ds;
+}
+}  // namespace pic
 
 struct pic_store {
   pic_store_desc desc{};
@@ -139,8 +167,7 @@ struct pic_store {
   std::unordered_map<uint64_t, Slot> map;
   Stage ring[kRing];
   int next = 0;
-  void *work = nullptr;          // split partials
-  size_t work_cap = 0;
+  DevShape shape{256, 8};        // compute units and XCDs of the store's device
 };
 
 namespace {
@@ -173,17 +200,18 @@ pic_status stage_acquire(pic_store *s, size_t bytes, Stage **out) {
   return PIC_OK;
 }
 
-pic_status ensure_work(pic_store *s, size_t bytes) {
-  if (s->work_cap >= bytes) return PIC_OK;
-  if (s->work) {
-    HIP_TRY(hipDeviceSynchronize(), "hipDeviceSynchronize(workspace)");
-    (void)hipFree(s->work);
-    s->work = nullptr;
-    s->work_cap = 0;
+// Grows the workspace of an acquired staging slot (whose previous call has
+// completed, so the old buffer is free).
+pic_status ensure_work(Stage *st, size_t bytes) {
+  if (st->work_cap >= bytes) return PIC_OK;
+  if (st->work) {
+    (void)hipFree(st->work);
+    st->work = nullptr;
+    st->work_cap = 0;
   }
   size_t cap = round_up((int64_t)bytes, 1 << 20);
-  HIP_TRY(hipMalloc(&s->work, cap), "hipMalloc(workspace)");
-  s->work_cap = cap;
+  HIP_TRY(hipMalloc(&st->work, cap), "hipMalloc(workspace)");
+  st->work_cap = cap;
   return PIC_OK;
 }
 
@@ -493,6 +521,17 @@ pic_status plan_call(pic_store *s, const pic_link_req *req, int32_t n_q_heads, f
   return PIC_OK;
 }
 
+// Points the own-KV links of `links` (the plan's tables) at their slots in
+// the workspace `work`.
+void place_own(const pic_store *s, const Plan &P, void *work, LinkEntry *links) {
+  const bool mla = s->desc.kind == PIC_MLA;
+  for (auto &o : P.own) {
+    LinkEntry &E = links[o.first];
+    E.k = (char *)work + o.second;
+    E.v = mla ? E.k : (const char *)E.k + (int64_t)E.lp * s->k_tok_elems * s->esz;
+  }
+}
+
 // Writes the plan's tables into a staging slot (host-mapped pinned memory)
 // and points lp's tables at the slot's device copy; the call's prologue
 // kernel moves them there.
@@ -509,7 +548,9 @@ struct Prologue {
   int64_t copy_bytes = 0;
 };
 
-pic_status upload(pic_store *s, const Plan &P, hipStream_t st, Stage **stage, LinkParams &lp,
+// The slot also holds the call's workspace (work_bytes), where the own-KV
+// links are pointed.
+pic_status upload(pic_store *s, Plan &P, size_t work_bytes, Stage **stage, LinkParams &lp,
                   TableLayout &tl) {
   const size_t nl = P.links.size(), nr = P.reqs.size();
   tl.off_r = round_up(sizeof(LinkEntry) * nl, 256);
@@ -519,12 +560,16 @@ pic_status upload(pic_store *s, const Plan &P, hipStream_t st, Stage **stage, Li
   const size_t off_r = tl.off_r, off_o = tl.off_o, bytes = tl.bytes;
   pic_status rc = stage_acquire(s, bytes, stage);
   if (rc != PIC_OK) return rc;
+  if (work_bytes > 0) {
+    rc = ensure_work(*stage, work_bytes);
+    if (rc != PIC_OK) return rc;
+  }
+  place_own(s, P, (*stage)->work, P.links.data());
   char *h = (char *)(*stage)->host;
   if (nl) memcpy(h, P.links.data(), sizeof(LinkEntry) * nl);
   memcpy(h + off_r, P.reqs.data(), sizeof(ReqEntry) * nr);
   memcpy(h + off_o, P.order.data(), sizeof(int32_t) * nr);
   if (!P.doc_lim.empty()) memcpy(h + tl.off_d, P.doc_lim.data(), sizeof(int32_t) * P.doc_lim.size());
-  (void)st;
   char *dv = (char *)(*stage)->dev;
   lp.links = (const LinkEntry *)dv;
   lp.reqs = (const ReqEntry *)(dv + off_r);
@@ -631,7 +676,8 @@ pic_status setup_call(pic_store *s, const pic_link_req *req, int32_t n_q_heads, 
   lp.nrb = std::max(1, (P.max_rows + rows_per_block - 1) / rows_per_block);
   lp.max_rows = P.max_rows;
   lp.n_groups = req->batch * d.n_kv_heads;
-  if (kern == Kern::Mfma128) lp.n_groups = (int32_t)round_up(lp.n_groups, 8);
+  lp.n_xcd = s->shape.xcds;
+  if (kern == Kern::Mfma128) lp.n_groups = (int32_t)round_up(lp.n_groups, lp.n_xcd);
 
   int32_t splits = 1;
   const int64_t blocks = (int64_t)req->batch * d.n_kv_heads * lp.nrb;
@@ -639,9 +685,10 @@ pic_status setup_call(pic_store *s, const pic_link_req *req, int32_t n_q_heads, 
     if (num_splits > 0) {
       splits = num_splits;
     } else {
-      // about 2048 work items (one wave each for the decode kernel, a
+      // about 8 work items per CU (one wave each for the decode kernel, a
       // workgroup each otherwise), never more splits than tiles
-      splits = (int32_t)std::max<int64_t>(1, std::min<int64_t>((2048 + blocks - 1) / blocks, 256));
+      const int64_t items = 8 * (int64_t)s->shape.cus;
+      splits = (int32_t)std::max<int64_t>(1, std::min<int64_t>((items + blocks - 1) / blocks, 256));
       splits = std::min(splits, std::max(1, P.max_tiles));
     }
   } else {
@@ -650,14 +697,14 @@ pic_status setup_call(pic_store *s, const pic_link_req *req, int32_t n_q_heads, 
     // of cached ones), or a single small request -- leave most CUs idle and
     // let the longest request set the kernel time. Split every request's
     // key range so that its longest piece is no longer than the average work
-    // per resident workgroup of the GPU (256 CUs times the kernel's
+    // per resident workgroup of the GPU (its CUs times the kernel's
     // workgroups per CU), with a minimum piece (8 tiles for the matrix-core
     // kernels, 1 for the vector-ALU kernel, whose tiles are slow) and at
     // most 16 pieces.
     const int64_t per_cu =
         kern == Kern::Mla ? 1 : kern == Kern::Mfma128 ? mfma_d128_blocks_per_cu() : 4;
     const int min_piece = kern == Kern::Valu ? 1 : 8;
-    const int64_t slots = 256 * per_cu;
+    const int64_t slots = (int64_t)s->shape.cus * per_cu;
     int64_t work = 0;   // tiles summed over all non-empty workgroups
     for (const ReqEntry &R : P.reqs) {
       const int64_t rows = (int64_t)R.lq * lp.group;
@@ -673,17 +720,6 @@ pic_status setup_call(pic_store *s, const pic_link_req *req, int32_t n_q_heads, 
   C.part_off = round_up(P.own_bytes, 256);
   C.part_bytes = splits > 1 ? rows * splits * (d.d_v + 2) * sizeof(float) : 0;
   return PIC_OK;
-}
-
-// Points the own-KV links of `links` (the plan's tables) at their slots in
-// the workspace `work`.
-void place_own(const pic_store *s, const Plan &P, void *work, LinkEntry *links) {
-  const bool mla = s->desc.kind == PIC_MLA;
-  for (auto &o : P.own) {
-    LinkEntry &E = links[o.first];
-    E.k = (char *)work + o.second;
-    E.v = mla ? E.k : (const char *)E.k + (int64_t)E.lp * s->k_tok_elems * s->esz;
-  }
 }
 
 // Enqueues a call whose tables are already on the device (lp.links, reqs,
@@ -747,15 +783,10 @@ pic_status link_call(pic_store *s, const pic_link_req *req, int32_t n_q_heads, c
   // the workspace is allocated on the store's device
   DeviceGuard dg(s->device);
   if (!dg.ok) return fail(PIC_ERR_HIP, "cannot select the store's device");
-  if (C.work_bytes() > 0) {
-    rc = ensure_work(s, C.work_bytes());
-    if (rc != PIC_OK) return rc;
-  }
-  place_own(s, C.P, s->work, C.P.links.data());
   Stage *stage = nullptr;
   TableLayout tl;
   LinkParams lp = C.lp;
-  rc = upload(s, C.P, st, &stage, lp, tl);
+  rc = upload(s, C.P, C.work_bytes(), &stage, lp, tl);
   if (rc != PIC_OK) return rc;
   Prologue pro;
   const char *hd = (const char *)stage->host_dev;
@@ -764,7 +795,7 @@ pic_status link_call(pic_store *s, const pic_link_req *req, int32_t n_q_heads, c
   pro.copy_src = hd;
   pro.copy_dst = stage->dev;
   pro.copy_bytes = (int64_t)tl.bytes;
-  rc = launch_call(s, C, lp, s->work, pro, q, k_self, v_self, scale, out, lse, st);
+  rc = launch_call(s, C, lp, stage->work, pro, q, k_self, v_self, scale, out, lse, st);
   if (rc != PIC_OK) return rc;
   HIP_TRY(hipEventRecord(stage->done, st), "hipEventRecord(stage)");
   stage->pending = true;
@@ -813,6 +844,7 @@ pic_status pic_store_create(const pic_store_desc *desc, pic_store **out) {
   s->layer_bytes = s->capacity * (s->k_tok_elems + s->v_tok_elems) * s->esz;
   s->free_runs.emplace(0, s->capacity / kTile);
   hipError_t e = hipGetDevice(&s->device);
+  if (e == hipSuccess) s->shape = device_shape();
   if (e == hipSuccess) e = hipMalloc((void **)&s->pool, (size_t)s->layer_bytes * s->n_layers);
   if (e != hipSuccess) {
     delete s;
@@ -839,10 +871,10 @@ pic_status pic_store_destroy(pic_store *s) {
   for (Stage &st : s->ring) {
     if (st.host) (void)hipHostFree(st.host);
     if (st.dev) (void)hipFree(st.dev);
+    if (st.work) (void)hipFree(st.work);
     if (st.done) (void)hipEventDestroy(st.done);
   }
   for (auto &pr : s->pending) (void)hipEventDestroy(pr.first);
-  if (s->work) (void)hipFree(s->work);
   if (s->pool) (void)hipFree(s->pool);
   delete s;
   return PIC_OK;
@@ -1319,7 +1351,8 @@ pic_status pic_mla_absorb_q(int32_t n_tokens, int32_t n_heads, const void *q, co
                             void *q_out, void *stream) {
   pic_status rc = check_proj(n_tokens, n_heads, {q, w_uk_t, q_out});
   if (rc != PIC_OK || n_tokens == 0) return rc;
-  hipError_t e = launch_mla_absorb_q(q, w_uk_t, q_out, n_tokens, n_heads, (hipStream_t)stream);
+  hipError_t e = launch_mla_absorb_q(q, w_uk_t, q_out, n_tokens, n_heads, device_shape(),
+                                     (hipStream_t)stream);
   if (e != hipSuccess) return hip_fail(e, "proj_kernel (absorb)");
   return PIC_OK;
 }
@@ -1328,7 +1361,8 @@ pic_status pic_mla_up_v(int32_t n_tokens, int32_t n_heads, const void *o_lat, co
                         void *out, void *stream) {
   pic_status rc = check_proj(n_tokens, n_heads, {o_lat, w_uv, out});
   if (rc != PIC_OK || n_tokens == 0) return rc;
-  hipError_t e = launch_mla_up_v(o_lat, w_uv, out, n_tokens, n_heads, (hipStream_t)stream);
+  hipError_t e = launch_mla_up_v(o_lat, w_uv, out, n_tokens, n_heads, device_shape(),
+                                 (hipStream_t)stream);
   if (e != hipSuccess) return hip_fail(e, "proj_kernel (up)");
   return PIC_OK;
 }

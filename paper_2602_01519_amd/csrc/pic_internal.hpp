@@ -68,8 +68,18 @@ struct LinkParams {
   int32_t nrb;            // row blocks per (request, kv head)
   int32_t max_rows;       // most rows of one (request, kv head)
   int32_t n_groups;       // batch * n_kv_heads, padded as the kernel requires
+  int32_t n_xcd;          // accelerator dies (XCDs) of the device, each with its own L2
   float scale_log2;       // softmax_scale * log2(e)
 };
+
+// Shape of the current device: compute units and XCDs. Workgroups with
+// consecutive ids are dispatched round-robin to the XCDs, so a kernel that
+// wants some of them to share an L2 maps ids with the XCD count.
+struct DevShape {
+  int32_t cus;
+  int32_t xcds;
+};
+DevShape device_shape();
 
 // Launchers (each returns the launch status).
 hipError_t launch_put_rows(const void *src, void *dst, int64_t n_tokens, int32_t lp,
@@ -97,14 +107,14 @@ hipError_t launch_write_rows(const RowDst *dst, int32_t n, const void *src_k, co
 // Copies bytes (a multiple of 16) from a host-mapped buffer to the device.
 hipError_t launch_table_copy(const void *src, void *dst, int64_t bytes, hipStream_t st);
 
-// Lays each request's own KV (token-major k_self / v_self) out like a chunk
-// slot at its own link (the request's last link), zero-padded to lp.
+// The dense MLA projections around the latent link (see pic.h).
 hipError_t launch_mla_absorb_q(const void *q, const void *w_uk_t, void *q_out, int32_t n_tokens,
-                               int32_t n_heads, hipStream_t st);
+                               int32_t n_heads, const DevShape &ds, hipStream_t st);
 hipError_t launch_mla_up_v(const void *o_lat, const void *w_uv, void *out, int32_t n_tokens,
-                           int32_t n_heads, hipStream_t st);
-// The call's prologue: lays out the own KV of every request in its slot
-// in `work` (when max_own_lp > 0) and copies copy_bytes of tables from
+                           int32_t n_heads, const DevShape &ds, hipStream_t st);
+// The call's prologue: lays out the own KV of every request (token-major
+// k_self / v_self) like a chunk slot at its own link (the request's last
+// link), zero-padded to lp, in `work` (when max_own_lp > 0) and copies copy_bytes of tables from
 // copy_src to copy_dst (when copy_bytes > 0). The layout takes each
 // request's own rows and slot from `own` (host, batch entries, batch <=
 // kOwnArgs: passed as kernel arguments, so it does not wait for a read of

@@ -1,13 +1,9 @@
 """GPU parity: the HIP path through the C ABI against the fp64 oracle.
 
-Tolerances (from the stated accuracy bar): bf16 inputs max-abs <= 2e-2 and
-mean-abs <= 2e-3 over the compared outputs; fp32 inputs max-abs and mean-abs
-<= 1e-4. The log-sum-exp is compared to 4e-3 (bf16) / 1e-4 (fp32) absolute:
-on the bf16 path the row sum adds the probabilities as rounded to bf16 for
-the PV product (round to nearest, unit roundoff 2^-8), so ln(sum) can be off
-by up to ln(1 + 2^-8) = 3.9e-3 in a row with few visible keys, where the
-roundings do not average out; the fp32 score and exponential errors add
-about 1e-5. The gather hook must be bit-exact.
+The bar (element-wise, relative L2 and log-sum-exp tolerances, with the
+derivation of each) is in parity_gate.py; every comparison here and in the
+other GPU test files goes through compare(). The gather hook must be
+bit-exact.
 """
 import dataclasses
 import math
@@ -17,31 +13,23 @@ import pytest
 import torch
 
 import oracle
+import parity_gate as G
 from paper_2602_01519_amd import pic, runner
 from paper_2602_01519_amd import workloads as W
 
 pytestmark = pytest.mark.gpu
 
-TOL = {W.F32: (1e-4, 1e-4, 1e-4), W.BF16: (2e-2, 2e-3, 4e-3)}
+TOL = {W.F32: G.TOL[G.F32], W.BF16: G.TOL[G.BF16]}
 
 
 def compare(cfg, out, lse, ref, ref_lse, sel=None, label=""):
     if sel is not None:
         rows = sel.reshape(out.shape[0], out.shape[1]).astype(bool)
         out, ref, lse, ref_lse = out[rows], ref[rows], lse[rows], ref_lse[rows]
-    max_tol, mean_tol, lse_tol = TOL[cfg.dtype]
-    assert np.all(np.isfinite(out)), f"{label}: non-finite output"
-    err = np.abs(out - ref)
-    print(f"{label}: max_abs={err.max() if err.size else 0:.3e} mean_abs={err.mean() if err.size else 0:.3e} "
-          f"rel_l2={np.linalg.norm(err) / max(np.linalg.norm(ref), 1e-30):.3e}", flush=True)
-    if err.size:
-        assert err.max() <= max_tol, f"{label}: max abs err {err.max()}"
-        assert err.mean() <= mean_tol, f"{label}: mean abs err {err.mean()}"
-    fin = np.isfinite(ref_lse)
-    assert np.array_equal(fin, np.isfinite(lse)), f"{label}: lse finiteness differs"
-    assert np.all(np.isneginf(lse[~fin]))
-    if fin.any():
-        assert np.abs(lse[fin] - ref_lse[fin]).max() <= lse_tol, f"{label}: lse err"
+    dt = G.F32 if cfg.dtype == W.F32 else G.BF16
+    G.record(label, dt, out, ref)
+    bad = G.failures(dt, out, ref, lse, ref_lse)
+    assert not bad, f"{label}: " + "; ".join(bad)
 
 
 def run_and_check(cfg, decode=None, num_splits=0, requests=None, links=None):
@@ -290,12 +278,13 @@ def test_prefill_and_decode_agree_on_single_token_requests():
     a, la = run_and_check(cfg, decode=False)
     b, lb = run_and_check(cfg, decode=True, num_splits=5)
     assert np.abs(a - b).max() <= 2e-2
-    assert np.abs(la - lb).max() <= 2 * TOL[W.BF16][2]   # each within the lse bound of the oracle
+    assert np.abs(la - lb).max() <= 2 * TOL[W.BF16].lse   # each within the lse bound of the oracle
 
 
 # ---------------------------------------------------------------------------
-# the five benchmark workloads at their full sizes (sampled requests where the
-# oracle would take minutes)
+# the benchmark workloads at their full sizes, in the launch configuration
+# bench.py times: every request, except long_rag, where four requests span
+# the heaviest-first order (the oracle would take minutes for all sixteen)
 
 
 def test_config_tiny_f32():
@@ -303,30 +292,46 @@ def test_config_tiny_f32():
 
 
 def test_config_llama_prefill():
-    run_and_check(W.CONFIGS["llama_prefill"], requests=[0, 5])
+    run_and_check(W.CONFIGS["llama_prefill"])
+
+
+def long_rag_sample(cfg):
+    """The heaviest and the lightest request and two between them, by the
+    work (tiles x query rows) the launch orders its requests by."""
+    p = W.make_plan(cfg)
+    n = np.diff(p.chunk_offsets)
+    order = sorted(range(cfg.batch), key=lambda r: (-int(n[r]), r))
+    picks = [order[0], order[len(order) // 3], order[2 * len(order) // 3], order[-1]]
+    return sorted(set(picks))
 
 
 def test_config_long_rag():
     cfg = W.CONFIGS["long_rag"]
-    p = W.make_plan(cfg)
-    n = np.diff(p.chunk_offsets)
-    run_and_check(cfg, requests=[int(np.argmax(n)), int(np.argmin(n))])
+    run_and_check(cfg, requests=long_rag_sample(cfg))
 
 
 def test_config_decode():
-    run_and_check(W.CONFIGS["decode"], requests=[0, 17, 63])
+    run_and_check(W.CONFIGS["decode"])
 
 
 def test_config_mla():
-    run_and_check(W.CONFIGS["mla"], requests=[3])
+    run_and_check(W.CONFIGS["mla"])
 
 
 def test_config_skinny_rag():
-    cfg = W.CONFIGS["skinny_rag"]
-    p = W.make_plan(cfg)
-    n = np.diff(p.chunk_offsets)
-    # the longest and the shortest link lists, and one request per question length
-    run_and_check(cfg, requests=sorted({int(np.argmax(n)), int(np.argmin(n)), 0, 1, 2}))
+    run_and_check(W.CONFIGS["skinny_rag"])
+
+
+def test_config_llama_prefill_double_scale():
+    """The literal reading of the Llama prefill config's query scale: Q is
+    drawn N(0,1)/sqrt(128) and the call still passes softmax_scale
+    1/sqrt(128) (Eq. 2 and 7 scale by 1/sqrt(d)), so the logits have a
+    standard deviation of ~0.09 and attention is nearly uniform over ~5k
+    keys; outputs are ~1e-2, below the element-wise bar, and the relative
+    L2 bar decides."""
+    cfg = dataclasses.replace(W.CONFIGS["llama_prefill"], name="llama_prefill_double_scale",
+                              scale=1.0 / math.sqrt(128.0))
+    run_and_check(cfg)
 
 
 # Short questions over long documents: the prefill entry splits the key range
@@ -362,7 +367,7 @@ def test_chunk_order_permutation_on_gpu():
         torch.cuda.synchronize()
         b, lb = dw.results()
         assert np.abs(a - b).max() <= 2e-2 and np.abs(a - b).mean() <= 2e-3
-        assert np.abs(la - lb).max() <= 2 * TOL[W.BF16][2]   # each within the lse bound of the oracle
+        assert np.abs(la - lb).max() <= 2 * TOL[W.BF16].lse   # each within the lse bound of the oracle
     finally:
         dw.close()
 
@@ -461,3 +466,66 @@ def test_peak_microbenchmarks():
     with pytest.raises(pic.PicError):
         pic.peak_hbm_read(host, host.nbytes)
 
+
+
+# ---------------------------------------------------------------------------
+# calls in flight on two streams
+
+
+def _random_bf16(rng, shape):
+    return W.f32_to_bf16_bits(rng.standard_normal(shape, dtype=np.float32))
+
+
+@pytest.mark.parametrize("decode", [False, True])
+def test_two_streams_in_flight(decode):
+    """Two different batches on one store, enqueued back to back on two
+    streams several times over: each call lays out its own KV and writes its
+    split partials in a workspace no call in flight shares, so both results
+    match the oracle."""
+    q_len = (1, 1, 1, 1) if decode else (16, 40, 24, 48)
+    cfg = W.small_config("two_streams", d_k=128, n_q_heads=32, n_kv_heads=8,
+                         chunk_lens=(1024, 1024, 700, 1024, 300, 1024, 513, 1024), batch=4,
+                         links=(4, 7), q_len=q_len, self_len=(70, 129, 64, 200), seed=23,
+                         decode=decode)
+    wl = W.make_workload(cfg)
+    dw = runner.upload(wl)
+    rng = np.random.default_rng(99)
+    p = wl.plan
+    # batch B: other links (reversed, one repeated) and other query / own tensors
+    links_b = []
+    for r in range(p.batch):
+        idx = [int(c) for c in p.chunk_index[p.chunk_offsets[r]:p.chunk_offsets[r + 1]]][::-1]
+        links_b.append(idx + idx[:1])
+    co_b = np.zeros(p.batch + 1, np.int32)
+    co_b[1:] = np.cumsum([len(l) for l in links_b])
+    ids_b = wl.chunk_ids[np.array([c for l in links_b for c in l], np.int64)]
+    q_b = W.f32_to_bf16_bits(W.bf16_bits_to_f32(_random_bf16(rng, wl.q.shape)) *
+                             np.float32(1 / math.sqrt(128)))
+    ks_b, vs_b = _random_bf16(rng, wl.k_self.shape), _random_bf16(rng, wl.v_self.shape)
+    dq_b, dks_b, dvs_b = (runner.to_device(a, "cuda") for a in (q_b, ks_b, vs_b))
+    out_b = torch.empty_like(dw.out)
+    lse_b = torch.empty_like(dw.lse)
+    s1, s2 = torch.cuda.Stream(), torch.cuda.Stream()
+    call = pic.link_decode if decode else pic.link_attn
+    kw = dict(num_splits=3) if decode else {}
+    scale = float(np.float32(cfg.scale))
+    try:
+        torch.cuda.synchronize()
+        for _ in range(6):
+            call(dw.store, p.chunk_offsets, wl.link_ids(), p.q_offsets, p.self_offsets,
+                 cfg.n_q_heads, dw.q, dw.k_self, dw.v_self, scale, dw.out, dw.lse,
+                 stream=s1.cuda_stream, **kw)
+            call(dw.store, co_b, ids_b, p.q_offsets, p.self_offsets, cfg.n_q_heads, dq_b, dks_b,
+                 dvs_b, scale, out_b, lse_b, stream=s2.cuda_stream, **kw)
+        torch.cuda.synchronize()
+        out_a, lse_a = dw.results()
+        ref_a, rl_a = oracle.run_workload(wl, dw.chunks)
+        compare(cfg, out_a, lse_a, ref_a, rl_a, label="stream A")
+        ref_b, rl_b = oracle.link_attn(
+            dtype=cfg.dtype, mla=False, n_q_heads=cfg.n_q_heads, d_v=cfg.d_v,
+            links=[[dw.chunks[c] for c in l] for l in links_b], q=q_b, q_offsets=p.q_offsets,
+            k_self=ks_b, v_self=vs_b, self_offsets=p.self_offsets, tau=scale)
+        compare(cfg, runner.to_host(out_b, cfg.dtype), lse_b.cpu().numpy().astype(np.float64),
+                ref_b, rl_b, label="stream B")
+    finally:
+        dw.close()
