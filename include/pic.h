@@ -222,6 +222,29 @@ pic_status pic_link_decode(pic_store *store, const pic_link_req *req, int32_t n_
                            float softmax_scale, int32_t num_splits, void *out, float *lse,
                            void *stream);
 
+/* pic_link_decode for callers that cannot allocate device memory: code
+ * under HIP graph capture, tight serving loops, harnesses that forbid
+ * hipMalloc. Same arguments, kernels, split choice and result as
+ * pic_link_decode, but the call's tables, own-KV layout and split partials
+ * live in the library's static device scratch, a file-scope array of
+ * 64 MiB that each GPU the library runs on holds until the process ends;
+ * the call allocates nothing (no hipMalloc, hipFree, pinned staging or
+ * event). The host tables are copied with hipMemcpyAsync from pageable
+ * memory, which the runtime completes before returning (the host therefore
+ * waits for the stream's earlier work). Every kernel writes what it later
+ * reads, so nothing in the scratch has to start at zero.
+ * All calls on one GPU share its scratch: calls must not overlap on a GPU
+ * (enqueue them on one stream, or order them); calls that overlap race.
+ * Errors: as pic_link_decode, and INVALID when the call needs more than the
+ * 64 MiB (about 256 B of tables per link and request, plus
+ * ceil(L_s / 64) * 64 own tokens * H_kv * (d_k + d_v) * esize per request,
+ * plus Tq * H_q * splits * (d_v + 2) * 4 B when the keys are split); such a
+ * call launches nothing. */
+pic_status pic_link_decode_noalloc(pic_store *store, const pic_link_req *req, int32_t n_q_heads,
+                                   const void *q, const void *k_self, const void *v_self,
+                                   float softmax_scale, int32_t num_splits, void *out, float *lse,
+                                   void *stream);
+
 /* A request batch resolved once for repeated calls. Comb runs the same
  * links in each of its cross-attention layers and again at every decode
  * step (generated tokens attend to the same documents, Sec. 4 and Eq. 12);

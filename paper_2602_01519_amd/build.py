@@ -24,6 +24,7 @@ SOURCES = [
     "kernels_mla.hip",
     "kernels_peaks.hip",
     "kernels_mla_proj.hip",
+    "static_scratch.hip",
 ]
 
 # Per-file code generation flags. The MLA kernel keeps its accumulators in

@@ -724,9 +724,12 @@ pic_status setup_call(pic_store *s, const pic_link_req *req, int32_t n_q_heads, 
 
 // Enqueues a call whose tables are already on the device (lp.links, reqs,
 // order set): own-KV staging, the attention kernel, the split combine.
+// timed: the attention launch may be bracketed by the measurement events
+// (pic_prof_begin); the entry point that allocates nothing passes false.
 pic_status launch_call(const pic_store *s, const Setup &C, LinkParams lp, void *work,
                        const Prologue &pro, const void *q, const void *k_self,
-                       const void *v_self, float scale, void *out, float *lse, hipStream_t st) {
+                       const void *v_self, float scale, void *out, float *lse, hipStream_t st,
+                       bool timed = true) {
   const pic_store_desc &d = s->desc;
   const bool mla = d.kind == PIC_MLA;
   lp.q = q;
@@ -747,9 +750,9 @@ pic_status launch_call(const pic_store *s, const Setup &C, LinkParams lp, void *
                                    pro.copy_src, pro.copy_dst, pro.copy_bytes, st);
     if (e != hipSuccess) return hip_fail(e, "prep_own_kernel");
   }
-  std::pair<hipEvent_t, hipEvent_t> ev;
+  std::pair<hipEvent_t, hipEvent_t> ev{nullptr, nullptr};
   const char *name = "";
-  prof_start(st, &ev);
+  if (timed) prof_start(st, &ev);
   hipError_t e;
   if (C.kern == Kern::Decode128)
     e = launch_link_decode_d128(lp, st, &name);
@@ -1162,6 +1165,60 @@ pic_status pic_link_decode(pic_store *s, const pic_link_req *req, int32_t n_q_he
                            void *stream) {
   return link_call(s, req, n_q_heads, q, k_self, v_self, softmax_scale, num_splits, out, lse,
                    stream, Mode::Decode);
+}
+
+pic_status pic_link_decode_noalloc(pic_store *s, const pic_link_req *req, int32_t n_q_heads,
+                                   const void *q, const void *k_self, const void *v_self,
+                                   float softmax_scale, int32_t num_splits, void *out, float *lse,
+                                   void *stream) {
+  if (!req) return fail(PIC_ERR_INVALID, "req is NULL");
+  Setup C;
+  pic_status rc = setup_call(s, req, n_q_heads, softmax_scale, req->layer, num_splits,
+                             Mode::Decode, C);
+  if (rc != PIC_OK) return rc;
+  if (req->batch == 0) return PIC_OK;
+  rc = check_tensors(s, C.P, q, k_self, v_self, out);
+  if (rc != PIC_OK) return rc;
+  if (C.P.total_q == 0) return PIC_OK;
+  // scratch layout: [link table][request table][order][per-query limits][workspace]
+  Plan &P = C.P;
+  const size_t nl = P.links.size(), nr = P.reqs.size();
+  const size_t off_r = round_up(sizeof(LinkEntry) * nl, 256);
+  const size_t off_o = off_r + round_up(sizeof(ReqEntry) * nr, 256);
+  const size_t off_d = off_o + round_up(sizeof(int32_t) * nr, 256);
+  const size_t tables = off_d + round_up(sizeof(int32_t) * P.doc_lim.size(), 256);
+  const size_t need = tables + C.work_bytes();
+  if (need > kStaticScratchBytes)
+    return fail(PIC_ERR_INVALID,
+                "the call needs %zu bytes of scratch (tables, own KV, split partials); the static "
+                "scratch holds %zu", need, kStaticScratchBytes);
+  DeviceGuard dg(s->device);
+  if (!dg.ok) return fail(PIC_ERR_HIP, "cannot select the store's device");
+  void *base = nullptr;
+  HIP_TRY(static_scratch(&base), "hipGetSymbolAddress(scratch)");
+  char *dev = (char *)base;
+  place_own(s, P, dev + tables, P.links.data());
+  std::vector<char> host(tables, 0);
+  if (nl) memcpy(host.data(), P.links.data(), sizeof(LinkEntry) * nl);
+  memcpy(host.data() + off_r, P.reqs.data(), sizeof(ReqEntry) * nr);
+  memcpy(host.data() + off_o, P.order.data(), sizeof(int32_t) * nr);
+  if (!P.doc_lim.empty())
+    memcpy(host.data() + off_d, P.doc_lim.data(), sizeof(int32_t) * P.doc_lim.size());
+  const hipStream_t st = (hipStream_t)stream;
+  // pageable source: the runtime copies it before returning (no staging
+  // buffer of ours, no allocation)
+  HIP_TRY(hipMemcpyAsync(dev, host.data(), tables, hipMemcpyHostToDevice, st),
+          "hipMemcpyAsync(tables to scratch)");
+  LinkParams lp = C.lp;
+  lp.links = (const LinkEntry *)dev;
+  lp.reqs = (const ReqEntry *)(dev + off_r);
+  lp.order = (const int32_t *)(dev + off_o);
+  lp.doc_lim = P.doc_lim.empty() ? nullptr : (const int32_t *)(dev + off_d);
+  Prologue pro;
+  pro.links = lp.links;
+  pro.reqs = lp.reqs;
+  return launch_call(s, C, lp, dev + tables, pro, q, k_self, v_self, softmax_scale, out, lse, st,
+                     false);
 }
 
 pic_status pic_link_plan_create(pic_store *s, const pic_link_req *req, int32_t n_q_heads,

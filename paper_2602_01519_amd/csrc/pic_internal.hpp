@@ -156,6 +156,13 @@ double peak_mfma_flops(int32_t iters);
 hipError_t launch_peak_mfma(float *out, int32_t iters, hipStream_t st);
 hipError_t launch_peak_read(const void *src, int64_t bytes, float *out, hipStream_t st);
 
+// The library's static device scratch (a file-scope array, no allocation):
+// its size, and its address on the current device (resolved once per
+// device). Used by the entry points that must not allocate.
+constexpr size_t kStaticScratchBytes = size_t(64) << 20;
+constexpr int kMaxDevices = 64;
+hipError_t static_scratch(void **out);
+
 // Log-sum-exp merge of split partials into out / lse.
 hipError_t launch_combine(const LinkParams &p, int dtype, hipStream_t st);
 

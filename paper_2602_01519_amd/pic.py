@@ -78,6 +78,7 @@ def lib():
             "pic_store_usage": [vp, vp, vp, vp],
             "pic_link_attn": [vp, vp, i32, vp, vp, vp, f32, vp, vp, vp],
             "pic_link_decode": [vp, vp, i32, vp, vp, vp, f32, i32, vp, vp, vp],
+            "pic_link_decode_noalloc": [vp, vp, i32, vp, vp, vp, f32, i32, vp, vp, vp],
             "pic_debug_gather": [vp, vp, i32, i32, vp, vp, vp],
             "pic_link_plan_create": [vp, vp, i32, i32, i32, vp],
             "pic_link_plan_run": [vp, i32, vp, vp, vp, f32, vp, vp, vp],
@@ -225,6 +226,19 @@ def link_decode(store: Store, chunk_offsets, chunk_ids, q_offsets, self_offsets,
     _check(lib().pic_link_decode(store.handle, ctypes.byref(req), int(n_q_heads), _ptr(q), _ptr(k_self),
                                  _ptr(v_self), float(softmax_scale), int(num_splits), _ptr(out),
                                  _ptr(lse), stream))
+
+
+def link_decode_noalloc(store: Store, chunk_offsets, chunk_ids, q_offsets, self_offsets,
+                        n_q_heads: int, q, k_self, v_self, softmax_scale: float, out, lse=None,
+                        num_splits: int = 0, stream: Optional[int] = None, layer: int = 0,
+                        chunk_starts=None, q_doc_limits=None):
+    """pic_link_decode_noalloc: pic_link_decode in the library's static scratch."""
+    keep: list = []
+    req = _req(chunk_offsets, chunk_ids, q_offsets, self_offsets, keep, layer, chunk_starts,
+               q_doc_limits)
+    _check(lib().pic_link_decode_noalloc(store.handle, ctypes.byref(req), int(n_q_heads), _ptr(q),
+                                         _ptr(k_self), _ptr(v_self), float(softmax_scale),
+                                         int(num_splits), _ptr(out), _ptr(lse), stream))
 
 
 def debug_gather(store: Store, ids, k_out, v_out, stream: Optional[int] = None, layer: int = 0):
