@@ -48,6 +48,7 @@
 #ifndef PIC_H
 #define PIC_H
 
+#include <stddef.h>
 #include <stdint.h>
 
 #ifdef __cplusplus
@@ -148,6 +149,33 @@ pic_status pic_store_derive(pic_store *store, uint64_t new_id, uint64_t base_id,
 pic_status pic_store_write_rows(pic_store *store, uint64_t chunk_id, int32_t layer,
                                 int32_t n_rows, const int32_t *rows, const void *k,
                                 const void *v, void *stream);
+
+/* Handing a store to another process on the same GPU, in place: the PIC
+ * manager of the paper sends the handles of the PICaches it collected to the
+ * inference engine over the GPU's inter-process memory API, so tensors pass
+ * between processes without copies (Sec. 5.3, System Details).
+ * pic_store_export: waits for the device (every put and copy enqueued so far
+ *   has landed), then writes a self-contained description of the store --
+ *   its shape, an inter-process handle of its pool and its chunk index as it
+ *   stands -- into buf (host, buf_bytes). *bytes_out receives the size
+ *   needed; buf = NULL only asks for it. Chunks put or removed later are not
+ *   in the description: the exporting process keeps the store and the
+ *   exported chunks alive (no pic_store_remove, no pic_store_destroy) while
+ *   importers use them. Errors: INVALID (NULL store or bytes_out, buffer too
+ *   small, an imported store), UNSUPPORTED (pool of 2 GiB or more: the
+ *   pool's n_layers * capacity_tokens * H_kv * (d_k + d_v) * esize must stay
+ *   below 2^31 bytes), HIP.
+ * pic_store_import: in another process on the same GPU (with that device
+ *   current), maps the exported pool and rebuilds the chunk index. The result
+ *   is a read-only store: link calls, link plans, pic_store_lookup,
+ *   pic_store_usage and pic_debug_gather work as on the original;
+ *   pic_store_put, pic_store_remove, pic_store_derive and
+ *   pic_store_write_rows return INVALID. pic_store_destroy unmaps the pool
+ *   (the exporter still owns it). Mapping a pool in the process that
+ *   exported it is not supported. Errors: INVALID (not a description made by
+ *   pic_store_export, or a corrupt one), HIP (the mapping failed), OOM. */
+pic_status pic_store_export(pic_store *store, void *buf, size_t buf_bytes, size_t *bytes_out);
+pic_status pic_store_import(const void *buf, size_t buf_bytes, pic_store **out);
 
 /* Hash-table lookup (Sec. 3 step 1): *n_tokens_out = the chunk's length.
  * Errors: INVALID, NOT_FOUND. */

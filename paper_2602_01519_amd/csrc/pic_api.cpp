@@ -168,6 +168,7 @@ struct pic_store {
   Stage ring[kRing];
   int next = 0;
   DevShape shape{256, 8};        // compute units and XCDs of the store's device
+  bool imported = false;         // pool mapped from another process (read-only)
 };
 
 namespace {
@@ -878,7 +879,12 @@ pic_status pic_store_destroy(pic_store *s) {
     if (st.done) (void)hipEventDestroy(st.done);
   }
   for (auto &pr : s->pending) (void)hipEventDestroy(pr.first);
-  if (s->pool) (void)hipFree(s->pool);
+  if (s->pool) {
+    if (s->imported)
+      (void)hipIpcCloseMemHandle(s->pool);
+    else
+      (void)hipFree(s->pool);
+  }
   delete s;
   return PIC_OK;
 }
@@ -886,6 +892,7 @@ pic_status pic_store_destroy(pic_store *s) {
 pic_status pic_store_put(pic_store *s, uint64_t chunk_id, int64_t n_tokens, const void *k,
                          const void *v, void *stream) {
   if (!s) return fail(PIC_ERR_INVALID, "store is NULL");
+  if (s->imported) return fail(PIC_ERR_INVALID, "the store was imported from another process and is read-only");
   if (n_tokens <= 0 || n_tokens > INT32_MAX / 4) return fail(PIC_ERR_INVALID, "n_tokens out of range");
   if (!k) return fail(PIC_ERR_INVALID, "k is NULL");
   const bool gqa = s->desc.kind == PIC_GQA;
@@ -951,6 +958,7 @@ pic_status pic_store_put(pic_store *s, uint64_t chunk_id, int64_t n_tokens, cons
 pic_status pic_store_derive(pic_store *s, uint64_t new_id, uint64_t base_id, int32_t n_rows,
                             const int32_t *rows, void *stream) {
   if (!s) return fail(PIC_ERR_INVALID, "store is NULL");
+  if (s->imported) return fail(PIC_ERR_INVALID, "the store was imported from another process and is read-only");
   auto bit = s->map.find(base_id);
   if (bit == s->map.end()) return fail(PIC_ERR_NOT_FOUND, "base chunk id 0x%llx not in the store",
                                        (unsigned long long)base_id);
@@ -1046,6 +1054,7 @@ pic_status pic_store_derive(pic_store *s, uint64_t new_id, uint64_t base_id, int
 pic_status pic_store_write_rows(pic_store *s, uint64_t chunk_id, int32_t layer, int32_t n_rows,
                                 const int32_t *rows, const void *k, const void *v, void *stream) {
   if (!s) return fail(PIC_ERR_INVALID, "store is NULL");
+  if (s->imported) return fail(PIC_ERR_INVALID, "the store was imported from another process and is read-only");
   auto it = s->map.find(chunk_id);
   if (it == s->map.end()) return fail(PIC_ERR_NOT_FOUND, "chunk id 0x%llx not in the store",
                                       (unsigned long long)chunk_id);
@@ -1095,6 +1104,7 @@ pic_status pic_store_write_rows(pic_store *s, uint64_t chunk_id, int32_t layer, 
 
 pic_status pic_store_remove(pic_store *s, uint64_t chunk_id, void *stream) {
   if (!s) return fail(PIC_ERR_INVALID, "store is NULL");
+  if (s->imported) return fail(PIC_ERR_INVALID, "the store was imported from another process and is read-only");
   auto it = s->map.find(chunk_id);
   if (it == s->map.end()) return fail(PIC_ERR_NOT_FOUND, "chunk id 0x%llx not in the store",
                                       (unsigned long long)chunk_id);
@@ -1132,6 +1142,159 @@ pic_status pic_store_remove(pic_store *s, uint64_t chunk_id, void *stream) {
   else
     s->pending.emplace_back(ev, std::move(freed));
   s->map.erase(it);
+  return PIC_OK;
+}
+
+namespace {
+
+// Layout of an exported store: header, then per chunk its record and runs.
+constexpr uint64_t kExportMagic = 0x31524f5453434950ull;   // "PICSTOR1"
+struct ExportHeader {
+  uint64_t magic;
+  uint64_t bytes;                // whole blob
+  pic_store_desc desc;
+  int64_t capacity, layer_bytes, k_tok_elems, v_tok_elems, used, n_chunks;
+  int32_t n_layers, esz;
+  hipIpcMemHandle_t handle;      // the pool
+};
+struct ExportChunk {
+  uint64_t id;
+  int64_t len;
+  int32_t n_runs, derived;
+};
+struct ExportRun {
+  int64_t page0;
+  int32_t pages, tok0, ntok, skip;
+};
+
+// Pools from 2 GiB up are not exported: opening such a mapping in another
+// process has not returned on the target machines.
+constexpr int64_t kMaxExportBytes = (int64_t(1) << 31) - 1;
+
+size_t export_size(const pic_store *s) {
+  size_t n = sizeof(ExportHeader);
+  for (const auto &kv : s->map) n += sizeof(ExportChunk) + kv.second.runs.size() * sizeof(ExportRun);
+  return n;
+}
+
+}  // namespace
+
+pic_status pic_store_export(pic_store *s, void *buf, size_t buf_bytes, size_t *bytes_out) {
+  if (!s || !bytes_out) return fail(PIC_ERR_INVALID, "store/bytes_out is NULL");
+  if (s->imported) return fail(PIC_ERR_INVALID, "an imported store cannot be exported again");
+  const int64_t pool_bytes = s->layer_bytes * s->n_layers;
+  if (pool_bytes > kMaxExportBytes)
+    return fail(PIC_ERR_UNSUPPORTED, "pool of %lld bytes: only pools below 2 GiB are exported",
+                (long long)pool_bytes);
+  const size_t need = export_size(s);
+  *bytes_out = need;
+  if (!buf) return PIC_OK;
+  if (buf_bytes < need) return fail(PIC_ERR_INVALID, "buffer of %zu bytes, %zu needed", buf_bytes, need);
+  DeviceGuard dg(s->device);
+  if (!dg.ok) return fail(PIC_ERR_HIP, "cannot select the store's device");
+  // every put and copy enqueued so far lands before another process reads
+  HIP_TRY(hipDeviceSynchronize(), "hipDeviceSynchronize(export)");
+  ExportHeader h{};
+  h.magic = kExportMagic;
+  h.bytes = need;
+  h.desc = s->desc;
+  h.capacity = s->capacity;
+  h.layer_bytes = s->layer_bytes;
+  h.k_tok_elems = s->k_tok_elems;
+  h.v_tok_elems = s->v_tok_elems;
+  h.used = s->used;
+  h.n_chunks = (int64_t)s->map.size();
+  h.n_layers = s->n_layers;
+  h.esz = s->esz;
+  HIP_TRY(hipIpcGetMemHandle(&h.handle, s->pool), "hipIpcGetMemHandle(pool)");
+  char *o = (char *)buf;
+  memcpy(o, &h, sizeof h);
+  o += sizeof h;
+  for (const auto &kv : s->map) {
+    const ExportChunk ch{kv.first, kv.second.len, (int32_t)kv.second.runs.size(),
+                         kv.second.derived ? 1 : 0};
+    memcpy(o, &ch, sizeof ch);
+    o += sizeof ch;
+    for (const Run &r : kv.second.runs) {
+      const ExportRun er{r.page0, r.pages, r.tok0, r.ntok, r.skip};
+      memcpy(o, &er, sizeof er);
+      o += sizeof er;
+    }
+  }
+  return PIC_OK;
+}
+
+pic_status pic_store_import(const void *buf, size_t buf_bytes, pic_store **out) {
+  if (!buf || !out) return fail(PIC_ERR_INVALID, "buf/out is NULL");
+  *out = nullptr;
+  ExportHeader h;
+  if (buf_bytes < sizeof h) return fail(PIC_ERR_INVALID, "blob too short");
+  memcpy(&h, buf, sizeof h);
+  if (h.magic != kExportMagic) return fail(PIC_ERR_INVALID, "not an exported store");
+  if (h.bytes > buf_bytes || h.n_chunks < 0 || h.n_layers < 1 || h.n_layers > 256 ||
+      (h.esz != 2 && h.esz != 4) || h.capacity <= 0 || h.capacity % kTile ||
+      h.layer_bytes != h.capacity * (h.k_tok_elems + h.v_tok_elems) * h.esz ||
+      h.layer_bytes * h.n_layers > kMaxExportBytes)
+    return fail(PIC_ERR_INVALID, "inconsistent exported store header");
+  const int64_t pages = h.capacity / kTile;
+  pic_store *s = new (std::nothrow) pic_store();
+  if (!s) return fail(PIC_ERR_OOM, "host allocation failed");
+  s->desc = h.desc;
+  s->esz = h.esz;
+  s->capacity = h.capacity;
+  s->used = h.used;
+  s->k_tok_elems = h.k_tok_elems;
+  s->v_tok_elems = h.v_tok_elems;
+  s->n_layers = h.n_layers;
+  s->layer_bytes = h.layer_bytes;
+  const char *in = (const char *)buf + sizeof h, *end = (const char *)buf + h.bytes;
+  for (int64_t c = 0; c < h.n_chunks; ++c) {
+    ExportChunk ch;
+    if (in + sizeof ch > end) break;
+    memcpy(&ch, in, sizeof ch);
+    in += sizeof ch;
+    if (ch.n_runs < 1 || ch.len < 1 || in + (size_t)ch.n_runs * sizeof(ExportRun) > end) {
+      delete s;
+      return fail(PIC_ERR_INVALID, "corrupt chunk record in the exported store");
+    }
+    Slot sl;
+    sl.len = ch.len;
+    sl.derived = ch.derived != 0;
+    int64_t covered = 0;
+    for (int32_t i = 0; i < ch.n_runs; ++i) {
+      ExportRun er;
+      memcpy(&er, in, sizeof er);
+      in += sizeof er;
+      // every view lies inside the pool and the views cover the chunk in order
+      if (er.page0 < 0 || er.pages < 1 || er.page0 + er.pages > pages || er.skip < 0 ||
+          er.ntok < 1 || er.tok0 != covered ||
+          (int64_t)er.skip * kTile + er.ntok > (int64_t)er.pages * kTile) {
+        delete s;
+        return fail(PIC_ERR_INVALID, "corrupt run in the exported store");
+      }
+      covered += er.ntok;
+      sl.runs.push_back(Run{er.page0, er.pages, er.tok0, er.ntok, er.skip});
+    }
+    if (covered != ch.len || !s->map.emplace(ch.id, std::move(sl)).second) {
+      delete s;
+      return fail(PIC_ERR_INVALID, "corrupt chunk record in the exported store");
+    }
+  }
+  if ((int64_t)s->map.size() != h.n_chunks) {
+    delete s;
+    return fail(PIC_ERR_INVALID, "truncated exported store");
+  }
+  hipError_t e = hipGetDevice(&s->device);
+  if (e == hipSuccess) {
+    s->shape = device_shape();
+    e = hipIpcOpenMemHandle((void **)&s->pool, h.handle, hipIpcMemLazyEnablePeerAccess);
+  }
+  if (e != hipSuccess) {
+    delete s;
+    return hip_fail(e, "hipIpcOpenMemHandle(pool)");
+  }
+  s->imported = true;
+  *out = s;
   return PIC_OK;
 }
 

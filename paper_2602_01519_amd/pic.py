@@ -76,6 +76,8 @@ def lib():
             "pic_store_derive": [vp, u64, u64, i32, vp, vp],
             "pic_store_write_rows": [vp, u64, i32, i32, vp, vp, vp, vp],
             "pic_store_usage": [vp, vp, vp, vp],
+            "pic_store_export": [vp, vp, ctypes.c_size_t, vp],
+            "pic_store_import": [vp, ctypes.c_size_t, vp],
             "pic_link_attn": [vp, vp, i32, vp, vp, vp, f32, vp, vp, vp],
             "pic_link_decode": [vp, vp, i32, vp, vp, vp, f32, i32, vp, vp, vp],
             "pic_link_decode_noalloc": [vp, vp, i32, vp, vp, vp, f32, i32, vp, vp, vp],
@@ -178,6 +180,24 @@ class Store:
         r = np.ascontiguousarray(rows, dtype=np.int32)
         _check(lib().pic_store_write_rows(self.handle, int(chunk_id), int(layer), int(r.size),
                                           r.ctypes.data if r.size else None, _ptr(k), _ptr(v), stream))
+
+    def export(self) -> bytes:
+        """pic_store_export: a description of the store another process can import."""
+        n = ctypes.c_size_t()
+        _check(lib().pic_store_export(self.handle, None, 0, ctypes.byref(n)))
+        buf = ctypes.create_string_buffer(n.value)
+        _check(lib().pic_store_export(self.handle, buf, n.value, ctypes.byref(n)))
+        return buf.raw[:n.value]
+
+    @classmethod
+    def import_(cls, blob: bytes) -> "Store":
+        """pic_store_import: a read-only store over another process's exported pool."""
+        self = cls.__new__(cls)
+        self.desc = None
+        h = ctypes.c_void_p()
+        _check(lib().pic_store_import(blob, len(blob), ctypes.byref(h)))
+        self.handle = h
+        return self
 
     def lookup(self, chunk_id: int) -> int:
         n = ctypes.c_int64()

@@ -67,3 +67,18 @@ def test_null_arguments_are_rejected():
     assert L.pic_link_plan_create(None, None, 8, pic.PREFILL, 0, None) == pic.ERR_INVALID
     assert L.pic_link_plan_run(None, 0, None, None, None, 1.0, None, None, None) == pic.ERR_INVALID
     assert L.pic_link_plan_destroy(None) == pic.OK
+
+
+def test_import_rejects_what_export_did_not_write():
+    """pic_store_import checks the description before any HIP call."""
+    L = pic.lib()
+    h = ctypes.c_void_p(123)
+    assert L.pic_store_import(None, 0, ctypes.byref(h)) == pic.ERR_INVALID
+    blob = bytes(64)
+    assert L.pic_store_import(blob, len(blob), ctypes.byref(h)) == pic.ERR_INVALID
+    assert not h.value
+    junk = bytes(range(256)) * 4
+    assert L.pic_store_import(junk, len(junk), ctypes.byref(h)) == pic.ERR_INVALID
+    assert "exported store" in pic.last_error()
+    n = ctypes.c_size_t()
+    assert L.pic_store_export(None, None, 0, ctypes.byref(n)) == pic.ERR_INVALID
