@@ -81,43 +81,66 @@ def _pmc_per_dispatch(csv_path: str, kernel_prefix: str, counter: str):
     return sum(vals) / len(vals)
 
 
+# HBM bytes from the L2 -> memory request counters of gfx950: reads by request
+# size (32, 64 or 128 bytes), writes as 32- or 64-byte requests. (The
+# profiler's derived FETCH_SIZE takes 128-byte reads from a counter that
+# reads zero on gfx950 and counts them as 64 bytes: a 2 GiB read stream
+# shows as 1 GiB.)
+RD_COUNTERS = ("TCC_EA0_RDREQ_32B", "TCC_EA0_RDREQ_64B", "TCC_EA0_RDREQ_128B")
+WR_COUNTERS = ("TCC_EA0_WRREQ", "TCC_EA0_WRREQ_64B")
+
+
+def read_bytes(rd_csv: str, kernel_prefix: str):
+    n32, n64, n128 = (_pmc_per_dispatch(rd_csv, kernel_prefix, c) for c in RD_COUNTERS)
+    return 32 * n32 + 64 * n64 + 128 * n128
+
+
+def write_bytes(wr_csv: str, kernel_prefix: str):
+    wr, wr64 = (_pmc_per_dispatch(wr_csv, kernel_prefix, c) for c in WR_COUNTERS)
+    return 32 * (wr - wr64) + 64 * wr64
+
+
 def summarize_traffic(args):
     """Writes profiles/traffic_<kernel>_<workload>.json from four rocprofv3 --pmc
-    CSVs: FETCH_SIZE and WRITE_SIZE (KiB per dispatch) of the kernel, and of a
-    plain device copy of known size, whose ratio calibrates the counters."""
-    fetch_csv, write_csv, copy_fetch_csv, copy_write_csv = args.summarize_traffic
-    copy_bytes = args.copy_mib * (1 << 20)
-    cf = _pmc_per_dispatch(copy_fetch_csv, "copyBuffer", "FETCH_SIZE") * 1024.0
-    cw = _pmc_per_dispatch(copy_write_csv, "copyBuffer", "WRITE_SIZE") * 1024.0
-    kf = _pmc_per_dispatch(fetch_csv, args.kernel, "FETCH_SIZE") * 1024.0
-    kw = _pmc_per_dispatch(write_csv, args.kernel, "WRITE_SIZE") * 1024.0
-    f_scale, w_scale = copy_bytes / cf, copy_bytes / cw
+    CSVs: the read-request counters (RD_COUNTERS) and write-request counters
+    (WR_COUNTERS) of the kernel, and the same counters of the streaming-read
+    and streaming-write kernels over --calib-mib MiB, which check the byte
+    formula on dispatches of known size."""
+    rd_csv, wr_csv, calib_rd_csv, calib_wr_csv = args.summarize_traffic
+    calib_bytes = args.calib_mib * (1 << 20)
+    cr = read_bytes(calib_rd_csv, "peak_read_kernel")
+    cw = write_bytes(calib_wr_csv, "peak_write_kernel")
+    kr, kw = read_bytes(rd_csv, args.kernel), write_bytes(wr_csv, args.kernel)
+    base = args.kernel.split("<")[0]
+    name = args.traffic_name or base
     rec = {
         "kernel": args.kernel,
         "workload": args.config,
-        "kernel_source_sha": kernel_source_sha(args.kernel),
-        "fetch_bytes_raw": kf, "write_bytes_raw": kw,
-        "copy_bytes": copy_bytes, "copy_fetch_raw": cf, "copy_write_raw": cw,
-        "fetch_scale": f_scale, "write_scale": w_scale,
-        "hbm_bytes_per_launch": kf * f_scale + kw * w_scale,
+        "kernel_source_sha": kernel_source_sha(base),
+        "counters": list(RD_COUNTERS + WR_COUNTERS),
+        "read_bytes": kr, "write_bytes": kw,
+        "calib_bytes": calib_bytes, "calib_read_measured": cr, "calib_write_measured": cw,
+        "hbm_bytes_per_launch": kr + kw,
     }
     os.makedirs(PROFILES, exist_ok=True)
-    out = os.path.join(PROFILES, f"traffic_{args.kernel}_{args.config}.json")
+    out = os.path.join(PROFILES, f"traffic_{name}_{args.config}.json")
     json.dump(rec, open(out, "w"), indent=1)
     print(json.dumps(rec))
     return 0
 
 
-def copy_calibration(args):
-    """A plain device-to-device copy of --copy-mib MiB, for counter calibration."""
+def stream_calibration(args):
+    """--calib read|write: streaming-read (or -write) passes over --calib-mib MiB,
+    the known-size dispatches that calibrate the traffic counters; prints the
+    measured rates."""
     import torch
-    n = args.copy_mib * (1 << 20)
-    src = torch.empty(n, dtype=torch.uint8, device="cuda").random_(0, 255)
-    dst = torch.empty_like(src)
-    for _ in range(args.warmup + args.steps):
-        dst.copy_(src)
-    torch.cuda.synchronize()
-    print(json.dumps({"copy_bytes": n, "copies": args.warmup + args.steps}))
+    from paper_2602_01519_amd import pic
+    n = args.calib_mib * (1 << 20)
+    buf = torch.empty(n, dtype=torch.uint8, device="cuda")
+    fn = pic.peak_hbm_read if args.calib == "read" else pic.peak_hbm_write
+    rates = [fn(buf, n) for _ in range(args.steps)]
+    print(json.dumps({"calib": args.calib, "bytes": n, "dispatches": args.steps,
+                      "gbs": [round(r, 1) for r in rates]}))
     return 0
 
 
@@ -299,11 +322,16 @@ def main(argv=None):
                          "skinny_rag")
     ap.add_argument("--cpu-budget", type=float, default=15.0,
                     help="seconds of oracle time for the CPU baseline (0 = skip)")
-    ap.add_argument("--copy-mib", type=int, default=0,
-                    help="run a plain device copy of this many MiB instead (counter calibration)")
+    ap.add_argument("--calib", choices=["read", "write"],
+                    help="run streaming-read or -write passes of --calib-mib MiB instead "
+                         "(traffic counter calibration)")
+    ap.add_argument("--calib-mib", type=int, default=2048)
     ap.add_argument("--summarize-traffic", nargs=4, metavar="CSV",
-                    help="kernel FETCH_SIZE csv, kernel WRITE_SIZE csv, copy FETCH csv, copy WRITE csv")
+                    help="kernel read-request csv, kernel write-request csv, and the same "
+                         "two for the streaming-read and streaming-write calibration runs")
     ap.add_argument("--kernel", default="link_mfma_d128_kernel")
+    ap.add_argument("--traffic-name", default=None,
+                    help="file name stem of the traffic record (default: the kernel's base name)")
     ap.add_argument("--projections", action="store_true",
                     help="time the MLA absorption / up-projection kernels instead (one line each)")
     args = ap.parse_args(argv)
@@ -323,8 +351,8 @@ def main(argv=None):
         print("bench.py needs a GPU", file=sys.stderr)
         return 2
     torch.cuda.set_device(0)
-    if args.copy_mib:
-        return copy_calibration(args)
+    if args.calib:
+        return stream_calibration(args)
     if args.projections:
         return projections(args)
     cfg = W.CONFIGS[args.config]

@@ -356,9 +356,13 @@ pic_status pic_prof_end(double *kernel_ms, int64_t *launches, char *name_buf, in
  * pic_peak_hbm_read: HBM read rate in GB/s of one streaming pass over buf
  *   (device memory, 16-byte aligned, bytes a positive multiple of 16; use a
  *   buffer far larger than the last-level cache).
+ * pic_peak_hbm_write: the same for one streaming pass of stores over buf
+ *   (overwrites it). One dispatch of either moves exactly `bytes`, which
+ *   also calibrates the HBM traffic counters of a profiler.
  * Errors: INVALID, HIP. */
 pic_status pic_peak_mfma_bf16(int32_t iters, double *tflops, void *stream);
 pic_status pic_peak_hbm_read(const void *buf, int64_t bytes, double *gbs, void *stream);
+pic_status pic_peak_hbm_write(void *buf, int64_t bytes, double *gbs, void *stream);
 
 const char *pic_status_str(pic_status status);
 const char *pic_last_error(void);

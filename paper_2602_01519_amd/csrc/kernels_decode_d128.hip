@@ -69,8 +69,8 @@ struct Tile {
 // Uniform facts of the tile being loaded / computed.
 struct TileInfo {
   const char *k;    // first K row of the tile, kv head applied (bytes)
-  const char *v;    // V^T row 0 at the tile's first key, kv head applied
-  int lp;           // V^T row stride (elements)
+  const char *v;    // the tile's V^T panel, kv head applied
+  int lp;           // padded tokens of the link
   int nvalid;       // valid keys in the tile
   int j0;           // key index of the tile's first key within its link
   int own;          // own-KV tile (causal mask)
@@ -96,7 +96,7 @@ __device__ __forceinline__ TileInfo tile_info(Cursor &c, int t) {
       r.j0 = tt * kT;
       r.own = t >= c.doc_tiles32;
       r.k = uni(e.k) + ((int64_t)c.kvh * lp + tt * kT) * kD * 2;
-      r.v = uni(e.v) + ((int64_t)c.kvh * kD * lp + tt * kT) * 2;
+      r.v = uni(e.v) + ((int64_t)c.kvh * kD * lp + tt * kT * kD) * 2;   // the tile's V^T panel
       return r;
     }
     ++c.li;
@@ -104,8 +104,18 @@ __device__ __forceinline__ TileInfo tile_info(Cursor &c, int t) {
 }
 
 // Per-lane byte offsets of the tile's loads: K block b, step s: key row
-// krow_b, d = 32 s + 8 (l/16); V block b: value row 16 b + l%16, keys
-// 8 (l/16) .. +7.
+// krow_b, d = 32 s + 8 (l/16); V block b: value row 16 b + l%16 of the
+// tile's 32-key panel, keys 8 (l/16) .. +7 (two lanes of a 16-lane group
+// read one 128-byte line).
+// The keys are read once per call: the loads carry the nontemporal hint
+// (streaming, measured 11% faster on a plain read stream).
+typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(1))) const u32x4 *global_u32x4;
+__device__ __forceinline__ uint4 load_nt(const char *p) {
+  const u32x4 w = __builtin_nontemporal_load((global_u32x4)p);
+  return make_uint4(w.x, w.y, w.z, w.w);
+}
+
 __device__ __forceinline__ void load_tile(const TileInfo &r, int lane, Tile &x) {
   const int grp = lane >> 4, m = lane & 15;
 #pragma unroll
@@ -113,11 +123,10 @@ __device__ __forceinline__ void load_tile(const TileInfo &r, int lane, Tile &x) 
     const int krow = 8 * (m >> 2) + 4 * b + (m & 3);
 #pragma unroll
     for (int s = 0; s < 4; ++s)
-      x.k[b * 4 + s] = *(const uint4 *)(r.k + (uint32_t)((krow * kD + 32 * s + 8 * grp) * 2));
+      x.k[b * 4 + s] = load_nt(r.k + (uint32_t)((krow * kD + 32 * s + 8 * grp) * 2));
   }
 #pragma unroll
-  for (int b = 0; b < 8; ++b)
-    x.v[b] = *(const uint4 *)(r.v + ((uint32_t)(16 * b + m) * (uint32_t)r.lp * 2u + 16u * grp));
+  for (int b = 0; b < 8; ++b) x.v[b] = load_nt(r.v + (uint32_t)((16 * b + m) * kT * 2 + 16 * grp));
 }
 
 struct State {

@@ -42,9 +42,9 @@ __global__ void put_rows_kernel(const uint4 *__restrict__ src, uint4 *__restrict
   }
 }
 
-// src token-major [n][heads][width] -> dst [heads][width][lp] (token axis
-// contiguous), columns >= n zero. 64x64 tiles through LDS so both the read
-// and the write are coalesced.
+// src token-major [n][heads][width] -> dst [heads][lp / 32][width][32]
+// (32-token panels, tokens contiguous), columns >= n zero. 64x64 tiles
+// through LDS so both the read and the write are coalesced.
 template <typename E>
 __global__ void put_transposed_kernel(const E *__restrict__ src, E *__restrict__ dst, int64_t n,
                                       int32_t lp, int32_t heads, int32_t width) {
@@ -65,7 +65,7 @@ __global__ void put_transposed_kernel(const E *__restrict__ src, E *__restrict__
     const int el = i >> 6, tl = i & 63;
     const int64_t t = t0 + tl;
     const int e = e0 + el;
-    if (e < width && t < lp) dst[((int64_t)h * width + e) * lp + t] = tile[tl][el];
+    if (e < width && t < lp) dst[vt_offset(h, e, t, lp, width)] = tile[tl][el];
   }
 }
 
@@ -91,7 +91,7 @@ __device__ __forceinline__ const E *key_row(const LinkEntry &e, int head, int ro
 template <typename E>
 __device__ __forceinline__ const E *value_at(const LinkEntry &e, int head, int dim, int row,
                                              int d_v) {
-  return (const E *)e.v + ((int64_t)head * d_v + dim) * e.lp + row;
+  return (const E *)e.v + vt_offset(head, dim, row, e.lp, d_v);
 }
 
 template <typename E>
@@ -136,7 +136,7 @@ __global__ void write_rows_kernel(const RowDst *__restrict__ dst, int32_t n,
   if (!mla)
     for (int x = threadIdx.x; x < heads * d_v; x += blockDim.x) {
       const int h = x / d_v, e = x - h * d_v;
-      ((E *)d.v)[((int64_t)h * d_v + e) * d.lp] = src_v[(int64_t)i * heads * d_v + x];
+      ((E *)d.v)[(int64_t)h * d_v * d.lp + e * kPanel] = src_v[(int64_t)i * heads * d_v + x];
     }
 }
 
@@ -196,7 +196,8 @@ __device__ __forceinline__ void prep_transposed_tile(const ReqEntry &R, const Li
     } vals;
 #pragma unroll
     for (int x = 0; x < EPV; ++x) vals.e[x] = tile_s[(tc * EPV + x) * ROW + el];
-    *(uint4 *)(dst + ((int64_t)h * width + e) * L.lp + t0 + tc * EPV) = vals.u;
+    // EPV tokens (4 or 8) never straddle a 32-token panel
+    *(uint4 *)(dst + vt_offset(h, e, t0 + tc * EPV, L.lp, width)) = vals.u;
   }
 }
 
@@ -383,9 +384,13 @@ __global__ __launch_bounds__(256) void link_valu_kernel(LinkParams p) {
     // K rows (d_k elements, whole 16-byte units) and V^T rows (64 keys)
     copy_rows_lds((const char *)key_row<T>(E, MLA ? 0 : kvh, tt * kTile, d_k),
                   (int64_t)d_k * sizeof(T), kTile, kwords / 4, ks, kstride);
+    // V^T: the tile's two 32-token panels, each d_v rows of 32 keys
     if (!MLA)
-      copy_rows_lds((const char *)value_at<T>(E, kvh, 0, tt * kTile, d_v),
-                    (int64_t)E.lp * sizeof(T), d_v, vwords / 4, vts, vstride);
+#pragma unroll
+      for (int hp = 0; hp < kTile / kPanel; ++hp)
+        copy_rows_lds((const char *)value_at<T>(E, kvh, 0, tt * kTile + hp * kPanel, d_v),
+                      (int64_t)kPanel * sizeof(T), d_v, kPanel * (int)sizeof(T) / 16,
+                      vts + hp * (kPanel / EPW), vstride);
     __syncthreads();
 
     // scores: lane = key

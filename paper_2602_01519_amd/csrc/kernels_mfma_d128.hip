@@ -27,8 +27,8 @@
 // (three buffer pairs, 96 KB; the copy of tile t+2 is issued while tile t+1
 // is in flight), measured 13.5% faster on the skinny-question workload and
 // about 1% slower where every wave is busy.
-// The store keeps V transposed per chunk, so a V^T tile is 128 rows of 128
-// contiguous bytes. The M index of the QK^T product is permuted (key row
+// The store keeps V transposed per chunk in panels of 32 tokens, so a V^T
+// tile is two contiguous 8 KB panels of 128 rows of 64 bytes. The M index of the QK^T product is permuted (key row
 // pi(m) feeds M index m) so that the scores a lane receives for a 16-key PV
 // step are 8 consecutive keys: P^T feeds the PV product straight from
 // registers and the V^T fragment for those keys is one 16-byte LDS read.
@@ -101,7 +101,7 @@ __device__ __forceinline__ float half_swap_sum(float x) {
 struct TileRef {
   const char *k;     // first K row of the tile (kv head applied), bytes
   const char *v;     // V^T row 0 at the tile's first key (kv head applied)
-  int lp;            // V^T row stride in elements
+  int lp;            // padded tokens of the link
   int nvalid;        // valid keys in the tile
   int j0;            // key index of the tile's first key within its link
   int tok;           // ... within the request's linked rows (document tiles)
@@ -124,7 +124,7 @@ struct Ctx {
   int llen, llp, ltile0, lend; // its tokens, padded tokens, first tile, tile after its last
   int ltok0;                   // its first row within the request's linked rows
   uint32_t koff[kCopySets];    // byte offsets of this lane's K chunks within a tile
-  uint32_t vrow[kCopySets], vcol[kCopySets];   // row / byte column of its V^T chunks
+  uint32_t voff[kCopySets];    // byte offsets of its V^T chunks within a tile's two panels
 };
 
 __device__ __forceinline__ void cursor_load(Ctx &c) {
@@ -151,7 +151,7 @@ __device__ __forceinline__ TileRef tile_ref(Ctx &c, int t) {
   r.tok = c.ltok0 + tt * kTile;
   r.own = t >= c.R.doc_tiles;
   r.k = c.lk + ((int64_t)c.kvh * c.llp + tt * kTile) * kD * 2;
-  r.v = c.lv + ((int64_t)c.kvh * kD * c.llp + tt * kTile) * 2;
+  r.v = c.lv + ((int64_t)c.kvh * kD * c.llp + tt * kTile * kD) * 2;   // the tile's two panels
   return r;
 }
 
@@ -165,25 +165,32 @@ __device__ __forceinline__ TileRef tile_ref(Ctx &c, int t) {
 // possible LDS access in flight, which turns every wait for an LDS fragment
 // read into a wait for all of them; with buffer copies it keeps precise
 // counts and the fragment reads stay ahead of their MFMAs.
+// kAux: the copies' cache policy; kNonTemporal for calls in which every K/V
+// byte is read by one workgroup only (short questions: the key range is
+// split, not shared by row blocks), so it need not stay in the caches.
+constexpr int kNonTemporal = 2;
+template <int kAux>
 __device__ __forceinline__ void lds_dma16(const void *base, uint32_t voff, uint4 *dst) {
   const __amdgpu_buffer_rsrc_t rs =
       __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(base), (short)0, -1, 0x00020000);
-  __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (lds_ptr)dst, 16, voff, 0, 0, 0);
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (lds_ptr)dst, 16, voff, 0, 0, kAux);
 }
 
+template <int kAux>
 __device__ __forceinline__ void tile_copy(const Ctx &c, int i, const TileRef &r, uint4 *kdst,
                                           uint4 *vdst) {
   if (i < kCopySets) {
-    lds_dma16(r.k, c.koff[i], kdst + (i * kWaves + c.wave) * 64);
+    lds_dma16<kAux>(r.k, c.koff[i], kdst + (i * kWaves + c.wave) * 64);
   } else {
     const int u = i - kCopySets;
-    lds_dma16(r.v, c.vrow[u] * (uint32_t)r.lp * 2u + c.vcol[u], vdst + (u * kWaves + c.wave) * 64);
+    lds_dma16<kAux>(r.v, c.voff[u], vdst + (u * kWaves + c.wave) * 64);
   }
 }
+template <int kAux>
 __device__ __forceinline__ void issue_tile(const Ctx &c, const TileRef &r, uint4 *kdst,
                                            uint4 *vdst) {
 #pragma unroll
-  for (int i = 0; i < 2 * kCopySets; ++i) tile_copy(c, i, r, kdst, vdst);
+  for (int i = 0; i < 2 * kCopySets; ++i) tile_copy<kAux>(c, i, r, kdst, vdst);
 }
 
 // Workgroup barrier of the tile loop, without the memory fence of
@@ -237,7 +244,7 @@ __device__ __forceinline__ void mask_tile(const Ctx &c, f32x16 &s0, f32x16 &s1, 
 // rescale), O += V^T P^T from vt. In both matrix sections the LDS fragment
 // reads are issued a few MFMAs ahead of their use (scheduling groups), so an
 // MFMA does not wait on the read issued right before it.
-template <bool kLim>
+template <bool kLim, int kAux>
 __device__ __forceinline__ void compute_tile(const Ctx &c, const uint4 *kt, const uint4 *vt,
                                              const bf16x8 (&qf)[8], Acc &a, const TileRef &ref,
                                              int lim, const DocLim &dlm, float sc,
@@ -264,7 +271,7 @@ __device__ __forceinline__ void compute_tile(const Ctx &c, const uint4 *kt, cons
       kb[st + kQkAhead] = as_bf16x8(kt[k_slot(32 + krow0, (st + kQkAhead) * 2 + c.g)]);
     }
     constexpr int kEvery = 8 / (2 * kCopySets);   // QK steps per copy
-    if (st % kEvery == 0) tile_copy(c, st / kEvery, nref, nk, nv);
+    if (st % kEvery == 0) tile_copy<kAux>(c, st / kEvery, nref, nk, nv);
     s0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka[st], qf[st], s0, 0, 0, 0);
     s1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kb[st], qf[st], s1, 0, 0, 0);
     __builtin_amdgcn_sched_barrier(0);
@@ -329,6 +336,7 @@ __global__ __launch_bounds__(kWaves * 64, 8 / kWaves) void link_mfma_d128_kernel
   __shared__ uint4 sv0[kD * 8], sv1[kD * 8];
   __shared__ uint4 sk2[kStages == 3 ? kTile * 16 : 1], sv2[kStages == 3 ? kD * 8 : 1];
 
+  constexpr int kAux = kStages == 3 ? kNonTemporal : 0;
   Ctx c;
   c.lane = threadIdx.x & 63;
   c.wave = uni(threadIdx.x >> 6);
@@ -390,9 +398,10 @@ __global__ __launch_bounds__(kWaves * 64, 8 / kWaves) void link_mfma_d128_kernel
     const int s = (u * kWaves + c.wave) * 64 + c.lane;
     const int key = s >> 4, kc = (s & 15) ^ hk(key & 15);
     c.koff[u] = (uint32_t)((key * kD + kc * 8) * 2);
-    const int dv = s >> 3;
-    c.vrow[u] = (uint32_t)dv;
-    c.vcol[u] = (uint32_t)(((s & 7) ^ hv(dv & 31)) * 16);
+    // V^T chunk cc (keys 8 cc .. 8 cc + 7) of value row dv: panel cc / 4,
+    // row dv, 16-byte unit cc % 4
+    const int dv = s >> 3, cc = (s & 7) ^ hv(dv & 31);
+    c.voff[u] = (uint32_t)((cc >> 2) * kD * kPanel * 2 + dv * kPanel * 2 + (cc & 3) * 16);
   }
 
   c.links = (const_links)p.links + c.R.link0;
@@ -405,7 +414,7 @@ __global__ __launch_bounds__(kWaves * 64, 8 / kWaves) void link_mfma_d128_kernel
   TileRef ref0{}, ref1{}, ref2{};
   if (t_begin < t_end) {
     ref0 = tile_ref(c, t_begin);
-    issue_tile(c, ref0, sk0, sv0);
+    issue_tile<kAux>(c, ref0, sk0, sv0);
   }
 
   // Q fragments: d = step*16 + g*8 + (0..7)
@@ -424,7 +433,7 @@ __global__ __launch_bounds__(kWaves * 64, 8 / kWaves) void link_mfma_d128_kernel
   // counts fixed)
   if (kStages == 3 && t_begin < t_end) {
     ref1 = t_begin + 1 < t_end ? tile_ref(c, t_begin + 1) : ref0;
-    issue_tile(c, ref1, sk1, sv1);
+    issue_tile<kAux>(c, ref1, sk1, sv1);
   }
 
   Acc a;
@@ -451,25 +460,25 @@ __global__ __launch_bounds__(kWaves * 64, 8 / kWaves) void link_mfma_d128_kernel
     for (int t = t_begin; t < t_end; t += 3) {
       ref2 = t + 2 < t_end ? tile_ref(c, t + 2) : ref1;
       if (active)
-        compute_tile<kLim>(c, sk0, sv0, qf, a, ref0, lim, dlm, sc, ref2, sk2, sv2);
+        compute_tile<kLim, kAux>(c, sk0, sv0, qf, a, ref0, lim, dlm, sc, ref2, sk2, sv2);
       else
-        issue_tile(c, ref2, sk2, sv2);
+        issue_tile<kAux>(c, ref2, sk2, sv2);
       asm volatile("s_waitcnt vmcnt(%0)" ::"n"(2 * kCopySets) : "memory");
       tile_barrier();
       if (t + 1 >= t_end) break;
       ref0 = t + 3 < t_end ? tile_ref(c, t + 3) : ref2;
       if (active)
-        compute_tile<kLim>(c, sk1, sv1, qf, a, ref1, lim, dlm, sc, ref0, sk0, sv0);
+        compute_tile<kLim, kAux>(c, sk1, sv1, qf, a, ref1, lim, dlm, sc, ref0, sk0, sv0);
       else
-        issue_tile(c, ref0, sk0, sv0);
+        issue_tile<kAux>(c, ref0, sk0, sv0);
       asm volatile("s_waitcnt vmcnt(%0)" ::"n"(2 * kCopySets) : "memory");
       tile_barrier();
       if (t + 2 >= t_end) break;
       ref1 = t + 4 < t_end ? tile_ref(c, t + 4) : ref0;
       if (active)
-        compute_tile<kLim>(c, sk2, sv2, qf, a, ref2, lim, dlm, sc, ref1, sk1, sv1);
+        compute_tile<kLim, kAux>(c, sk2, sv2, qf, a, ref2, lim, dlm, sc, ref1, sk1, sv1);
       else
-        issue_tile(c, ref1, sk1, sv1);
+        issue_tile<kAux>(c, ref1, sk1, sv1);
       asm volatile("s_waitcnt vmcnt(%0)" ::"n"(2 * kCopySets) : "memory");
       tile_barrier();
     }
@@ -487,18 +496,18 @@ __global__ __launch_bounds__(kWaves * 64, 8 / kWaves) void link_mfma_d128_kernel
       // tile t in buffers 0; copy tile t+1 into buffers 1
       ref1 = t + 1 < t_end ? tile_ref(c, t + 1) : ref0;
       if (active)
-        compute_tile<kLim>(c, sk0, sv0, qf, a, ref0, lim, dlm, sc, ref1, sk1, sv1);
+        compute_tile<kLim, kAux>(c, sk0, sv0, qf, a, ref0, lim, dlm, sc, ref1, sk1, sv1);
       else
-        issue_tile(c, ref1, sk1, sv1);
+        issue_tile<kAux>(c, ref1, sk1, sv1);
       asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
       __syncthreads();
       if (t + 1 >= t_end) break;
       // tile t+1 in buffers 1; copy tile t+2 into buffers 0
       ref0 = t + 2 < t_end ? tile_ref(c, t + 2) : ref1;
       if (active)
-        compute_tile<kLim>(c, sk1, sv1, qf, a, ref1, lim, dlm, sc, ref0, sk0, sv0);
+        compute_tile<kLim, kAux>(c, sk1, sv1, qf, a, ref1, lim, dlm, sc, ref0, sk0, sv0);
       else
-        issue_tile(c, ref0, sk0, sv0);
+        issue_tile<kAux>(c, ref0, sk0, sv0);
       asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
       __syncthreads();
     }

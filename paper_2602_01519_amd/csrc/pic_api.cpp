@@ -294,10 +294,11 @@ LinkEntry run_entry(const pic_store *s, const Run &r, int32_t layer) {
   const int64_t skip_tok = (int64_t)r.skip * kTile;
   const char *block = s->pool + (int64_t)layer * s->layer_bytes + r.page0 * kTile * slot_tok_bytes;
   LinkEntry E{};
-  // K rows and V^T columns of the view start skip_tok tokens into the block
+  // K rows and V^T panels of the view start skip_tok tokens into the block
+  // (skip_tok is a multiple of the 32-token panel: skip_tok * d_v elements)
   E.k = block + skip_tok * s->desc.d_k * s->esz;
   E.v = s->desc.kind == PIC_GQA
-            ? block + (int64_t)lp * s->k_tok_elems * s->esz + skip_tok * s->esz
+            ? block + (int64_t)lp * s->k_tok_elems * s->esz + skip_tok * s->desc.d_v * s->esz
             : E.k;
   E.len = r.ntok;
   E.lp = lp;
@@ -454,11 +455,11 @@ pic_status plan_call(pic_store *s, const pic_link_req *req, int32_t n_q_heads, f
       for (const Run &run : sl.runs) {
         if (run.tok0 + run.ntok <= start) continue;
         LinkEntry E = run_entry(s, run, layer);
-        // skip the run's pages before `start`: rows of K, columns of V^T
-        // (the row stride stays the run's)
+        // skip the run's pages before `start`: rows of K, panels of V^T
+        // (the head stride stays the run's)
         const int32_t skip = std::max(0, start - run.tok0);
         E.k = (const char *)E.k + (int64_t)skip * d.d_k * s->esz;
-        E.v = d.kind == PIC_MLA ? E.k : (const char *)E.v + (int64_t)skip * s->esz;
+        E.v = d.kind == PIC_MLA ? E.k : (const char *)E.v + (int64_t)skip * d.d_v * s->esz;
         E.len -= skip;
         E.tile0 = (int32_t)tiles;
         E.tok0 = (int32_t)toks;
@@ -1024,10 +1025,10 @@ pic_status pic_store_derive(pic_store *s, uint64_t new_id, uint64_t base_id, int
                            (size_t)S.lp * d.d_k * s->esz, kw, (size_t)d.n_kv_heads,
                            hipMemcpyDeviceToDevice, st);
       if (e != hipSuccess) break;
-      if (d.kind == PIC_GQA) {
-        e = hipMemcpy2DAsync((void *)D.v, (size_t)D.lp * s->esz, S.v, (size_t)S.lp * s->esz,
-                             (size_t)kTile * s->esz, (size_t)d.n_kv_heads * d.d_v,
-                             hipMemcpyDeviceToDevice, st);
+      if (d.kind == PIC_GQA) {   // a page is two whole V^T panels per head
+        e = hipMemcpy2DAsync((void *)D.v, (size_t)D.lp * d.d_v * s->esz, S.v,
+                             (size_t)S.lp * d.d_v * s->esz, (size_t)kTile * d.d_v * s->esz,
+                             (size_t)d.n_kv_heads, hipMemcpyDeviceToDevice, st);
         if (e != hipSuccess) break;
       }
     }
@@ -1080,7 +1081,7 @@ pic_status pic_store_write_rows(pic_store *s, uint64_t chunk_id, int32_t layer, 
     const LinkEntry E = run_entry(s, r, layer);
     const int64_t t = rows[i] - r.tok0;
     dst[i].k = (char *)E.k + t * s->desc.d_k * s->esz;
-    dst[i].v = gqa ? (char *)E.v + t * s->esz : nullptr;
+    dst[i].v = gqa ? (char *)E.v + vt_offset(0, 0, t, E.lp, s->desc.d_v) * s->esz : nullptr;
     dst[i].lp = E.lp;
   }
   DeviceGuard dg(s->device);
@@ -1666,6 +1667,24 @@ pic_status pic_peak_hbm_read(const void *buf, int64_t bytes, double *gbs, void *
   double ms = 0.0;
   const pic_status rc = time_peak((hipStream_t)stream, &ms, [&](float *out) {
     return pic::launch_peak_read(buf, bytes, out, (hipStream_t)stream);
+  });
+  if (rc != PIC_OK) return rc;
+  *gbs = ms > 0.0 ? (double)bytes / (ms * 1e-3) / 1e9 : 0.0;
+  return PIC_OK;
+}
+
+pic_status pic_peak_hbm_write(void *buf, int64_t bytes, double *gbs, void *stream) {
+  if (!gbs || !buf) return fail(PIC_ERR_INVALID, "buf and gbs must not be NULL");
+  if (bytes <= 0 || bytes % 16 != 0 || (uintptr_t)buf % 16 != 0)
+    return fail(PIC_ERR_INVALID, "bytes must be a positive multiple of 16 and buf 16-byte aligned");
+  hipPointerAttribute_t at{};
+  if (hipPointerGetAttributes(&at, buf) != hipSuccess || at.type != hipMemoryTypeDevice) {
+    (void)hipGetLastError();
+    return fail(PIC_ERR_INVALID, "buf is not device memory");
+  }
+  double ms = 0.0;
+  const pic_status rc = time_peak((hipStream_t)stream, &ms, [&](float *) {
+    return pic::launch_peak_write(buf, bytes, (hipStream_t)stream);
   });
   if (rc != PIC_OK) return rc;
   *gbs = ms > 0.0 ? (double)bytes / (ms * 1e-3) / 1e9 : 0.0;

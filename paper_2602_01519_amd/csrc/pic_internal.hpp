@@ -16,13 +16,26 @@ constexpr int kTile = 64;
 // Layout of one chunk slot with padded length lp (elements of the store's
 // dtype):
 //   GQA  K block  [n_kv_heads][lp][d_k]    (head-major, token rows)
-//        V block  [n_kv_heads][d_v][lp]    (transposed: the value dim is the
-//                                          row, tokens contiguous)
+//        V block  [n_kv_heads][lp / 32][d_v][32]
+//                                          (transposed in panels of 32 tokens:
+//                                          value dim = row of a panel, its 32
+//                                          tokens contiguous)
 //   MLA  K block  [lp][d_k]                (value = first d_v of each row)
 // The transposed V lets a matrix-core operand read 8 consecutive keys of one
-// value column with a single 16-byte load. A request's own KV is laid out
-// the same way (in the call's workspace) before the attention kernel runs,
-// so every key tile of a request -- document or own -- is read alike.
+// value column with a single 16-byte load; the panels keep the rows of a
+// 32-key tile together, so a 32-key tile reads whole 128-byte lines (two
+// bf16 rows, or one fp32 row) and a 64-key tile is one contiguous block. A
+// request's own KV is laid out the same way (in the call's workspace) before
+// the attention kernel runs, so every key tile of a request -- document or
+// own -- is read alike.
+constexpr int kPanel = 32;
+
+// Element offset of value dim e of token t (relative to the slot's first
+// token) of head h in a V block with padded length lp.
+__host__ __device__ __forceinline__ int64_t vt_offset(int64_t h, int64_t e, int64_t t, int64_t lp,
+                                                     int64_t d_v) {
+  return h * d_v * lp + (t / kPanel) * (d_v * kPanel) + e * kPanel + (t % kPanel);
+}
 
 // A per-row limit on the visible linked rows that no request reaches.
 constexpr int kNoLimit = 1 << 30;
@@ -91,8 +104,8 @@ hipError_t launch_gather(const LinkEntry *links, int32_t n_links, int64_t total_
                          void *k_out, void *v_out, hipStream_t st);
 
 // Destination of one row written into a chunk slot: its K row of head 0
-// (head h at + h * lp * d_k elements) and its V^T column of head 0, dim 0
-// (head h, dim e at + (h * d_v + e) * lp; unused for MLA).
+// (head h at + h * lp * d_k elements) and its V^T entry of head 0, dim 0
+// (head h, dim e at + h * d_v * lp + e * kPanel; unused for MLA).
 struct RowDst {
   void *k;
   void *v;
@@ -155,6 +168,7 @@ int64_t peak_out_floats();
 double peak_mfma_flops(int32_t iters);
 hipError_t launch_peak_mfma(float *out, int32_t iters, hipStream_t st);
 hipError_t launch_peak_read(const void *src, int64_t bytes, float *out, hipStream_t st);
+hipError_t launch_peak_write(void *dst, int64_t bytes, hipStream_t st);
 
 // The library's static device scratch (a file-scope array, no allocation):
 // its size, and its address on the current device (resolved once per

@@ -92,6 +92,7 @@ def lib():
             "pic_prof_end": [vp, vp, vp, i32],
             "pic_peak_mfma_bf16": [i32, vp, vp],
             "pic_peak_hbm_read": [vp, i64, vp, vp],
+            "pic_peak_hbm_write": [vp, i64, vp, vp],
         }
         for name, args in sig.items():
             fn = getattr(L, name)
@@ -326,6 +327,13 @@ def peak_hbm_read(buf, nbytes: int, stream: Optional[int] = None) -> float:
     """Achievable HBM read rate (GB/s) over device buffer buf; blocking."""
     out = ctypes.c_double()
     _check(lib().pic_peak_hbm_read(_ptr(buf), int(nbytes), ctypes.byref(out), stream))
+    return out.value
+
+
+def peak_hbm_write(buf, nbytes: int, stream: Optional[int] = None) -> float:
+    """Achievable HBM write rate (GB/s) over device buffer buf (overwritten); blocking."""
+    out = ctypes.c_double()
+    _check(lib().pic_peak_hbm_write(_ptr(buf), int(nbytes), ctypes.byref(out), stream))
     return out.value
 
 

@@ -460,6 +460,11 @@ def test_peak_microbenchmarks():
     assert 10.0 < gbs < 1e6            # a 64 MiB pass may be served from cache
     with pytest.raises(pic.PicError):
         pic.peak_mfma_bf16(0)
+    gbs_w = pic.peak_hbm_write(buf, buf.numel())
+    assert 10.0 < gbs_w < 1e6
+    assert bool(torch.any(buf != 0))           # the stores landed
+    with pytest.raises(pic.PicError):
+        pic.peak_hbm_write(buf, 15)
     with pytest.raises(pic.PicError):
         pic.peak_hbm_read(buf, 15)
     host = np.zeros(1024, np.uint8)
