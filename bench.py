@@ -47,6 +47,7 @@ KERNEL_SOURCES = {
     "link_decode_d128_kernel": "kernels_decode_d128.hip",
     "link_mla_kernel": "kernels_mla.hip",
     "link_valu_kernel": "kernels_generic.hip",
+    "proj_kernel": "kernels_mla_proj.hip",
 }
 PROFILES = os.path.join(ROOT, "profiles")
 
@@ -164,11 +165,13 @@ def projections(args):
     out = torch.empty((T, H, 128), dtype=torch.int16, device="cuda")
     st = torch.cuda.current_stream()
     flops = 2.0 * T * H * 128 * 512
-    cases = [("pic_mla_absorb_q", lambda: pic.mla_absorb_q(T, H, q, w_uk_t, q_out, st.cuda_stream),
+    cases = [("pic_mla_absorb_q", "mla_absorb",
+              lambda: pic.mla_absorb_q(T, H, q, w_uk_t, q_out, st.cuda_stream),
               (T * H * (192 + 576) + H * 512 * 128) * 2),
-             ("pic_mla_up_v", lambda: pic.mla_up_v(T, H, o_lat, w_uv, out, st.cuda_stream),
+             ("pic_mla_up_v", "mla_up",
+              lambda: pic.mla_up_v(T, H, o_lat, w_uv, out, st.cuda_stream),
               (T * H * (512 + 128) + H * 128 * 512) * 2)]
-    for name, fn, nbytes in cases:
+    for name, workload, fn, nbytes in cases:
         t_w = time.perf_counter()
         n_w = 0
         while n_w < args.warmup or time.perf_counter() - t_w < args.min_warmup_s:
@@ -188,8 +191,9 @@ def projections(args):
             "value": round(gbs, 1), "unit": "GB/s", "us_per_call": round(us, 3), "steps": args.steps,
             "dtype": "bf16", "data": "synthetic", "config": {"tokens": T, "heads": H},
             "algorithmic_bytes": nbytes, "flops": flops,
-            "roofline": {"bound": "hbm", "achieved": round(gbs, 1), "peak": PEAK_HBM_GBS,
-                         "unit": "GB/s", "frac": round(gbs / PEAK_HBM_GBS, 4)}}), flush=True)
+            "roofline": {"kernel": "proj_kernel", "bound": "hbm", "achieved": round(gbs, 1),
+                         "peak": PEAK_HBM_GBS, "unit": "GB/s", "frac": round(gbs / PEAK_HBM_GBS, 4),
+                         "traffic": traffic_record("proj_kernel", workload)}}), flush=True)
     return 0
 
 

@@ -85,25 +85,32 @@ __global__ __launch_bounds__(256, 1) void proj_kernel(ProjArgs p) {
   }
 
   const int n_blocks = (p.n_tokens + 31) / 32;
+  // No load or store depends on a branch: rows past the last token (and
+  // blocks past the last block) read the last token's row instead. A token's
+  // output column depends on its own activation row only, so those columns
+  // reproduce the last token's outputs bit for bit, and storing them to the
+  // last token's row rewrites it with the same bytes.
+  const int last = p.n_tokens - 1;
   // activation fragments of a block: b[s] = A[t][k0 + s*16 + g*8 .. +8]
-  auto load_a = [&](int tb, bf16x8 (&b)[8]) {
-    const int t = tb * 32 + (lane & 31);
-    const bool tv = tb < n_blocks && t < p.n_tokens;
-    const uint16_t *arow = ah + (tv ? (int64_t)t * p.a_tok : 0) + k0 + g * 8;
+  auto load_a = [&](int tb, uint4 (&b)[8]) {
+    const int t = min(tb * 32 + (lane & 31), last);
+    const uint16_t *arow = ah + (int64_t)t * p.a_tok + k0 + g * 8;
 #pragma unroll
-    for (int s = 0; s < 8; ++s)
-      b[s] = as_bf16x8(tv ? *(const uint4 *)(arow + s * 16) : make_uint4(0, 0, 0, 0));
+    for (int s = 0; s < 8; ++s) b[s] = *(const uint4 *)(arow + s * 16);
   };
-  bf16x8 b[8], bn[8];
-  load_a(part, b);
-  for (int tb = part; tb < n_blocks; tb += parts) {
-    load_a(tb + parts, bn);         // the next block's fragments load during this one
+  // rope piece of a block: 32 tokens x 128 bytes, one 16-byte piece per thread
+  auto load_rope = [&](int tb, uint4 &r) {
     if (kRope) {
-      // 32 tokens x 128 bytes of rope, one 16-byte piece per thread
-      const int tt = tb * 32 + (threadIdx.x >> 3), piece = threadIdx.x & 7;
-      if (tt < p.n_tokens)
-        *(uint4 *)(ch + (int64_t)tt * p.c_tok + 512 + piece * 8) =
-            *(const uint4 *)(ah + (int64_t)tt * p.a_tok + 128 + piece * 8);
+      const int tt = min(tb * 32 + (int)(threadIdx.x >> 3), last);
+      r = *(const uint4 *)(ah + (int64_t)tt * p.a_tok + 128 + (threadIdx.x & 7) * 8);
+    }
+  };
+  // Block tb from b / rope; once its products are issued, b / rope are
+  // refilled with block tb_next.
+  auto process = [&](int tb, uint4 (&b)[8], uint4 &rope, int tb_next) {
+    if (kRope) {
+      const int tt = min(tb * 32 + (int)(threadIdx.x >> 3), last);
+      *(uint4 *)(ch + (int64_t)tt * p.c_tok + 512 + (threadIdx.x & 7) * 8) = rope;
     }
     f32x16 acc[4];
 #pragma unroll
@@ -114,7 +121,10 @@ __global__ __launch_bounds__(256, 1) void proj_kernel(ProjArgs p) {
     for (int s = 0; s < 8; ++s)
 #pragma unroll
       for (int nt = 0; nt < 4; ++nt)
-        acc[nt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(w[nt][s], b[s], acc[nt], 0, 0, 0);
+        acc[nt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(w[nt][s], as_bf16x8(b[s]), acc[nt], 0,
+                                                          0, 0);
+    load_a(tb_next, b);
+    load_rope(tb_next, rope);
 
     // C^T tile: lane holds token t and n = nt*32 + jj*8 + g*4 + (0..3).
     // Stores: 16 bytes per lane.
@@ -145,8 +155,8 @@ __global__ __launch_bounds__(256, 1) void proj_kernel(ProjArgs p) {
         __bf16 v8[8];
 #pragma unroll
         for (int x = 0; x < 8; ++x) v8[x] = (__bf16)sum[x];
-        if (tb * 32 + tok < p.n_tokens)
-          *(uint4 *)(ch + (int64_t)(tb * 32 + tok) * p.c_tok + nb) = __builtin_bit_cast(uint4, v8);
+        *(uint4 *)(ch + (int64_t)min(tb * 32 + tok, last) * p.c_tok + nb) =
+            __builtin_bit_cast(uint4, v8);
       }
       __syncthreads();      // before the next block overwrites the partials
     } else {
@@ -167,14 +177,27 @@ __global__ __launch_bounds__(256, 1) void proj_kernel(ProjArgs p) {
       for (int j = 0; j < 8; ++j) {
         const int piece = lane + 64 * j, tok = piece >> 4, nb = (piece & 15) * 8;
         const uint4 v = *(const uint4 *)(mine + tok * kOutRow + nb);
-        if (tb * 32 + tok < p.n_tokens)
-          *(uint4 *)(ch + (int64_t)(tb * 32 + tok) * p.c_tok + n0 + nb) = v;
+        *(uint4 *)(ch + (int64_t)min(tb * 32 + tok, last) * p.c_tok + n0 + nb) = v;
       }
       __builtin_amdgcn_wave_barrier();      // reads done before the next block's writes
     }
-#pragma unroll
-    for (int st = 0; st < 8; ++st) b[st] = bn[st];
+  };
+  // Two blocks in flight: the fragments of blocks tb and tb + parts sit in
+  // b0 / b1 (two fixed register sets, so that no copy waits on a load).
+  uint4 b0[8], b1[8];
+  uint4 r0 = make_uint4(0, 0, 0, 0), r1 = make_uint4(0, 0, 0, 0);
+  load_a(part, b0);
+  load_rope(part, r0);
+  load_a(part + parts, b1);
+  load_rope(part + parts, r1);
+  const int n_mine = (n_blocks - part + parts - 1) / parts;   // blocks of this workgroup
+  int i = 0;
+  for (; i + 1 < n_mine; i += 2) {
+    const int tb = part + i * parts;
+    process(tb, b0, r0, tb + 2 * parts);
+    process(tb + parts, b1, r1, tb + 3 * parts);
   }
+  if (i < n_mine) process(part + i * parts, b0, r0, n_blocks);
 }
 
 // Workgroups per head: about one per CU over all heads, never more than
