@@ -27,8 +27,39 @@ namespace {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
 __device__ __forceinline__ bf16x8 as_bf16x8(uint4 u) { return __builtin_bit_cast(bf16x8, u); }
+
+typedef __attribute__((address_space(3))) void *lds_ptr;
+
+// Load-to-LDS copy: 16 bytes per lane from base + voff (bytes) to LDS at
+// dst + 16 * lane, through a buffer resource of `records` bytes (a lane past
+// them reads zeros and touches no memory). The compiler tracks such copies
+// per LDS array, so a read of one array does not wait for copies into
+// another.
+// base, records and dst must be uniform across the wave.
+__device__ __forceinline__ void lds_copy16(const void *base, uint32_t records, uint32_t voff,
+                                           void *dst) {
+  // (the resource is scalar: make the uniformity explicit, or the compiler
+  // loops over the distinct values it cannot rule out)
+  const uint64_t b = (uint64_t)base;
+  const uint64_t ub = (uint64_t)(uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)b) |
+                      ((uint64_t)(uint32_t)__builtin_amdgcn_readfirstlane((int)(b >> 32)) << 32);
+  const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
+      (void *)ub, (short)0, __builtin_amdgcn_readfirstlane((int)records), 0x00020000);
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (lds_ptr)dst, 16, voff, 0, 0, 0);
+}
+
+// Workgroup barrier without the memory fence of __syncthreads (whose release
+// half would wait for every copy and store in flight): this wave's LDS
+// accesses are done, and the empty asm statements keep the compiler from
+// moving memory accesses across it.
+__device__ __forceinline__ void block_barrier() {
+  asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
 
 struct ProjArgs {
   const uint16_t *a;      // activation, row (t, h) at a + t * a_tok + h * a_head
@@ -53,9 +84,22 @@ __global__ __launch_bounds__(256, 1) void proj_kernel(ProjArgs p) {
   // padded to 132 floats.
   // K = 128: each wave's bf16 output tile, [token][n] with rows padded to
   // 272 bytes, so that the stores go out as whole 256-byte row pieces.
+  // K = 128 also keeps a ring of kRing token blocks in LDS (see below).
   constexpr int kOutRow = 136;                          // bf16 per padded row
   constexpr int kRedRow = 132;
-  __shared__ __attribute__((aligned(16))) float red[kSplitK ? 4 * 32 * kRedRow : 4 * 32 * kOutRow / 2];
+  constexpr int kRing = 5;
+  constexpr int kSlotBytes = 32 * 256 + 32 * 128;       // q[., 0:128] then q[., 128:192]
+  constexpr int kAreaBytes = kSplitK ? 4 * 32 * kRedRow * 4 : 4 * 32 * kOutRow * 2;
+  __shared__ __attribute__((aligned(16))) uint4 smem[kAreaBytes / 16];
+  // the ring: one array per slot (see lds_copy16)
+  constexpr int kSlotVec = kSplitK ? 1 : kSlotBytes / 16;
+  __shared__ uint4 ring0[kSlotVec], ring1[kSlotVec], ring2[kSlotVec], ring3[kSlotVec],
+      ring4[kSlotVec];
+  static_assert(kRing == 5, "one array per slot");
+  auto ring_slot = [&](int q) -> unsigned char * {
+    return (unsigned char *)(q == 0 ? ring0 : q == 1 ? ring1 : q == 2 ? ring2 : q == 3 ? ring3 : ring4);
+  };
+  float *red = (float *)smem;
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int parts = p.parts;
@@ -75,15 +119,13 @@ __global__ __launch_bounds__(256, 1) void proj_kernel(ProjArgs p) {
   uint16_t *ch = p.c + (int64_t)h * p.c_head;
 
   // weight fragments: w[nt][s] = W[n0 + nt*32 + (lane&31)][k0 + s*16 + g*8 .. +8]
-  bf16x8 w[4][8];
-  {
-    const uint16_t *wh = p.w + (int64_t)h * N * K + (int64_t)(n0 + (lane & 31)) * K + k0 + g * 8;
-#pragma unroll
-    for (int nt = 0; nt < 4; ++nt)
-#pragma unroll
-      for (int s = 0; s < 8; ++s) w[nt][s] = as_bf16x8(*(const uint4 *)(wh + nt * 32 * K + s * 16));
-  }
-
+  // In that layout one load instruction touches 32 rows (32 bytes of each),
+  // which the L1 serves a line at a time. The slice is therefore read in
+  // whole 128-byte lines instead (instruction i of row group nt: rows
+  // nt*32 + 4i + lane/16, 16 bytes each of the 256-byte k range) and
+  // rearranged through a wave-private LDS area, rows padded to 272 bytes so
+  // that neither side conflicts on the banks. The area is the one the
+  // per-block outputs use later.
   const int n_blocks = (p.n_tokens + 31) / 32;
   // No load or store depends on a branch: rows past the last token (and
   // blocks past the last block) read the last token's row instead. A token's
@@ -91,28 +133,86 @@ __global__ __launch_bounds__(256, 1) void proj_kernel(ProjArgs p) {
   // reproduce the last token's outputs bit for bit, and storing them to the
   // last token's row rewrites it with the same bytes.
   const int last = p.n_tokens - 1;
-  // activation fragments of a block: b[s] = A[t][k0 + s*16 + g*8 .. +8]
-  auto load_a = [&](int tb, uint4 (&b)[8]) {
-    const int t = min(tb * 32 + (lane & 31), last);
-    const uint16_t *arow = ah + (int64_t)t * p.a_tok + k0 + g * 8;
+  const int n_mine = (n_blocks - part + parts - 1) / parts;   // blocks of this workgroup
+
+  constexpr int kRow = 136;                              // bf16 per padded LDS row
+  static_assert(kAreaBytes >= 4 * 32 * kRow * 2, "transpose area");
+  u32x4 raw[4][8];
+  {
+    const uint16_t *wh = p.w + (int64_t)h * N * K + (int64_t)(n0 + (lane >> 4)) * K + k0 +
+                         (lane & 15) * 8;
 #pragma unroll
-    for (int s = 0; s < 8; ++s) b[s] = *(const uint4 *)(arow + s * 16);
-  };
-  // rope piece of a block: 32 tokens x 128 bytes, one 16-byte piece per thread
-  auto load_rope = [&](int tb, uint4 &r) {
-    if (kRope) {
-      const int tt = min(tb * 32 + (int)(threadIdx.x >> 3), last);
-      r = *(const uint4 *)(ah + (int64_t)tt * p.a_tok + 128 + (threadIdx.x & 7) * 8);
+    for (int nt = 0; nt < 4; ++nt)
+#pragma unroll
+      for (int i = 0; i < 8; ++i) raw[nt][i] = *(const u32x4 *)(wh + (nt * 32 + 4 * i) * K);
+  }
+
+  // K = 128: the activation blocks stream through a ring of kRing LDS slots
+  // by load-to-LDS copies, kRing - 1 blocks ahead, shared by the four waves
+  // (which all need the same 32 x 128 slice). A slot holds the block's
+  // q[., 0:128] rows (256 bytes, the 16-byte chunk c of row r at position
+  // c ^ (r & 15), so that the fragment reads below hit 16 distinct bank
+  // groups) and its q[., 128:192] rope rows. Each wave copies its quarter
+  // of a block with three 1 KB copies (whole 128-byte lines), so its vector
+  // memory operations per block are fixed: 3 copies, then 1 + 8 stores.
+  // The wait for block i's copies therefore counts the operations issued
+  // after them: 3 (kRing - 2) + 9 min(i, kRing - 1). A refill past the last
+  // block is still issued, with an empty buffer range (no memory touched),
+  // to keep that count.
+  auto issue_block = [&](int tb, unsigned char *dst) {
+    const bool real = tb < n_blocks;
+    const int row0 = min(tb, n_blocks - 1) * 32;
+    const uint16_t *base = ah + (int64_t)row0 * p.a_tok;
+    const uint32_t tok_bytes = (uint32_t)p.a_tok * 2;
+    const uint32_t records = real ? 0xFFFFFFFFu : 0u;
+#pragma unroll
+    for (int jj = 0; jj < 2; ++jj) {
+      const int j = 2 * wave + jj, r = 4 * j + (lane >> 4);
+      const int c = (lane & 15) ^ (r & 15);
+      lds_copy16(base, records, (uint32_t)(min(row0 + r, last) - row0) * tok_bytes + c * 16,
+                 dst + j * 1024);
     }
+    const int r = 8 * wave + (lane >> 3);
+    lds_copy16(base, records,
+               (uint32_t)(min(row0 + r, last) - row0) * tok_bytes + 256 + (lane & 7) * 16,
+               dst + 8192 + wave * 1024);
   };
-  // Block tb from b / rope; once its products are issued, b / rope are
-  // refilled with block tb_next.
-  auto process = [&](int tb, uint4 (&b)[8], uint4 &rope, int tb_next) {
-    if (kRope) {
-      const int tt = min(tb * 32 + (int)(threadIdx.x >> 3), last);
-      *(uint4 *)(ch + (int64_t)tt * p.c_tok + 512 + (threadIdx.x & 7) * 8) = rope;
+  if constexpr (!kSplitK) {
+    asm volatile("" ::: "memory");
+#pragma unroll
+    for (int q = 0; q < kRing - 1; ++q) issue_block(part + q * parts, ring_slot(q));
+    asm volatile("" ::: "memory");
+  }
+
+  // weight fragments: w[nt][s] = W[n0 + nt*32 + (lane&31)][k0 + s*16 + g*8 .. +8]
+  // In that layout one load instruction touches 32 rows (32 bytes of each),
+  // which the L1 serves a line at a time. The slice is therefore read in
+  // whole 128-byte lines instead (instruction i of row group nt: rows
+  // nt*32 + 4i + lane/16, 16 bytes each of the 256-byte k range, in raw) and
+  // rearranged through a wave-private LDS area, rows padded to 272 bytes so
+  // that neither side conflicts on the banks. The area is the one the
+  // per-block outputs use later.
+  bf16x8 w[4][8];
+  {
+    uint16_t *tw = (uint16_t *)red + wave * 32 * kRow;
+#pragma unroll
+    for (int nt = 0; nt < 4; ++nt) {
+#pragma unroll
+      for (int i = 0; i < 8; ++i)
+        *(u32x4 *)(tw + (4 * i + (lane >> 4)) * kRow + (lane & 15) * 8) = raw[nt][i];
+      // (a wave's LDS accesses complete in order: the reads see the writes,
+      // and the next group's writes follow these reads)
+#pragma unroll
+      for (int st = 0; st < 8; ++st)
+        w[nt][st] = as_bf16x8(*(const uint4 *)(tw + (lane & 31) * kRow + st * 16 + g * 8));
     }
-    f32x16 acc[4];
+  }
+  // K = 512: the partial tiles of block 0 overlap other waves' areas
+  if (kSplitK) __syncthreads();
+
+  // The products of one block: C^T tile, lane holds token t and
+  // n = nt*32 + jj*8 + g*4 + (0..3).
+  auto products = [&](const uint4 (&b)[8], f32x16 (&acc)[4]) {
 #pragma unroll
     for (int nt = 0; nt < 4; ++nt)
 #pragma unroll
@@ -123,45 +223,38 @@ __global__ __launch_bounds__(256, 1) void proj_kernel(ProjArgs p) {
       for (int nt = 0; nt < 4; ++nt)
         acc[nt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(w[nt][s], as_bf16x8(b[s]), acc[nt], 0,
                                                           0, 0);
-    load_a(tb_next, b);
-    load_rope(tb_next, rope);
+  };
 
-    // C^T tile: lane holds token t and n = nt*32 + jj*8 + g*4 + (0..3).
-    // Stores: 16 bytes per lane.
-    if (kSplitK) {
-      // partial tiles to LDS as [wave][token][n]; then every thread adds the
-      // four partials of 8 consecutive n of one token (2 pieces per thread,
-      // consecutive lanes on consecutive tokens)
-      float *mine = red + wave * 32 * kRedRow;
-#pragma unroll
-      for (int nt = 0; nt < 4; ++nt)
-#pragma unroll
-        for (int jj = 0; jj < 4; ++jj)
-          *(float4 *)(mine + (lane & 31) * kRedRow + nt * 32 + jj * 8 + g * 4) =
-              make_float4(acc[nt][jj * 4], acc[nt][jj * 4 + 1], acc[nt][jj * 4 + 2],
-                          acc[nt][jj * 4 + 3]);
-      __syncthreads();
-#pragma unroll
-      for (int j = 0; j < 2; ++j) {
-        const int piece = threadIdx.x + 256 * j, tok = piece & 31, nb = (piece >> 5) * 8;
-        float sum[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          const float4 a = *(const float4 *)(red + (q * 32 + tok) * kRedRow + nb);
-          const float4 b = *(const float4 *)(red + (q * 32 + tok) * kRedRow + nb + 4);
-          sum[0] += a.x, sum[1] += a.y, sum[2] += a.z, sum[3] += a.w;
-          sum[4] += b.x, sum[5] += b.y, sum[6] += b.z, sum[7] += b.w;
-        }
-        __bf16 v8[8];
-#pragma unroll
-        for (int x = 0; x < 8; ++x) v8[x] = (__bf16)sum[x];
-        *(uint4 *)(ch + (int64_t)min(tb * 32 + tok, last) * p.c_tok + nb) =
-            __builtin_bit_cast(uint4, v8);
+  if constexpr (!kSplitK) {
+    // this wave's tile to LDS as bf16 [token][n], then out as row pieces
+    // (16 bytes per lane, 256 bytes per row)
+    uint16_t *mine = (uint16_t *)red + wave * 32 * kOutRow;
+    auto step = [&](int i, const unsigned char *slot, unsigned char *refill) {
+      const int tb = part + i * parts;
+      switch (min(i, kRing - 1)) {       // block i's copies (this wave's) have landed
+        case 0: asm volatile("s_waitcnt vmcnt(9)" ::: "memory"); break;
+        case 1: asm volatile("s_waitcnt vmcnt(18)" ::: "memory"); break;
+        case 2: asm volatile("s_waitcnt vmcnt(27)" ::: "memory"); break;
+        case 3: asm volatile("s_waitcnt vmcnt(36)" ::: "memory"); break;
+        default: asm volatile("s_waitcnt vmcnt(45)" ::: "memory"); break;
       }
-      __syncthreads();      // before the next block overwrites the partials
-    } else {
-      // this wave's tile to LDS as bf16 [token][n], then row pieces out
-      uint16_t *mine = (uint16_t *)red + wave * 32 * kOutRow;
+      block_barrier();                   // every wave's copies landed; block i-1's slot is free
+      issue_block(tb + (kRing - 1) * parts, refill);
+      asm volatile("" ::: "memory");
+      uint4 b[8];
+      {
+        const int t = lane & 31;
+#pragma unroll
+        for (int s = 0; s < 8; ++s)
+          b[s] = *(const uint4 *)(slot + (t * 16 + ((2 * s + g) ^ (t & 15))) * 16);
+      }
+      {
+        const uint4 rope = *(const uint4 *)(slot + 8192 + threadIdx.x * 16);
+        const int tt = min(tb * 32 + (int)(threadIdx.x >> 3), last);
+        *(uint4 *)(ch + (int64_t)tt * p.c_tok + 512 + (threadIdx.x & 7) * 8) = rope;
+      }
+      f32x16 acc[4];
+      products(b, acc);
 #pragma unroll
       for (int nt = 0; nt < 4; ++nt)
 #pragma unroll
@@ -179,25 +272,80 @@ __global__ __launch_bounds__(256, 1) void proj_kernel(ProjArgs p) {
         const uint4 v = *(const uint4 *)(mine + tok * kOutRow + nb);
         *(uint4 *)(ch + (int64_t)min(tb * 32 + tok, last) * p.c_tok + n0 + nb) = v;
       }
-      __builtin_amdgcn_wave_barrier();      // reads done before the next block's writes
+      __builtin_amdgcn_wave_barrier();   // reads done before the next block's writes
+    };
+    // unrolled by the ring size, so that every slot is a fixed array
+    for (int i0 = 0; i0 < n_mine; i0 += kRing) {
+      step(i0, ring_slot(0), ring_slot(4));
+      if (i0 + 1 >= n_mine) break;
+      step(i0 + 1, ring_slot(1), ring_slot(0));
+      if (i0 + 2 >= n_mine) break;
+      step(i0 + 2, ring_slot(2), ring_slot(1));
+      if (i0 + 3 >= n_mine) break;
+      step(i0 + 3, ring_slot(3), ring_slot(2));
+      if (i0 + 4 >= n_mine) break;
+      step(i0 + 4, ring_slot(4), ring_slot(3));
     }
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");   // no copy outlives the workgroup
+    return;
+  }
+
+  // K = 512: activation fragments in registers, two blocks in flight: the
+  // fragments of blocks tb and tb + parts sit in b0 / b1 (two fixed register
+  // sets, so that no copy waits on a load); a set is refilled with the block
+  // after next once its block's products are issued.
+  // activation fragments of a block: b[s] = A[t][k0 + s*16 + g*8 .. +8]
+  auto load_a = [&](int tb, uint4 (&b)[8]) {
+    const int t = min(tb * 32 + (lane & 31), last);
+    const uint16_t *arow = ah + (int64_t)t * p.a_tok + k0 + g * 8;
+#pragma unroll
+    for (int s = 0; s < 8; ++s) b[s] = *(const uint4 *)(arow + s * 16);
   };
-  // Two blocks in flight: the fragments of blocks tb and tb + parts sit in
-  // b0 / b1 (two fixed register sets, so that no copy waits on a load).
+  auto process = [&](int tb, uint4 (&b)[8], int tb_next) {
+    f32x16 acc[4];
+    products(b, acc);
+    load_a(tb_next, b);
+    // partial tiles to LDS as [wave][token][n]; then every thread adds the
+    // four partials of 8 consecutive n of one token (2 pieces per thread,
+    // consecutive lanes on consecutive tokens)
+    float *mine = red + wave * 32 * kRedRow;
+#pragma unroll
+    for (int nt = 0; nt < 4; ++nt)
+#pragma unroll
+      for (int jj = 0; jj < 4; ++jj)
+        *(float4 *)(mine + (lane & 31) * kRedRow + nt * 32 + jj * 8 + g * 4) =
+            make_float4(acc[nt][jj * 4], acc[nt][jj * 4 + 1], acc[nt][jj * 4 + 2],
+                        acc[nt][jj * 4 + 3]);
+    __syncthreads();
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      const int piece = threadIdx.x + 256 * j, tok = piece & 31, nb = (piece >> 5) * 8;
+      float sum[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const float4 a = *(const float4 *)(red + (q * 32 + tok) * kRedRow + nb);
+        const float4 b = *(const float4 *)(red + (q * 32 + tok) * kRedRow + nb + 4);
+        sum[0] += a.x, sum[1] += a.y, sum[2] += a.z, sum[3] += a.w;
+        sum[4] += b.x, sum[5] += b.y, sum[6] += b.z, sum[7] += b.w;
+      }
+      __bf16 v8[8];
+#pragma unroll
+      for (int x = 0; x < 8; ++x) v8[x] = (__bf16)sum[x];
+      *(uint4 *)(ch + (int64_t)min(tb * 32 + tok, last) * p.c_tok + nb) =
+          __builtin_bit_cast(uint4, v8);
+    }
+    __syncthreads();      // before the next block overwrites the partials
+  };
   uint4 b0[8], b1[8];
-  uint4 r0 = make_uint4(0, 0, 0, 0), r1 = make_uint4(0, 0, 0, 0);
   load_a(part, b0);
-  load_rope(part, r0);
   load_a(part + parts, b1);
-  load_rope(part + parts, r1);
-  const int n_mine = (n_blocks - part + parts - 1) / parts;   // blocks of this workgroup
   int i = 0;
   for (; i + 1 < n_mine; i += 2) {
     const int tb = part + i * parts;
-    process(tb, b0, r0, tb + 2 * parts);
-    process(tb + parts, b1, r1, tb + 3 * parts);
+    process(tb, b0, tb + 2 * parts);
+    process(tb + parts, b1, tb + 3 * parts);
   }
-  if (i < n_mine) process(part + i * parts, b0, r0, n_blocks);
+  if (i < n_mine) process(part + i * parts, b0, n_blocks);
 }
 
 // Workgroups per head: about one per CU over all heads, never more than

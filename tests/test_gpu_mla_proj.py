@@ -42,7 +42,7 @@ def check_bound(gpu, ref, absum, K, label):
     assert np.all(err <= lim), f"{label}: {int(np.sum(err > lim))} elements outside the bound"
 
 
-@pytest.mark.parametrize("T,H", [(37, 3), (1, 16), (2048, 16), (1541, 16), (300, 64)])
+@pytest.mark.parametrize("T,H", [(37, 3), (1, 16), (2048, 16), (1541, 16), (300, 64), (1000, 64)])
 def test_absorb_q(T, H):
     rng = np.random.default_rng(1000 + T + H)
     q = bf16(rng, (T, H, D_NOPE + D_ROPE))
@@ -59,7 +59,7 @@ def test_absorb_q(T, H):
     assert np.array_equal(got_bits[:, :, R_LAT:], q[:, :, D_NOPE:]), "rope part not copied exactly"
 
 
-@pytest.mark.parametrize("T,H", [(37, 3), (1, 16), (130, 2), (2048, 16), (1541, 16), (300, 64)])
+@pytest.mark.parametrize("T,H", [(37, 3), (1, 16), (130, 2), (2048, 16), (1541, 16), (300, 64), (1000, 64)])
 def test_up_v(T, H):
     rng = np.random.default_rng(2000 + T + H)
     o = bf16(rng, (T, H, R_LAT))
