@@ -314,8 +314,10 @@ __global__ __launch_bounds__(256) void link_valu_kernel(LinkParams p) {
   const int nrows = R.lq * group;
   const int row0 = rb * kValuRows;
   if (row0 >= nrows) return;
-  const int t_begin = (int)((int64_t)R.tiles * split / p.num_splits);
-  const int t_end = (int)((int64_t)R.tiles * (split + 1) / p.num_splits);
+  // the block's key range ends at the last own key its last row sees
+  const int vis = visible_tiles(R, min(nrows - 1, row0 + kValuRows - 1) / group);
+  const int t_begin = (int)((int64_t)vis * split / p.num_splits);
+  const int t_end = (int)((int64_t)vis * (split + 1) / p.num_splits);
 
   const T *__restrict__ q = (const T *)p.q;
 

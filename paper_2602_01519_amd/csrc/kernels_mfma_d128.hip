@@ -369,8 +369,11 @@ __global__ __launch_bounds__(kWaves * 64, 8 / kWaves) void link_mfma_d128_kernel
   const int nrows = R.lq * group;
   const int row0 = rb * kRows;
   if (row0 >= nrows) return;
-  const int t_begin = (int)((int64_t)R.tiles * split / p.num_splits);
-  const int t_end = (int)((int64_t)R.tiles * (split + 1) / p.num_splits);
+  // Own tiles past the causal limit of the block's last row hold no key any
+  // of its rows sees: the block's key range ends at the last visible one.
+  const int vis = visible_tiles(R, min(nrows - 1, row0 + kRows - 1) / group);
+  const int t_begin = (int)((int64_t)vis * split / p.num_splits);
+  const int t_end = (int)((int64_t)vis * (split + 1) / p.num_splits);
 
   // This lane's row. A wave whose 32 rows are all past the request's rows
   // (short questions: a 16-token question fills 64 of the 256 rows) only

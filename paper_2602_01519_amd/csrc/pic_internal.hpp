@@ -57,6 +57,17 @@ struct ReqEntry {
   int32_t tiles;          // doc_tiles + ceil(ls / kTile)
 };
 
+// Tiles of a request that hold a key visible to query token q_last or any
+// earlier one: every document tile, then the own tiles up to the one holding
+// own key q_last + ls - lq (the causal limit, bottom-right aligned).
+__host__ __device__ __forceinline__ int visible_tiles(const ReqEntry &r, int q_last) {
+  const int own_last = q_last + r.ls - r.lq;
+  return own_last >= 0 ? (r.doc_tiles + own_last / kTile + 1 < r.tiles
+                              ? r.doc_tiles + own_last / kTile + 1
+                              : r.tiles)
+                       : r.doc_tiles;
+}
+
 struct LinkParams {
   const LinkEntry *links;
   const ReqEntry *reqs;
