@@ -300,17 +300,53 @@ __device__ __forceinline__ void copy_rows_lds(const char *src, int64_t src_row_b
   }
 }
 
-template <typename T, bool MLA>
-__global__ __launch_bounds__(256) void link_valu_kernel(LinkParams p) {
+// kSmall: the call's tables come by value in `t` (a kernel argument) rather
+// than from device memory, and own-KV tiles are read straight from the
+// caller's token-major k_self / v_self: no prologue kernel before.
+// Transposes token-major value rows into LDS: element e of row r (src +
+// r * src_stride + e) lands at dst[e * dst_stride + r], for rows 0 .. rows-1
+// and e < d_v. Each thread loads the 16-byte units of 4 (row, unit) pairs
+// before storing any, as copy_rows_lds does.
+template <typename T>
+__device__ __forceinline__ void gather_vt_lds(const T *src, int64_t src_stride, int rows, int d_v,
+                                              T *dst, int dst_stride) {
+  constexpr int kPer = 16 / sizeof(T);
+  const int units = d_v / kPer;
+  const int n = rows * units;
+  for (int base = threadIdx.x; base < n; base += 4 * blockDim.x) {
+    uint4 v[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int i = min(base + u * (int)blockDim.x, n - 1);
+      const int r = i / units, c = i - r * units;
+      v[u] = *(const uint4 *)(src + r * src_stride + c * kPer);
+    }
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int i = base + u * blockDim.x;
+      if (i < n) {
+        const int r = i / units, c = i - r * units;
+        T x[kPer];
+        __builtin_memcpy(x, &v[u], 16);
+#pragma unroll
+        for (int k = 0; k < kPer; ++k) dst[(c * kPer + k) * dst_stride + r] = x[k];
+      }
+    }
+  }
+}
+
+template <typename T, bool MLA, bool kSmall>
+__device__ __forceinline__ void valu_body(const LinkParams &p, const SmallTabs &t) {
   extern __shared__ float smem[];
   const int d_k = p.d_k, d_v = p.d_v, group = p.group;
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  auto link = [&](int i) -> LinkEntry { return kSmall ? t.links[i] : p.links[i]; };
 
   const int g = blockIdx.x / p.nrb, rb = blockIdx.x % p.nrb;
   const int split = blockIdx.y;
-  const int req_i = p.order[g / p.n_kv_heads];
+  const int req_i = kSmall ? t.order[g / p.n_kv_heads] : p.order[g / p.n_kv_heads];
   const int kvh = g % p.n_kv_heads;
-  const ReqEntry R = p.reqs[req_i];
+  const ReqEntry R = kSmall ? t.reqs[req_i] : p.reqs[req_i];
   const int nrows = R.lq * group;
   const int row0 = rb * kValuRows;
   if (row0 >= nrows) return;
@@ -376,23 +412,35 @@ __global__ __launch_bounds__(256) void link_valu_kernel(LinkParams p) {
   for (int t = t_begin; t < t_end; ++t) {
     const bool own = t >= R.doc_tiles;
     __syncthreads();
-    while (p.links[R.link0 + li].tile0 + (p.links[R.link0 + li].len + kTile - 1) / kTile <= t) ++li;
-    const LinkEntry E = p.links[R.link0 + li];
+    while (link(R.link0 + li).tile0 + (link(R.link0 + li).len + kTile - 1) / kTile <= t) ++li;
+    const LinkEntry E = link(R.link0 + li);
     const int tt = t - E.tile0;
     const int nvalid = min(kTile, E.len - tt * kTile);
     const int j0 = tt * kTile;          // key index within the link (own: within the own KV)
     const int tok = E.tok0 + j0;        // ... within the request's linked rows
-    // 64 consecutive key rows (the slot's padding rows are zeros)
-    // K rows (d_k elements, whole 16-byte units) and V^T rows (64 keys)
-    copy_rows_lds((const char *)key_row<T>(E, MLA ? 0 : kvh, tt * kTile, d_k),
-                  (int64_t)d_k * sizeof(T), kTile, kwords / 4, ks, kstride);
-    // V^T: the tile's two 32-token panels, each d_v rows of 32 keys
-    if (!MLA)
+    if (kSmall && own) {
+      // own keys j0 .. j0 + nvalid - 1 from the caller's token-major rows
+      // (rows past nvalid stay unread: they are masked below)
+      const int kv_heads = MLA ? 1 : p.n_kv_heads;
+      const T *krow0 = (const T *)p.k_self + ((int64_t)(R.s0 + j0) * kv_heads + kvh) * d_k;
+      copy_rows_lds((const char *)krow0, (int64_t)kv_heads * d_k * sizeof(T), nvalid, kwords / 4,
+                    ks, kstride);
+      if (!MLA)
+        gather_vt_lds<T>((const T *)p.v_self + ((int64_t)(R.s0 + j0) * kv_heads + kvh) * d_v,
+                         (int64_t)kv_heads * d_v, nvalid, d_v, (T *)vts, vstride * EPW);
+    } else {
+      // 64 consecutive key rows (the slot's padding rows are zeros)
+      // K rows (d_k elements, whole 16-byte units) and V^T rows (64 keys)
+      copy_rows_lds((const char *)key_row<T>(E, MLA ? 0 : kvh, tt * kTile, d_k),
+                    (int64_t)d_k * sizeof(T), kTile, kwords / 4, ks, kstride);
+      // V^T: the tile's two 32-token panels, each d_v rows of 32 keys
+      if (!MLA)
 #pragma unroll
-      for (int hp = 0; hp < kTile / kPanel; ++hp)
-        copy_rows_lds((const char *)value_at<T>(E, kvh, 0, tt * kTile + hp * kPanel, d_v),
-                      (int64_t)kPanel * sizeof(T), d_v, kPanel * (int)sizeof(T) / 16,
-                      vts + hp * (kPanel / EPW), vstride);
+        for (int hp = 0; hp < kTile / kPanel; ++hp)
+          copy_rows_lds((const char *)value_at<T>(E, kvh, 0, tt * kTile + hp * kPanel, d_v),
+                        (int64_t)kPanel * sizeof(T), d_v, kPanel * (int)sizeof(T) / 16,
+                        vts + hp * (kPanel / EPW), vstride);
+    }
     __syncthreads();
 
     // scores: lane = key
@@ -518,6 +566,16 @@ __global__ __launch_bounds__(256) void link_valu_kernel(LinkParams p) {
   }
 }
 
+template <typename T, bool MLA>
+__global__ __launch_bounds__(256) void link_valu_kernel(LinkParams p) {
+  valu_body<T, MLA, false>(p, SmallTabs{});
+}
+
+template <typename T, bool MLA>
+__global__ __launch_bounds__(256) void link_small_kernel(LinkParams p, SmallTabs t) {
+  valu_body<T, MLA, true>(p, t);
+}
+
 // ---------------------------------------------------------------------------
 // Split-K combine: one wave per output row, lane j covering value dims
 // 2j, 2j+1 of each of the row's kChunks 128-wide chunks (8-byte loads: a
@@ -625,7 +683,28 @@ hipError_t launch_valu_t(const LinkParams &p, hipStream_t st) {
   return hipGetLastError();
 }
 
+template <typename T, bool MLA>
+hipError_t launch_small_t(const LinkParams &p, const SmallTabs &t, hipStream_t st) {
+  const size_t lds = valu_lds_bytes(sizeof(T), MLA, p.d_k, p.d_v);
+  hipError_t e = hipFuncSetAttribute((const void *)link_small_kernel<T, MLA>,
+                                     hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+  if (e != hipSuccess) return e;
+  dim3 grid(p.n_groups * p.nrb, p.num_splits);
+  hipLaunchKernelGGL((link_small_kernel<T, MLA>), grid, dim3(256), lds, st, p, t);
+  return hipGetLastError();
+}
+
 }  // namespace
+
+hipError_t launch_link_small(const LinkParams &p, const SmallTabs &t, int dtype, int mla,
+                             hipStream_t st, const char **name) {
+  if (dtype == 0) {
+    *name = mla ? "link_small_kernel<float,MLA>" : "link_small_kernel<float,GQA>";
+    return mla ? launch_small_t<float, true>(p, t, st) : launch_small_t<float, false>(p, t, st);
+  }
+  *name = mla ? "link_small_kernel<bf16,MLA>" : "link_small_kernel<bf16,GQA>";
+  return mla ? launch_small_t<uint16_t, true>(p, t, st) : launch_small_t<uint16_t, false>(p, t, st);
+}
 
 int valu_rows_per_block() { return kValuRows; }
 

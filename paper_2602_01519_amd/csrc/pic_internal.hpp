@@ -191,4 +191,16 @@ hipError_t static_scratch(void **out);
 // Log-sum-exp merge of split partials into out / lse.
 hipError_t launch_combine(const LinkParams &p, int dtype, hipStream_t st);
 
+// Tables of a small generic-kernel call, passed by value as a kernel
+// argument: the call then needs neither the table copy nor the own-KV
+// layout of the prologue (see link_small_kernel).
+constexpr int kSmallLinks = 32, kSmallReqs = 8;
+struct SmallTabs {
+  LinkEntry links[kSmallLinks];
+  ReqEntry reqs[kSmallReqs];
+  int32_t order[kSmallReqs];
+};
+hipError_t launch_link_small(const LinkParams &p, const SmallTabs &t, int dtype, int mla,
+                             hipStream_t st, const char **name);
+
 }  // namespace pic
