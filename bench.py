@@ -47,6 +47,7 @@ KERNEL_SOURCES = {
     "link_decode_d128_kernel": "kernels_decode_d128.hip",
     "link_mla_kernel": "kernels_mla.hip",
     "link_valu_kernel": "kernels_generic.hip",
+    "link_small_kernel": "kernels_generic.hip",
     "proj_kernel": "kernels_mla_proj.hip",
 }
 PROFILES = os.path.join(ROOT, "profiles")
