@@ -534,3 +534,36 @@ def test_two_streams_in_flight(decode):
                 ref_b, rl_b, label="stream B")
     finally:
         dw.close()
+
+
+# Generic-kernel calls whose tables fit a kernel argument (at most 32 links,
+# own-KV entries included, and 8 requests) run without the prologue: the
+# kernel reads its tables from its arguments and its own tiles straight from
+# k_self / v_self. Each case sits on one side of those limits, so both forms
+# are checked at the boundary.
+def _table_limit_case(dtype, batch, extra_link, decode=False):
+    n = batch
+    cfg = W.small_config(f"table_limit_{'f32' if dtype == W.F32 else 'bf16'}_{batch}_{extra_link}",
+                         dtype=dtype, d_k=64, chunk_lens=(70, 64, 1, 130, 9, 200), batch=n,
+                         q_len=tuple((1 if decode else (5, 1, 9, 33)[r % 4]) for r in range(n)),
+                         self_len=tuple((66, 1, 9, 40)[r % 4] for r in range(n)),
+                         links=(0, 0), seed=23, decode=decode)
+    # three document links per request (plus its own-KV entry): 8 requests
+    # make 32 table links, one more link makes 33
+    links = [[(r + j) % 6 for j in range(3)] for r in range(n)]
+    if extra_link:
+        links[-1].append(5)
+    return cfg, links
+
+
+@pytest.mark.parametrize("dtype", [W.F32, W.BF16])
+@pytest.mark.parametrize("batch,extra_link", [(8, False), (8, True), (9, False), (1, False)])
+def test_small_call_table_limits(dtype, batch, extra_link):
+    cfg, links = _table_limit_case(dtype, batch, extra_link)
+    run_and_check(cfg, links=links)
+
+
+@pytest.mark.parametrize("num_splits", [0, 1, 5])
+def test_small_call_decode(num_splits):
+    cfg, links = _table_limit_case(W.F32, 8, False, decode=True)
+    run_and_check(cfg, decode=True, num_splits=num_splits, links=links)
