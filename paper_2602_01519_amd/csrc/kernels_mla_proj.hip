@@ -183,6 +183,19 @@ __global__ __launch_bounds__(256, 1) void proj_kernel(ProjArgs p) {
     for (int q = 0; q < kRing - 1; ++q) issue_block(part + q * parts, ring_slot(q));
     asm volatile("" ::: "memory");
   }
+  // K = 512: the first two blocks' activation fragments (b[s] = A[t][k0 +
+  // s*16 + g*8 .. +8]) are loaded beside the weights, not after them
+  auto load_a = [&](int tb, uint4 (&b)[8]) {
+    const int t = min(tb * 32 + (lane & 31), last);
+    const uint16_t *arow = ah + (int64_t)t * p.a_tok + k0 + g * 8;
+#pragma unroll
+    for (int s = 0; s < 8; ++s) b[s] = *(const uint4 *)(arow + s * 16);
+  };
+  uint4 b0[8], b1[8];
+  if constexpr (kSplitK) {
+    load_a(part, b0);
+    load_a(part + parts, b1);
+  }
 
   // weight fragments: w[nt][s] = W[n0 + nt*32 + (lane&31)][k0 + s*16 + g*8 .. +8]
   // In that layout one load instruction touches 32 rows (32 bytes of each),
@@ -292,15 +305,9 @@ __global__ __launch_bounds__(256, 1) void proj_kernel(ProjArgs p) {
 
   // K = 512: activation fragments in registers, two blocks in flight: the
   // fragments of blocks tb and tb + parts sit in b0 / b1 (two fixed register
-  // sets, so that no copy waits on a load); a set is refilled with the block
-  // after next once its block's products are issued.
-  // activation fragments of a block: b[s] = A[t][k0 + s*16 + g*8 .. +8]
-  auto load_a = [&](int tb, uint4 (&b)[8]) {
-    const int t = min(tb * 32 + (lane & 31), last);
-    const uint16_t *arow = ah + (int64_t)t * p.a_tok + k0 + g * 8;
-#pragma unroll
-    for (int s = 0; s < 8; ++s) b[s] = *(const uint4 *)(arow + s * 16);
-  };
+  // sets, so that no copy waits on a load; the first two were issued beside
+  // the weight loads); a set is refilled with the block after next once its
+  // block's products are issued.
   auto process = [&](int tb, uint4 (&b)[8], int tb_next) {
     f32x16 acc[4];
     products(b, acc);
@@ -336,9 +343,6 @@ __global__ __launch_bounds__(256, 1) void proj_kernel(ProjArgs p) {
     }
     __syncthreads();      // before the next block overwrites the partials
   };
-  uint4 b0[8], b1[8];
-  load_a(part, b0);
-  load_a(part + parts, b1);
   int i = 0;
   for (; i + 1 < n_mine; i += 2) {
     const int tb = part + i * parts;
