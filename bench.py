@@ -325,6 +325,9 @@ def main(argv=None):
     ap.add_argument("--config", default="long_rag",
                     help="workload: long_rag (default), tiny_f32, llama_prefill, decode, mla, "
                          "skinny_rag")
+    ap.add_argument("--flush-mib", type=int, default=0,
+                    help="also time K steps each after writing this many MiB of scratch "
+                         "(cold last-level cache); reported as step_ms_flushed")
     ap.add_argument("--cpu-budget", type=float, default=15.0,
                     help="seconds of oracle time for the CPU baseline (0 = skip)")
     ap.add_argument("--calib", choices=["read", "write"],
@@ -405,6 +408,26 @@ def main(argv=None):
                  "p90": round(float(np.percentile(per_step, 90)), 5),
                  "steps": args.steps,
                  "how": "second pass of K steps, one event per step boundary"}
+    flushed = None
+    if args.flush_mib > 0:
+        # Cold-cache steps: before each step, writing a scratch buffer larger
+        # than the 256 MB last-level cache evicts the step's inputs; only the
+        # call is timed (events right around it).
+        scratch = torch.empty(args.flush_mib << 18, dtype=torch.float32, device="cuda")
+        cold = []
+        for _ in range(args.steps):
+            scratch.fill_(1.0)
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            dw.run()
+            e1.record(stream)
+            torch.cuda.synchronize()
+            cold.append(e0.elapsed_time(e1))
+        cold = np.array(cold)
+        flushed = {"flush_mib": args.flush_mib, "p10": round(float(np.percentile(cold, 10)), 5),
+                   "median": round(float(np.median(cold)), 5),
+                   "p90": round(float(np.percentile(cold, 90)), 5), "steps": args.steps}
+        del scratch
 
     flops, nbytes = algorithmic(cfg, wl)
     tflops = flops / (step_ms * 1e-3) / 1e12
@@ -448,6 +471,7 @@ def main(argv=None):
         "warmup_steps_run": warm_run,
         "ms_per_step": round(step_ms, 5),
         "step_ms_dist": step_dist,
+        **({"step_ms_flushed": flushed} if flushed else {}),
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
