@@ -567,3 +567,39 @@ def test_small_call_table_limits(dtype, batch, extra_link):
 def test_small_call_decode(num_splits):
     cfg, links = _table_limit_case(W.F32, 8, False, decode=True)
     run_and_check(cfg, decode=True, num_splits=num_splits, links=links)
+
+
+def test_request_order_search_keeps_results():
+    """A prefill batch whose row blocks take several rounds of each XCD's CUs
+    (40 requests x 8 kv heads, requests of very different lengths), so the
+    planner reorders the requests by simulating the dispatch. Every request
+    is checked against the oracle; a second call on the same store (which
+    reuses the order it kept for these request shapes) must give the same
+    bytes."""
+    n = 40
+    cfg = W.small_config("order_search", d_k=128, n_q_heads=32, n_kv_heads=8,
+                         chunk_lens=tuple(64 * (1 + i % 3) for i in range(12)), batch=n,
+                         q_len=tuple((64, 17, 40)[r % 3] for r in range(n)),
+                         self_len=tuple((64, 30, 40)[r % 3] for r in range(n)),
+                         links=(0, 0), seed=29)
+    links = [[(r * 7 + j) % 12 for j in range(1 + (r * 5) % 11)] for r in range(n)]
+    wl = W.make_workload(cfg)
+    offs = np.zeros(n + 1, np.int32)
+    offs[1:] = np.cumsum([len(l) for l in links])
+    idx = np.array([c for l in links for c in l], dtype=np.int64)
+    wl = dataclasses.replace(wl, plan=dataclasses.replace(wl.plan, chunk_offsets=offs,
+                                                          chunk_index=idx))
+    print("case order_search: 40 requests, two calls on one store", flush=True)
+    dw = runner.upload(wl)
+    try:
+        dw.run()
+        torch.cuda.synchronize()
+        out1, lse1 = dw.results()
+        dw.run()
+        torch.cuda.synchronize()
+        out2, lse2 = dw.results()
+        ref, ref_lse = oracle.run_workload(wl, dict(dw.chunks))
+    finally:
+        dw.close()
+    compare(cfg, out1, lse1, ref, ref_lse, label="order_search")
+    assert np.array_equal(out1, out2) and np.array_equal(lse1, lse2)
