@@ -269,6 +269,35 @@ __global__ void prep_own_kernel(PrepParams pp) {
 
 constexpr int kValuRows = 16;
 
+// All-lane max / sum of a wave without LDS round trips: DPP moves inside
+// each 16-lane row (lane ^ 1, lane ^ 2 by quad permutes, then the mirrors
+// of each 8-lane half and of the row), then lanes l ^ 16 and l ^ 32 by the
+// permlane swaps. Every lane ends with the wave's result.
+template <int kCtrl>
+__device__ __forceinline__ float dpp_mov(float x) {
+  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), kCtrl, 0xF, 0xF, false));
+}
+__device__ __forceinline__ float wave_max(float x) {
+  x = fmaxf(x, dpp_mov<0xB1>(x));    // quad_perm [1,0,3,2]
+  x = fmaxf(x, dpp_mov<0x4E>(x));    // quad_perm [2,3,0,1]
+  x = fmaxf(x, dpp_mov<0x141>(x));   // row_half_mirror
+  x = fmaxf(x, dpp_mov<0x140>(x));   // row_mirror
+  auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  x = fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+  r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ __forceinline__ float wave_sum(float x) {
+  x += dpp_mov<0xB1>(x);
+  x += dpp_mov<0x4E>(x);
+  x += dpp_mov<0x141>(x);
+  x += dpp_mov<0x140>(x);
+  auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  x = __uint_as_float(r[0]) + __uint_as_float(r[1]);
+  r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+
 // Copies rows of 16-byte units from global memory into LDS rows of 4-byte
 // words (row r, unit c at dst[r * stride + 4 c ..]): each thread issues 4
 // loads before storing any, so the loads' latencies overlap (a plain loop
@@ -464,9 +493,7 @@ __device__ __forceinline__ void valu_body(const LinkParams &p, const SmallTabs &
     for (int r = 0; r < 4; ++r) {
       bool vis = rvalid[r] && lane < nvalid && (own ? j0 + lane <= lim[r] : tok + lane < dl[r]);
       float sv = vis ? s[r] : -INFINITY;
-      float mx = sv;
-#pragma unroll
-      for (int o = 32; o > 0; o >>= 1) mx = fmaxf(mx, __shfl_xor(mx, o));
+      const float mx = wave_max(sv);
       const float mnew = fmaxf(m[r], mx);
       float pv = 0.f;
       alpha[r] = 1.f;
@@ -474,9 +501,7 @@ __device__ __forceinline__ void valu_body(const LinkParams &p, const SmallTabs &
         pv = vis ? exp2f(sv - mnew) : 0.f;
         alpha[r] = exp2f(m[r] - mnew);
       }
-      float sum = pv;
-#pragma unroll
-      for (int o = 32; o > 0; o >>= 1) sum += __shfl_xor(sum, o);
+      const float sum = wave_sum(pv);
       l[r] = l[r] * alpha[r] + sum;
       m[r] = mnew;
       pr[r] = pv;
