@@ -364,7 +364,21 @@ __device__ __forceinline__ void gather_vt_lds(const T *src, int64_t src_stride, 
   }
 }
 
-template <typename T, bool MLA, bool kSmall>
+// kPf: the tile's K and V units go out as one batch of register loads (at
+// most kPfUnits 16-byte units per thread each, unit counts powers of two),
+// stored to LDS after one wait, and the next tile's batch is issued before
+// the current tile is computed; the first tile's batch goes out beside the
+// query loads. Without it, K rows and each V panel were a memory round trip
+// of their own (tiny_f32: three per tile, ≈ 7 us per tile per workgroup).
+constexpr int kPfUnits = 8;
+
+struct PfTile {                 // the tile whose loads are in flight
+  LinkEntry E;
+  int tt, nvalid, j0, tok;
+  bool own;
+};
+
+template <typename T, bool MLA, bool kSmall, bool kPf>
 __device__ __forceinline__ void valu_body(const LinkParams &p, const SmallTabs &t) {
   extern __shared__ float smem[];
   const int d_k = p.d_k, d_v = p.d_v, group = p.group;
@@ -397,6 +411,104 @@ __device__ __forceinline__ void valu_body(const LinkParams &p, const SmallTabs &
   float4 *pb = (float4 *)(vts + (MLA ? 0 : d_v * vstride));  // [4][64]
   const T *ks_e = (const T *)ks;
   const T *vts_e = (const T *)vts;
+
+  int li = 0;
+  auto tile_info = [&](int tl) -> PfTile {
+    while (link(R.link0 + li).tile0 + (link(R.link0 + li).len + kTile - 1) / kTile <= tl) ++li;
+    PfTile x;
+    x.E = link(R.link0 + li);
+    x.tt = tl - x.E.tile0;
+    x.nvalid = min(kTile, x.E.len - x.tt * kTile);
+    x.j0 = x.tt * kTile;        // key index within the link (own: within the own KV)
+    x.tok = x.E.tok0 + x.j0;    // ... within the request's linked rows
+    x.own = tl >= R.doc_tiles;
+    return x;
+  };
+  // kPf unit coordinates of this thread (unit i = tid + 256 u): K unit c of
+  // row r; slot V unit c of panel row (panel, dv) = vr (panels [2][d_v][32]
+  // are contiguous, so panel row vr starts at vr * 32 elements); own V
+  // (token-major, small calls) unit c of key row r.
+  const int tid = threadIdx.x;
+  const int ku = d_k * (int)sizeof(T) / 16, lku = 31 - __clz(ku);
+  const int kc = tid & (ku - 1), kr0 = tid >> lku, krs = 256 >> lku;
+  const int n_k = kTile * ku;
+  constexpr int pu = kPanel * (int)sizeof(T) / 16;
+  constexpr int lpu = pu == 8 ? 3 : 2;
+  const int vc = tid & (pu - 1), vr0 = tid >> lpu, vrs = 256 >> lpu;
+  const int vu = d_v * (int)sizeof(T) / 16, lvu = 31 - __clz(vu), ldv = 31 - __clz(d_v);
+  const int oc = tid & (vu - 1), or0 = tid >> lvu, ors = 256 >> lvu;
+  const int n_v = MLA ? 0 : kTile * vu;
+  const int kv_heads = MLA ? 1 : p.n_kv_heads;
+  uint4 rk[kPfUnits], rv[kPfUnits];
+  auto pf_load = [&](const PfTile &x) {
+    const bool in_place = kSmall && x.own;   // own rows straight from k_self / v_self
+    const char *kb = in_place
+        ? (const char *)((const T *)p.k_self + ((int64_t)(R.s0 + x.j0) * kv_heads + kvh) * d_k)
+        : (const char *)key_row<T>(x.E, MLA ? 0 : kvh, x.j0, d_k);
+    const int64_t krow_b = (int64_t)(in_place ? kv_heads : 1) * d_k * sizeof(T);
+#pragma unroll
+    for (int u = 0; u < kPfUnits; ++u)
+      if (tid + 256 * u < n_k) {
+        const int r = kr0 + u * krs;
+        rk[u] = *(const uint4 *)(kb + (in_place ? min(r, x.nvalid - 1) : r) * krow_b + 16 * kc);
+      }
+    if (MLA) return;
+    if (in_place) {
+      const char *vb =
+          (const char *)((const T *)p.v_self + ((int64_t)(R.s0 + x.j0) * kv_heads + kvh) * d_v);
+      const int64_t vrow_b = (int64_t)kv_heads * d_v * sizeof(T);
+#pragma unroll
+      for (int u = 0; u < kPfUnits; ++u)
+        if (tid + 256 * u < n_v)
+          rv[u] = *(const uint4 *)(vb + min(or0 + u * ors, x.nvalid - 1) * vrow_b + 16 * oc);
+    } else {
+      const char *vb = (const char *)value_at<T>(x.E, kvh, 0, x.j0, d_v);
+#pragma unroll
+      for (int u = 0; u < kPfUnits; ++u)
+        if (tid + 256 * u < n_v)
+          rv[u] = *(const uint4 *)(vb + (int64_t)(vr0 + u * vrs) * kPanel * sizeof(T) + 16 * vc);
+    }
+  };
+  auto pf_store = [&](const PfTile &x) {
+#pragma unroll
+    for (int u = 0; u < kPfUnits; ++u)
+      if (tid + 256 * u < n_k) {
+        uint32_t *d = ks + (kr0 + u * krs) * kstride + 4 * kc;
+        d[0] = rk[u].x;
+        d[1] = rk[u].y;
+        d[2] = rk[u].z;
+        d[3] = rk[u].w;
+      }
+    if (MLA) return;
+    if (kSmall && x.own) {
+      constexpr int kPer = 16 / sizeof(T);
+      T *vt = (T *)vts;
+#pragma unroll
+      for (int u = 0; u < kPfUnits; ++u)
+        if (tid + 256 * u < n_v) {
+          T e[kPer];
+          __builtin_memcpy(e, &rv[u], 16);
+#pragma unroll
+          for (int k = 0; k < kPer; ++k) vt[(oc * kPer + k) * (vstride * EPW) + or0 + u * ors] = e[k];
+        }
+    } else {
+#pragma unroll
+      for (int u = 0; u < kPfUnits; ++u)
+        if (tid + 256 * u < n_v) {
+          const int vr = vr0 + u * vrs, dv = vr & (d_v - 1), hp = vr >> ldv;
+          uint32_t *d = vts + dv * vstride + hp * (kPanel / EPW) + 4 * vc;
+          d[0] = rv[u].x;
+          d[1] = rv[u].y;
+          d[2] = rv[u].z;
+          d[3] = rv[u].w;
+        }
+    }
+  };
+  PfTile cur{};
+  if (kPf && t_begin < t_end) {
+    cur = tile_info(t_begin);
+    pf_load(cur);
+  }
 
   // the block's query rows, scaled; 4 loads per thread in flight at once
   for (int base = threadIdx.x; base < kValuRows * d_k; base += 4 * blockDim.x) {
@@ -437,39 +549,45 @@ __device__ __forceinline__ void valu_body(const LinkParams &p, const SmallTabs &
   }
   const int nvj = (d_v + 63) / 64;
 
-  int li = 0;
   for (int t = t_begin; t < t_end; ++t) {
-    const bool own = t >= R.doc_tiles;
     __syncthreads();
-    while (link(R.link0 + li).tile0 + (link(R.link0 + li).len + kTile - 1) / kTile <= t) ++li;
-    const LinkEntry E = link(R.link0 + li);
-    const int tt = t - E.tile0;
-    const int nvalid = min(kTile, E.len - tt * kTile);
-    const int j0 = tt * kTile;          // key index within the link (own: within the own KV)
-    const int tok = E.tok0 + j0;        // ... within the request's linked rows
-    if (kSmall && own) {
-      // own keys j0 .. j0 + nvalid - 1 from the caller's token-major rows
-      // (rows past nvalid stay unread: they are masked below)
-      const int kv_heads = MLA ? 1 : p.n_kv_heads;
-      const T *krow0 = (const T *)p.k_self + ((int64_t)(R.s0 + j0) * kv_heads + kvh) * d_k;
-      copy_rows_lds((const char *)krow0, (int64_t)kv_heads * d_k * sizeof(T), nvalid, kwords / 4,
-                    ks, kstride);
-      if (!MLA)
-        gather_vt_lds<T>((const T *)p.v_self + ((int64_t)(R.s0 + j0) * kv_heads + kvh) * d_v,
-                         (int64_t)kv_heads * d_v, nvalid, d_v, (T *)vts, vstride * EPW);
+    PfTile x;
+    if constexpr (kPf) {
+      // tile t's loads have landed (the stores wait for them); tile t+1's
+      // go out now and run under this tile's arithmetic
+      pf_store(cur);
+      x = cur;
+      if (t + 1 < t_end) {
+        cur = tile_info(t + 1);
+        pf_load(cur);
+      }
     } else {
-      // 64 consecutive key rows (the slot's padding rows are zeros)
-      // K rows (d_k elements, whole 16-byte units) and V^T rows (64 keys)
-      copy_rows_lds((const char *)key_row<T>(E, MLA ? 0 : kvh, tt * kTile, d_k),
-                    (int64_t)d_k * sizeof(T), kTile, kwords / 4, ks, kstride);
-      // V^T: the tile's two 32-token panels, each d_v rows of 32 keys
-      if (!MLA)
+      x = tile_info(t);
+      if (kSmall && x.own) {
+        // own keys j0 .. j0 + nvalid - 1 from the caller's token-major rows
+        // (rows past nvalid stay unread: they are masked below)
+        const T *krow0 = (const T *)p.k_self + ((int64_t)(R.s0 + x.j0) * kv_heads + kvh) * d_k;
+        copy_rows_lds((const char *)krow0, (int64_t)kv_heads * d_k * sizeof(T), x.nvalid,
+                      kwords / 4, ks, kstride);
+        if (!MLA)
+          gather_vt_lds<T>((const T *)p.v_self + ((int64_t)(R.s0 + x.j0) * kv_heads + kvh) * d_v,
+                           (int64_t)kv_heads * d_v, x.nvalid, d_v, (T *)vts, vstride * EPW);
+      } else {
+        // 64 consecutive key rows (the slot's padding rows are zeros)
+        // K rows (d_k elements, whole 16-byte units) and V^T rows (64 keys)
+        copy_rows_lds((const char *)key_row<T>(x.E, MLA ? 0 : kvh, x.j0, d_k),
+                      (int64_t)d_k * sizeof(T), kTile, kwords / 4, ks, kstride);
+        // V^T: the tile's two 32-token panels, each d_v rows of 32 keys
+        if (!MLA)
 #pragma unroll
-        for (int hp = 0; hp < kTile / kPanel; ++hp)
-          copy_rows_lds((const char *)value_at<T>(E, kvh, 0, tt * kTile + hp * kPanel, d_v),
-                        (int64_t)kPanel * sizeof(T), d_v, kPanel * (int)sizeof(T) / 16,
-                        vts + hp * (kPanel / EPW), vstride);
+          for (int hp = 0; hp < kTile / kPanel; ++hp)
+            copy_rows_lds((const char *)value_at<T>(x.E, kvh, 0, x.j0 + hp * kPanel, d_v),
+                          (int64_t)kPanel * sizeof(T), d_v, kPanel * (int)sizeof(T) / 16,
+                          vts + hp * (kPanel / EPW), vstride);
+      }
     }
+    const bool own = x.own;
+    const int nvalid = x.nvalid, j0 = x.j0, tok = x.tok;
     __syncthreads();
 
     // scores: lane = key
@@ -591,14 +709,14 @@ __device__ __forceinline__ void valu_body(const LinkParams &p, const SmallTabs &
   }
 }
 
-template <typename T, bool MLA>
+template <typename T, bool MLA, bool kPf>
 __global__ __launch_bounds__(256) void link_valu_kernel(LinkParams p) {
-  valu_body<T, MLA, false>(p, SmallTabs{});
+  valu_body<T, MLA, false, kPf>(p, SmallTabs{});
 }
 
-template <typename T, bool MLA>
+template <typename T, bool MLA, bool kPf>
 __global__ __launch_bounds__(256) void link_small_kernel(LinkParams p, SmallTabs t) {
-  valu_body<T, MLA, true>(p, t);
+  valu_body<T, MLA, true, kPf>(p, t);
 }
 
 // ---------------------------------------------------------------------------
@@ -697,26 +815,50 @@ size_t valu_lds_bytes(int esz, int mla, int d_k, int d_v) {
          (mla ? 0 : 4 * d_v * vstride) + sizeof(float4) * 4 * 64;
 }
 
-template <typename T, bool MLA>
-hipError_t launch_valu_t(const LinkParams &p, hipStream_t st) {
+// Shapes the register-prefetch tile path (kPf) takes: 16-byte unit counts
+// per K and V row that are powers of two (and d_v one too), at most
+// kPfUnits units per thread for each of a tile's K and V.
+bool valu_prefetch_ok(int esz, bool mla, int d_k, int d_v) {
+  auto pow2 = [](int x) { return x > 0 && (x & (x - 1)) == 0; };
+  const int ku = d_k * esz / 16, vu = d_v * esz / 16;
+  if (d_k * esz % 16 || !pow2(ku) || kTile * ku > kPfUnits * 256) return false;
+  if (!mla && (d_v * esz % 16 || !pow2(vu) || !pow2(d_v) || kTile * vu > kPfUnits * 256))
+    return false;
+  return true;
+}
+
+template <typename T, bool MLA, bool kPf>
+hipError_t launch_valu_tp(const LinkParams &p, hipStream_t st) {
   const size_t lds = valu_lds_bytes(sizeof(T), MLA, p.d_k, p.d_v);
-  hipError_t e = hipFuncSetAttribute((const void *)link_valu_kernel<T, MLA>,
+  hipError_t e = hipFuncSetAttribute((const void *)link_valu_kernel<T, MLA, kPf>,
                                      hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
   if (e != hipSuccess) return e;
   dim3 grid(p.n_groups * p.nrb, p.num_splits);
-  hipLaunchKernelGGL((link_valu_kernel<T, MLA>), grid, dim3(256), lds, st, p);
+  hipLaunchKernelGGL((link_valu_kernel<T, MLA, kPf>), grid, dim3(256), lds, st, p);
+  return hipGetLastError();
+}
+
+template <typename T, bool MLA>
+hipError_t launch_valu_t(const LinkParams &p, hipStream_t st) {
+  return valu_prefetch_ok(sizeof(T), MLA, p.d_k, p.d_v) ? launch_valu_tp<T, MLA, true>(p, st)
+                                                        : launch_valu_tp<T, MLA, false>(p, st);
+}
+
+template <typename T, bool MLA, bool kPf>
+hipError_t launch_small_tp(const LinkParams &p, const SmallTabs &t, hipStream_t st) {
+  const size_t lds = valu_lds_bytes(sizeof(T), MLA, p.d_k, p.d_v);
+  hipError_t e = hipFuncSetAttribute((const void *)link_small_kernel<T, MLA, kPf>,
+                                     hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+  if (e != hipSuccess) return e;
+  dim3 grid(p.n_groups * p.nrb, p.num_splits);
+  hipLaunchKernelGGL((link_small_kernel<T, MLA, kPf>), grid, dim3(256), lds, st, p, t);
   return hipGetLastError();
 }
 
 template <typename T, bool MLA>
 hipError_t launch_small_t(const LinkParams &p, const SmallTabs &t, hipStream_t st) {
-  const size_t lds = valu_lds_bytes(sizeof(T), MLA, p.d_k, p.d_v);
-  hipError_t e = hipFuncSetAttribute((const void *)link_small_kernel<T, MLA>,
-                                     hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-  if (e != hipSuccess) return e;
-  dim3 grid(p.n_groups * p.nrb, p.num_splits);
-  hipLaunchKernelGGL((link_small_kernel<T, MLA>), grid, dim3(256), lds, st, p, t);
-  return hipGetLastError();
+  return valu_prefetch_ok(sizeof(T), MLA, p.d_k, p.d_v) ? launch_small_tp<T, MLA, true>(p, t, st)
+                                                        : launch_small_tp<T, MLA, false>(p, t, st);
 }
 
 }  // namespace
