@@ -311,6 +311,26 @@ pic_status pic_link_plan_destroy(pic_link_plan *plan);
 pic_status pic_debug_gather(pic_store *store, const uint64_t *ids, int32_t n, int32_t layer,
                             void *k_out, void *v_out, void *stream);
 
+/* Test hook, host only (no device work, no store): the request order the
+ * planner gives a bf16 d=128 prefill call, whose row blocks (256 rows of
+ * one request and kv head) are dispatched in that order, each on the first
+ * free CU of its XCD. Request r has q_len[r] query tokens, self_len[r] own
+ * tokens (causal, Sec. 4.1) and doc_tiles[r] 64-key tiles of linked
+ * documents (Sec. 4.2); the GQA group is n_q_heads / n_kv_heads; cus and
+ * xcds describe the device (workgroup ids go round-robin to the XCDs).
+ * order_out: host [batch], the request at each position: heaviest first
+ * (tiles x query tokens), improved by pairwise swaps when the row blocks
+ * of an XCD take several rounds of its CUs. finish_out: host [2] or NULL,
+ * the simulated finish time in tiles of the busiest XCD (a workgroup takes
+ * its visible tiles plus 1.5) for heaviest first and for the returned
+ * order; both 0 when no search runs.
+ * Errors: INVALID (NULL arrays, negative lengths, n_q_heads not a multiple
+ * of n_kv_heads, cus not a multiple of xcds). */
+pic_status pic_debug_request_order(const int32_t *q_len, const int32_t *self_len,
+                                   const int32_t *doc_tiles, int32_t batch, int32_t n_q_heads,
+                                   int32_t n_kv_heads, int32_t cus, int32_t xcds,
+                                   int32_t *order_out, double *finish_out);
+
 /* Dense per-head projections around absorbed MLA link attention, for the
  * DeepSeek-V2-Lite backbone (Sec. 5.1): per head h its latent rows c (512)
  * give non-absorbed keys [W_UK[h] c | k_rope] and values W_UV[h] c, with

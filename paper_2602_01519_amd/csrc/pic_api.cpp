@@ -665,15 +665,19 @@ struct OrderSim {
   }
 };
 
+// finish: when not NULL, receives the simulated finish time (in tiles) of
+// the busiest XCD for heaviest first and for the order chosen (both 0 when
+// no search runs). s: the store whose memo to use, or NULL for none.
 void balance_order_d128(pic_store *s, Plan &P, const LinkParams &lp, int rows_per_block,
-                        int slots) {
+                        int slots, double *finish = nullptr) {
+  if (finish) finish[0] = finish[1] = 0;
   const int B = (int)P.order.size();
   if (B < 3 || B > 64 || slots <= 0 || lp.n_kv_heads % lp.n_xcd) return;
   const int reps = lp.n_kv_heads / lp.n_xcd;
   if ((int64_t)B * reps * lp.nrb <= slots) return;   // one round: all start at once
   std::vector<int32_t> key = {lp.nrb, rows_per_block, lp.group, reps, slots, B};
   for (const ReqEntry &R : P.reqs) key.insert(key.end(), {R.lq, R.ls, R.doc_tiles, R.tiles});
-  if (key == s->order_key) {
+  if (s && !finish && key == s->order_key) {
     P.order = s->order_memo;
     return;
   }
@@ -685,11 +689,14 @@ void balance_order_d128(pic_store *s, Plan &P, const LinkParams &lp, int rows_pe
     h = pre;
     for (int i = 0; i < B; ++i) sim.add(h, best, order[i], INFINITY);
   }
+  if (finish) finish[0] = best;
+  auto same_shape = [&](int a, int b) {
+    const ReqEntry &x = P.reqs[a], &y = P.reqs[b];
+    return x.lq == y.lq && x.ls == y.ls && x.doc_tiles == y.doc_tiles && x.tiles == y.tiles;
+  };
   for (int i = 0; i + 1 < B; ++i) {
     for (int j = i + 1; j < B; ++j) {
-      if (P.reqs[order[i]].tiles == P.reqs[order[j]].tiles &&
-          P.reqs[order[i]].lq == P.reqs[order[j]].lq)
-        continue;
+      if (same_shape(order[i], order[j])) continue;
       std::swap(order[i], order[j]);
       h = pre;
       double top = pre_top;
@@ -702,9 +709,12 @@ void balance_order_d128(pic_store *s, Plan &P, const LinkParams &lp, int rows_pe
     }
     sim.add(pre, pre_top, order[i], INFINITY);
   }
+  if (finish) finish[1] = best;
   P.order = order;
-  s->order_key = std::move(key);
-  s->order_memo = order;
+  if (s) {
+    s->order_key = std::move(key);
+    s->order_memo = order;
+  }
 }
 
 pic_status setup_call(pic_store *s, const pic_link_req *req, int32_t n_q_heads, float scale,
@@ -1692,6 +1702,57 @@ pic_status pic_debug_gather(pic_store *s, const uint64_t *ids, int32_t n, int32_
   if (e != hipSuccess) return hip_fail(e, "gather_kernel");
   HIP_TRY(hipEventRecord(stage->done, st), "hipEventRecord(stage)");
   stage->pending = true;
+  return PIC_OK;
+}
+
+pic_status pic_debug_request_order(const int32_t *q_len, const int32_t *self_len,
+                                   const int32_t *doc_tiles, int32_t batch, int32_t n_q_heads,
+                                   int32_t n_kv_heads, int32_t cus, int32_t xcds,
+                                   int32_t *order_out, double *finish_out) {
+  if (batch < 0 || (batch > 0 && (!q_len || !self_len || !doc_tiles || !order_out)))
+    return fail(PIC_ERR_INVALID, "NULL array");
+  if (n_kv_heads <= 0 || n_q_heads <= 0 || n_q_heads % n_kv_heads || cus <= 0 || xcds <= 0 ||
+      cus % xcds)
+    return fail(PIC_ERR_INVALID, "bad head counts or device shape");
+  Plan P;
+  P.reqs.resize(batch);
+  int32_t max_rows = 0;
+  const int group = n_q_heads / n_kv_heads;
+  for (int32_t r = 0; r < batch; ++r) {
+    if (q_len[r] < 0 || self_len[r] < 0 || doc_tiles[r] < 0 ||
+        (int64_t)q_len[r] * group > INT32_MAX / 2 || self_len[r] > INT32_MAX / 2 ||
+        doc_tiles[r] > INT32_MAX / 4)
+      return fail(PIC_ERR_INVALID, "request %d: length out of range", r);
+    ReqEntry &R = P.reqs[r];
+    R = ReqEntry{};
+    R.lq = q_len[r];
+    R.ls = self_len[r];
+    R.doc_tiles = doc_tiles[r];
+    R.tiles = R.doc_tiles + (R.ls + kTile - 1) / kTile;
+    max_rows = std::max(max_rows, R.lq * group);
+  }
+  // heaviest first, as plan_call orders
+  P.order.resize(batch);
+  for (int32_t r = 0; r < batch; ++r) P.order[r] = r;
+  std::stable_sort(P.order.begin(), P.order.end(), [&](int32_t a, int32_t b) {
+    return (int64_t)P.reqs[a].tiles * P.reqs[a].lq > (int64_t)P.reqs[b].tiles * P.reqs[b].lq;
+  });
+  LinkParams lp{};
+  lp.batch = batch;
+  lp.n_q_heads = n_q_heads;
+  lp.n_kv_heads = n_kv_heads;
+  lp.group = group;
+  lp.n_xcd = xcds;
+  const int rows_per_block = mfma_d128_rows_per_block();
+  lp.nrb = std::max(1, (max_rows + rows_per_block - 1) / rows_per_block);
+  lp.n_groups = (int32_t)round_up((int64_t)batch * n_kv_heads, xcds);
+  double finish[2];
+  balance_order_d128(nullptr, P, lp, rows_per_block, cus / xcds * mfma_d128_blocks_per_cu(), finish);
+  std::copy(P.order.begin(), P.order.end(), order_out);
+  if (finish_out) {
+    finish_out[0] = finish[0];
+    finish_out[1] = finish[1];
+  }
   return PIC_OK;
 }
 

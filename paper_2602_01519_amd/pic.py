@@ -82,6 +82,7 @@ def lib():
             "pic_link_decode": [vp, vp, i32, vp, vp, vp, f32, i32, vp, vp, vp],
             "pic_link_decode_noalloc": [vp, vp, i32, vp, vp, vp, f32, i32, vp, vp, vp],
             "pic_debug_gather": [vp, vp, i32, i32, vp, vp, vp],
+            "pic_debug_request_order": [vp, vp, vp, i32, i32, i32, i32, i32, vp, vp],
             "pic_link_plan_create": [vp, vp, i32, i32, i32, vp],
             "pic_link_plan_run": [vp, i32, vp, vp, vp, f32, vp, vp, vp],
             "pic_link_plan_destroy": [vp],
@@ -260,6 +261,22 @@ def link_decode_noalloc(store: Store, chunk_offsets, chunk_ids, q_offsets, self_
     _check(lib().pic_link_decode_noalloc(store.handle, ctypes.byref(req), int(n_q_heads), _ptr(q),
                                          _ptr(k_self), _ptr(v_self), float(softmax_scale),
                                          int(num_splits), _ptr(out), _ptr(lse), stream))
+
+
+def debug_request_order(q_len, self_len, doc_tiles, n_q_heads: int, n_kv_heads: int, cus: int,
+                        xcds: int):
+    """pic_debug_request_order: the d=128 prefill request order (host only).
+    Returns (order, finish) with finish = [heaviest first, returned order]."""
+    q_len = np.ascontiguousarray(q_len, dtype=np.int32)
+    self_len = np.ascontiguousarray(self_len, dtype=np.int32)
+    doc_tiles = np.ascontiguousarray(doc_tiles, dtype=np.int32)
+    n = len(q_len)
+    order = np.zeros(max(n, 1), np.int32)
+    finish = np.zeros(2, np.float64)
+    _check(lib().pic_debug_request_order(q_len.ctypes.data, self_len.ctypes.data,
+                                         doc_tiles.ctypes.data, n, n_q_heads, n_kv_heads, cus,
+                                         xcds, order.ctypes.data, finish.ctypes.data))
+    return order[:n], finish
 
 
 def debug_gather(store: Store, ids, k_out, v_out, stream: Optional[int] = None, layer: int = 0):
