@@ -603,3 +603,60 @@ def test_request_order_search_keeps_results():
         dw.close()
     compare(cfg, out1, lse1, ref, ref_lse, label="order_search")
     assert np.array_equal(out1, out2) and np.array_equal(lse1, lse2)
+
+
+def _merge_case(kind, dtype):
+    common = dict(chunk_lens=(70, 64, 1, 130, 200), batch=3, links=(1, 4), q_len=(37, 5, 20),
+                  self_len=(41, 5, 84), seed=31)
+    if kind == W.MLA:
+        return W.small_config("merge_mla", kind=W.MLA, n_q_heads=16, d_k=576, d_v=512,
+                              q_std=1.0, scale=1 / math.sqrt(192), **common)
+    if dtype == W.F32:
+        return W.small_config("merge_f32", dtype=W.F32, d_k=64, **common)
+    return W.small_config("merge_gqa", d_k=128, **common)
+
+
+@pytest.mark.parametrize("case", ["gqa", "mla", "f32"])
+def test_cross_and_self_merge_to_the_joint_call(case):
+    """Comb keeps document KV in cross-attention layers (Eq. 7-8) beside
+    causal self-attention (Eq. 2-3); the generic link puts both under one
+    softmax. The GPU's cross-only call (no own KV) and self-only call (no
+    links), merged on the host by log-sum-exp in fp64, must match the
+    oracle's joint result to the parity bar, and the GPU's joint call."""
+    cfg = _merge_case(W.MLA if case == "mla" else W.GQA, W.F32 if case == "f32" else W.BF16)
+    wl = W.make_workload(cfg)
+    p = wl.plan
+    print(f"case merge {cfg.name}", flush=True)
+    dw = runner.upload(wl)
+    try:
+        st = torch.cuda.current_stream().cuda_stream
+        scale = float(np.float32(cfg.scale))
+        dw.run()
+        torch.cuda.synchronize()
+        joint, joint_lse = dw.results()
+        outs = []
+        for part in ("cross", "self"):
+            out = torch.empty_like(dw.out)
+            lse = torch.empty_like(dw.lse)
+            if part == "cross":
+                pic.link_attn(dw.store, p.chunk_offsets, wl.link_ids(), p.q_offsets, None,
+                              cfg.n_q_heads, dw.q, None, None, scale, out, lse, stream=st)
+            else:
+                pic.link_attn(dw.store, np.zeros(cfg.batch + 1, np.int32),
+                              np.zeros(0, np.uint64), p.q_offsets, p.self_offsets, cfg.n_q_heads,
+                              dw.q, dw.k_self, dw.v_self, scale, out, lse, stream=st)
+            torch.cuda.synchronize()
+            outs.append((runner.to_host(out, cfg.dtype).astype(np.float64),
+                         lse.cpu().numpy().astype(np.float64)))
+        ref, ref_lse = oracle.run_workload(wl, dict(dw.chunks))
+    finally:
+        dw.close()
+    (oc, lc), (os_, ls) = outs
+    m = np.maximum(lc, ls)
+    wc = np.where(np.isneginf(lc), 0.0, np.exp(lc - m))
+    ws = np.where(np.isneginf(ls), 0.0, np.exp(ls - m))
+    merged = (wc[..., None] * oc + ws[..., None] * os_) / (wc + ws)[..., None]
+    merged_lse = m + np.log(wc + ws)
+    compare(cfg, merged, merged_lse, ref, ref_lse, label=f"merge {cfg.name}")
+    compare(cfg, merged, merged_lse, joint.astype(np.float64), joint_lse,
+            label=f"merge vs joint {cfg.name}")
