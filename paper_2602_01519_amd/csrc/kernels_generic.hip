@@ -861,6 +861,307 @@ hipError_t launch_small_t(const LinkParams &p, const SmallTabs &t, hipStream_t s
                                                         : launch_small_tp<T, MLA, false>(p, t, st);
 }
 
+// ---------------------------------------------------------------------------
+// Lean small-call kernel (GQA, d_k = d_v = D fixed at compile time, power-of-
+// two query group): the computation of link_small_kernel for calls that are
+// latency-bound, 16 rows per workgroup. A wave alone on its SIMD issues at
+// most one instruction every four cycles, so such a call's time is its
+// per-wave instruction count plus its memory round trips; this kernel keeps
+// both low. The grid carries (row block, split, request x kv head); every
+// tile's link comes from the host's tile map; each 16-byte unit of a tile is
+// one load and one LDS store, and the next tile's loads run under the
+// current tile's arithmetic. Products run on 16x16 matrix-core instructions
+// (fp32: v_mfma_f32_16x16x4_f32, bf16: v_mfma_f32_16x16x16_bf16): wave w
+// takes keys 16w .. 16w+15 of every tile for all 16 rows and keeps its own
+// online softmax, as S^T = K Q^T and O^T += V^T P^T, so each lane's
+// probabilities are exactly its operand of the value product and never leave
+// its registers; the four waves' (m, l, O) are merged through LDS at the end.
+// Queries stay in registers for the whole call.
+//
+// 16x16 operand layouts (lane l): A[m = l & 15][k-slot group l >> 4],
+// B[k-slot group l >> 4][n = l & 15], C register j: [m = 4 (l >> 4) + j][n = l & 15].
+// For S^T the key of lane l's row of K is 16w + (l & 15) and its k-slot group
+// reads head dims [D/4 (l >> 4), D/4 (l >> 4 + 1)) of that row and of the
+// query row l & 15; C register j then holds key 16w + 4 (l >> 4) + j, row l & 15.
+
+template <typename T, int D>
+struct LeanShape {
+  static constexpr int E = 16 / (int)sizeof(T);        // elements per 16-byte unit
+  static constexpr int KU = D / E;                      // units per K row
+  static constexpr int KSW = D * (int)sizeof(T) / 4 + 4;    // K row stride in LDS (words)
+  static constexpr int VSW = kTile * (int)sizeof(T) / 4 + 4; // V^T row stride (64 keys)
+  static constexpr int PRU = kPanel / E;                // units per row of a 32-key panel
+  static constexpr int NU = kTile * KU / 256;           // K (and V) units per thread
+  static constexpr int SEG = D / 4;                     // head dims per k-slot group
+  static constexpr int SEGU = SEG / E;                  // their 16-byte units
+  static constexpr int NB = D / 16;                     // 16-wide value-dim blocks
+  static constexpr int OSW = D + 1;                     // merge buffer row stride (floats)
+  static constexpr int TILE_WORDS = kTile * KSW + D * VSW;
+  static constexpr int MERGE_WORDS = 4 * kValuRows * OSW;
+  static constexpr int ML_OFF = TILE_WORDS > MERGE_WORDS ? TILE_WORDS : MERGE_WORDS;
+  static constexpr int WORDS = ML_OFF + 2 * 4 * kValuRows;   // + per-wave m and l
+  static_assert(NU >= 1 && kTile * KU % 256 == 0, "whole units per thread");
+  static_assert(SEGU >= 1 && SEG % E == 0, "whole units per k-slot group");
+};
+
+typedef float lean_f4 __attribute__((ext_vector_type(4)));
+typedef short lean_s4 __attribute__((ext_vector_type(4)));
+
+// max / sum over the four lanes l & 15 + 16 g (one row of a 16x16 C tile)
+__device__ __forceinline__ float quad_rows_max(float x) {
+  auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  x = fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+  r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ __forceinline__ float quad_rows_sum(float x) {
+  auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  x = __uint_as_float(r[0]) + __uint_as_float(r[1]);
+  r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+
+template <typename T, int D>
+__global__ __launch_bounds__(256) void link_lean_kernel(LinkParams p, LeanTabs t) {
+  using S = LeanShape<T, D>;
+  constexpr int E = S::E;
+  constexpr bool F32 = sizeof(T) == 4;
+  __shared__ __attribute__((aligned(16))) uint32_t lds[S::WORDS];
+  uint32_t *ks = lds, *vts = lds + kTile * S::KSW;
+
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int lr = lane & 15, lg4 = lane >> 4;
+  const int rb = blockIdx.x, split = blockIdx.y;
+  const int pos = blockIdx.z / p.n_kv_heads, kvh = blockIdx.z - pos * p.n_kv_heads;
+  const ReqEntry R = t.reqs[pos];
+  const int lg = __builtin_ctz(p.group);
+  const int nrows = R.lq << lg;
+  const int row0 = rb * kValuRows;
+  if (row0 >= nrows) return;
+  const int vis = visible_tiles(R, min(nrows - 1, row0 + kValuRows - 1) >> lg);
+  const int t_begin = vis * split / p.num_splits, t_end = vis * (split + 1) / p.num_splits;
+  const int kvn = p.n_kv_heads;
+
+  // the loads of one tile into registers: K units (key, c) and V^T units
+  // (panel, value dim, key unit) in slot order; own tiles from the caller's
+  // token-major rows (rows past the tile's valid keys reread its last one)
+  struct Tile {
+    const T *kb, *vb;
+    int nvalid, j0;
+    bool own;
+  };
+  auto tile_at = [&](int tl) {
+    const LinkEntry L = t.links[R.link0 + t.tile_link[t.tile_base[pos] + tl]];
+    Tile x;
+    x.j0 = (tl - L.tile0) * kTile;
+    x.nvalid = min(kTile, L.len - x.j0);
+    x.own = tl >= R.doc_tiles;
+    if (x.own) {
+      x.kb = (const T *)p.k_self + ((int64_t)(R.s0 + x.j0) * kvn + kvh) * D;
+      x.vb = (const T *)p.v_self + ((int64_t)(R.s0 + x.j0) * kvn + kvh) * D;
+    } else {
+      x.kb = (const T *)L.k + ((int64_t)kvh * L.lp + x.j0) * D;
+      x.vb = (const T *)L.v + vt_offset(kvh, 0, x.j0, L.lp, D);
+    }
+    return x;
+  };
+  uint4 rk[S::NU], rv[S::NU];
+  auto issue = [&](const Tile &x) {
+#pragma unroll
+    for (int u = 0; u < S::NU; ++u) {
+      const int i = tid + 256 * u, key = i / S::KU, c = i % S::KU;
+      if (x.own) {
+        const int64_t r = (int64_t)min(key, x.nvalid - 1) * kvn * D;
+        rk[u] = *(const uint4 *)(x.kb + r + c * E);
+        rv[u] = *(const uint4 *)(x.vb + r + c * E);
+      } else {
+        rk[u] = *(const uint4 *)(x.kb + (int64_t)i * E);
+        rv[u] = *(const uint4 *)(x.vb + (int64_t)i * E);
+      }
+    }
+  };
+  auto land = [&](const Tile &x) {
+#pragma unroll
+    for (int u = 0; u < S::NU; ++u) {
+      const int i = tid + 256 * u, key = i / S::KU, c = i % S::KU;
+      // (whole-struct copies of array elements put the arrays in scratch)
+      *(uint4 *)(ks + key * S::KSW + 4 * c) = make_uint4(rk[u].x, rk[u].y, rk[u].z, rk[u].w);
+      if (x.own) {
+        // token-major: the unit holds value dims c*E .. c*E+E-1 of one key
+        using U = std::conditional_t<F32, uint32_t, uint16_t>;   // T's bits
+        const uint32_t w[4] = {rv[u].x, rv[u].y, rv[u].z, rv[u].w};
+        U *vt = (U *)vts + key;
+        constexpr int VSE = S::VSW * 4 / (int)sizeof(T);    // V^T row stride (elements)
+#pragma unroll
+        for (int k = 0; k < E; ++k) {
+          const uint32_t wk = w[k * (int)sizeof(T) / 4];
+          vt[(c * E + k) * VSE] = (U)(F32 ? wk : k & 1 ? wk >> 16 : wk & 0xffffu);
+        }
+      } else {
+        // slot V^T: panel, value dim, unit of 32-key panel row
+        const int pan = i / (D * S::PRU), dv = (i / S::PRU) % D, kc = i % S::PRU;
+        *(uint4 *)(vts + dv * S::VSW + pan * (kPanel * (int)sizeof(T) / 4) + 4 * kc) =
+            make_uint4(rv[u].x, rv[u].y, rv[u].z, rv[u].w);
+      }
+    }
+  };
+
+  Tile cur{};
+  if (t_begin < t_end) {
+    cur = tile_at(t_begin);
+    issue(cur);
+  }
+  // query row lr of the block, head dims [SEG lg4, SEG (lg4 + 1)), as the
+  // B operand of S^T = K Q^T (rows past the request: zeros)
+  const int qrow = row0 + lr;
+  const bool qvalid = qrow < nrows;
+  uint4 qu[S::SEGU];
+  {
+    const int row = min(qrow, nrows - 1);
+    const T *qp = (const T *)p.q +
+                  ((int64_t)(R.q0 + (row >> lg)) * p.n_q_heads + kvh * p.group + (row & (p.group - 1))) * D +
+                  S::SEG * lg4;
+#pragma unroll
+    for (int u = 0; u < S::SEGU; ++u) {
+      const uint4 v = *(const uint4 *)(qp + u * E);
+      qu[u] = qvalid ? make_uint4(v.x, v.y, v.z, v.w) : make_uint4(0u, 0u, 0u, 0u);
+    }
+  }
+  const int lim = ((min(qrow, nrows - 1)) >> lg) + R.ls - R.lq;   // last own key row lr sees
+  float m = -INFINITY, l = 0.f;
+  lean_f4 oacc[S::NB];
+#pragma unroll
+  for (int c = 0; c < S::NB; ++c) oacc[c] = lean_f4{0.f, 0.f, 0.f, 0.f};
+
+  for (int tl = t_begin; tl < t_end; ++tl) {
+    __syncthreads();              // the previous tile's reads are done
+    land(cur);
+    const Tile x = cur;
+    if (tl + 1 < t_end) {
+      cur = tile_at(tl + 1);
+      issue(cur);
+    }
+    __syncthreads();
+
+    // S^T block: keys 16 wave .. +15 of the tile x rows 0..15
+    lean_f4 sacc = {0.f, 0.f, 0.f, 0.f};
+    const uint4 *krow = (const uint4 *)(ks + (16 * wave + lr) * S::KSW) + S::SEGU * lg4;
+#pragma unroll
+    for (int u = 0; u < S::SEGU; ++u) {
+      const uint4 kk = krow[u];
+      const uint4 qq = qu[u];
+      if constexpr (F32) {
+        sacc = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(kk.x), __uint_as_float(qq.x), sacc, 0, 0, 0);
+        sacc = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(kk.y), __uint_as_float(qq.y), sacc, 0, 0, 0);
+        sacc = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(kk.z), __uint_as_float(qq.z), sacc, 0, 0, 0);
+        sacc = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(kk.w), __uint_as_float(qq.w), sacc, 0, 0, 0);
+      } else {
+        const lean_s4 a0 = {(short)(kk.x & 0xffff), (short)(kk.x >> 16), (short)(kk.y & 0xffff), (short)(kk.y >> 16)};
+        const lean_s4 b0 = {(short)(qq.x & 0xffff), (short)(qq.x >> 16), (short)(qq.y & 0xffff), (short)(qq.y >> 16)};
+        const lean_s4 a1 = {(short)(kk.z & 0xffff), (short)(kk.z >> 16), (short)(kk.w & 0xffff), (short)(kk.w >> 16)};
+        const lean_s4 b1 = {(short)(qq.z & 0xffff), (short)(qq.z >> 16), (short)(qq.w & 0xffff), (short)(qq.w >> 16)};
+        sacc = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(a0, b0, sacc, 0, 0, 0);
+        sacc = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(a1, b1, sacc, 0, 0, 0);
+      }
+    }
+    // online softmax of row lr over this wave's 16 keys (register j: key
+    // 16 wave + 4 lg4 + j of the tile)
+    float sv[4];
+    float mx = -INFINITY;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int kt = 16 * wave + 4 * lg4 + j;
+      const bool vk = qvalid && kt < x.nvalid && (!x.own || x.j0 + kt <= lim);
+      sv[j] = vk ? sacc[j] * p.scale_log2 : -INFINITY;
+      mx = fmaxf(mx, sv[j]);
+    }
+    const float mnew = fmaxf(m, quad_rows_max(mx));
+    float pj[4], alpha = 1.f, rs = 0.f;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      pj[j] = mnew == -INFINITY ? 0.f : exp2f(sv[j] - mnew);
+      rs += pj[j];
+    }
+    if (mnew != -INFINITY) alpha = exp2f(m - mnew);
+    l = l * alpha + quad_rows_sum(rs);
+    m = mnew;
+
+    // O^T += V^T P^T: value dims 16 c + lr, this wave's 16 keys
+    const uint32_t *vrow = vts + lr * S::VSW + (16 * wave + 4 * lg4) * (int)sizeof(T) / 4;
+#pragma unroll
+    for (int c = 0; c < S::NB; ++c) {
+      oacc[c] *= alpha;
+      if constexpr (F32) {
+        const uint4 vv = *(const uint4 *)(vrow + 16 * c * S::VSW);
+        oacc[c] = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(vv.x), pj[0], oacc[c], 0, 0, 0);
+        oacc[c] = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(vv.y), pj[1], oacc[c], 0, 0, 0);
+        oacc[c] = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(vv.z), pj[2], oacc[c], 0, 0, 0);
+        oacc[c] = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(vv.w), pj[3], oacc[c], 0, 0, 0);
+      } else {
+        const uint2 vv = *(const uint2 *)(vrow + 16 * c * S::VSW);
+        const lean_s4 a = {(short)(vv.x & 0xffff), (short)(vv.x >> 16), (short)(vv.y & 0xffff), (short)(vv.y >> 16)};
+        const lean_s4 b = {(short)bf16_rne(pj[0]), (short)bf16_rne(pj[1]), (short)bf16_rne(pj[2]),
+                           (short)bf16_rne(pj[3])};
+        oacc[c] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(a, b, oacc[c], 0, 0, 0);
+      }
+    }
+  }
+
+  // merge the four waves' (m, l, O) of each row; O^T register j of block c
+  // is value dim 16 c + 4 lg4 + j of row lr
+  __syncthreads();                // the last tile's reads are done
+  constexpr int NW = 4;                                   // waves with a partial
+  float *ob = (float *)lds;                               // [wave][row][OSW]
+  float *mb = (float *)(lds + S::ML_OFF), *lb = mb + NW * kValuRows;
+#pragma unroll
+  for (int c = 0; c < S::NB; ++c)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) ob[(wave * kValuRows + lr) * S::OSW + 16 * c + 4 * lg4 + j] = oacc[c][j];
+  if (lg4 == 0) {
+    mb[wave * kValuRows + lr] = m;
+    lb[wave * kValuRows + lr] = l;
+  }
+  __syncthreads();
+  // thread i: outputs (row, dv) = divmod(i + 256 k, D)
+  const int64_t total_rows = (int64_t)p.total_q * p.n_q_heads;
+  for (int idx = tid; idx < kValuRows * D; idx += 256) {
+    const int row = idx / D, dv = idx % D;
+    if (row0 + row >= nrows) break;       // later indices are later rows
+    float M = -INFINITY;
+#pragma unroll
+    for (int w = 0; w < NW; ++w) M = fmaxf(M, mb[w * kValuRows + row]);
+    float L = 0.f, o = 0.f;
+#pragma unroll
+    for (int w = 0; w < NW; ++w) {
+      const float mw = mb[w * kValuRows + row];
+      const float wt = M == -INFINITY || mw == -INFINITY ? 0.f : exp2f(mw - M);
+      L += wt * lb[w * kValuRows + row];
+      o += wt * ob[(w * kValuRows + row) * S::OSW + dv];
+    }
+    const int grow = row0 + row;
+    const int64_t orow =
+        (int64_t)(R.q0 + (grow >> lg)) * p.n_q_heads + kvh * p.group + (grow & (p.group - 1));
+    if (p.num_splits == 1) {
+      ((T *)p.out)[orow * D + dv] = from_f32<T>(L > 0.f ? o / L : 0.f);
+      if (dv == 0 && p.lse) p.lse[orow] = L > 0.f ? (M + log2f(L)) * 0.69314718055994531f : -INFINITY;
+    } else {
+      const int64_t prow = split * total_rows + orow;
+      p.part_o[prow * D + dv] = o;
+      if (dv == 0) {
+        p.part_m[prow] = M;
+        p.part_l[prow] = L;
+      }
+    }
+  }
+}
+
+template <typename T, int D>
+hipError_t launch_lean_t(const LinkParams &p, const LeanTabs &t, hipStream_t st) {
+  dim3 grid(p.nrb, p.num_splits, p.batch * p.n_kv_heads);
+  hipLaunchKernelGGL((link_lean_kernel<T, D>), grid, dim3(256), 0, st, p, t);
+  return hipGetLastError();
+}
+
 }  // namespace
 
 hipError_t launch_link_small(const LinkParams &p, const SmallTabs &t, int dtype, int mla,
@@ -871,6 +1172,24 @@ hipError_t launch_link_small(const LinkParams &p, const SmallTabs &t, int dtype,
   }
   *name = mla ? "link_small_kernel<bf16,MLA>" : "link_small_kernel<bf16,GQA>";
   return mla ? launch_small_t<uint16_t, true>(p, t, st) : launch_small_t<uint16_t, false>(p, t, st);
+}
+
+bool lean_supported(int dtype, int d_k, int d_v, int group) {
+  if (d_k != d_v || group < 1 || (group & (group - 1))) return false;
+  return d_k == 32 || d_k == 64 || (d_k == 128 && dtype == 0);
+}
+
+hipError_t launch_link_lean(const LinkParams &p, const LeanTabs &t, int dtype, hipStream_t st,
+                            const char **name) {
+  if (dtype == 0) {
+    *name = "link_lean_kernel<float>";
+    if (p.d_k == 32) return launch_lean_t<float, 32>(p, t, st);
+    if (p.d_k == 64) return launch_lean_t<float, 64>(p, t, st);
+    return launch_lean_t<float, 128>(p, t, st);
+  }
+  *name = "link_lean_kernel<bf16>";
+  if (p.d_k == 32) return launch_lean_t<uint16_t, 32>(p, t, st);
+  return launch_lean_t<uint16_t, 64>(p, t, st);
 }
 
 int valu_rows_per_block() { return kValuRows; }

@@ -53,14 +53,16 @@ pic_status hip_fail(hipError_t e, const char *what) {
 // Restores the caller's current device on scope exit.
 struct DeviceGuard {
   int prev = -1;
-  bool ok = true;
+  bool ok = true, switched = false;
   explicit DeviceGuard(int dev) {
     if (hipGetDevice(&prev) != hipSuccess) { ok = false; return; }
-    if (prev != dev && hipSetDevice(dev) != hipSuccess) ok = false;
+    if (prev != dev) {
+      switched = true;
+      if (hipSetDevice(dev) != hipSuccess) ok = false;
+    }
   }
   ~DeviceGuard() {
-    int cur;
-    if (prev >= 0 && hipGetDevice(&cur) == hipSuccess && cur != prev) (void)hipSetDevice(prev);
+    if (switched && prev >= 0) (void)hipSetDevice(prev);
   }
 };
 
@@ -619,6 +621,7 @@ struct Setup {
   Plan P;
   Kern kern = Kern::Valu;
   int32_t splits = 1;
+  bool lean = false;             // a small call the lean kernel runs
   LinkParams lp{};               // shapes only: no tables, tensors or scale yet
   std::vector<OwnArg> own_args;  // per request, for the prologue (batch <= kOwnArgs)
   size_t part_off = 0, part_bytes = 0;
@@ -811,6 +814,15 @@ pic_status setup_call(pic_store *s, const pic_link_req *req, int32_t n_q_heads, 
     splits = (int32_t)std::min<int64_t>(16, (P.max_tiles + per_slot - 1) / per_slot);
     splits = std::max(1, std::min(splits, P.max_tiles / min_piece));
   }
+  // A small generic call of a shape the lean kernel is built for (tables as
+  // a kernel argument, at most kLeanTiles tiles in all) runs it.
+  if (kern == Kern::Valu && !mla && lean_supported(d.dtype, d.d_k, d.d_v, lp.group) &&
+      P.links.size() <= (size_t)kSmallLinks && P.reqs.size() <= (size_t)kSmallReqs &&
+      P.doc_lim.empty()) {
+    int64_t tiles = 0;
+    for (const ReqEntry &R : P.reqs) tiles += R.tiles;
+    C.lean = tiles <= kLeanTiles;
+  }
   C.splits = splits;
   lp.num_splits = splits;
   if (kern == Kern::Mfma128 && splits == 1)
@@ -897,11 +909,6 @@ pic_status small_link_call(pic_store *s, const Setup &C, const void *q, const vo
     lp.part_m = lp.part_o + rows * C.splits * d.d_v;
     lp.part_l = lp.part_m + rows * C.splits;
   }
-  SmallTabs t;
-  memset(&t, 0, sizeof(t));
-  std::copy(C.P.links.begin(), C.P.links.end(), t.links);
-  std::copy(C.P.reqs.begin(), C.P.reqs.end(), t.reqs);
-  std::copy(C.P.order.begin(), C.P.order.end(), t.order);
   lp.links = nullptr;
   lp.reqs = nullptr;
   lp.order = nullptr;
@@ -914,8 +921,34 @@ pic_status small_link_call(pic_store *s, const Setup &C, const void *q, const vo
   lp.scale_log2 = scale * 1.4426950408889634f;
   std::pair<hipEvent_t, hipEvent_t> ev{nullptr, nullptr};
   const char *name = "";
-  prof_start(st, &ev);
-  hipError_t e = launch_link_small(lp, t, d.dtype, d.kind == PIC_MLA, st, &name);
+  hipError_t e;
+  if (C.lean) {
+    LeanTabs t;
+    memset(&t, 0, sizeof(t));
+    std::copy(C.P.links.begin(), C.P.links.end(), t.links);
+    int32_t base = 0;
+    for (size_t i = 0; i < C.P.order.size(); ++i) {
+      const ReqEntry &R = C.P.reqs[C.P.order[i]];
+      t.reqs[i] = R;
+      t.tile_base[i] = base;
+      for (int32_t k = 0; k < R.nlinks; ++k) {
+        const LinkEntry &L = C.P.links[R.link0 + k];
+        const int32_t n = (L.len + kTile - 1) / kTile;
+        for (int32_t j = 0; j < n; ++j) t.tile_link[base + L.tile0 + j] = (uint8_t)k;
+      }
+      base += R.tiles;
+    }
+    prof_start(st, &ev);
+    e = launch_link_lean(lp, t, d.dtype, st, &name);
+  } else {
+    SmallTabs t;
+    memset(&t, 0, sizeof(t));
+    std::copy(C.P.links.begin(), C.P.links.end(), t.links);
+    std::copy(C.P.reqs.begin(), C.P.reqs.end(), t.reqs);
+    std::copy(C.P.order.begin(), C.P.order.end(), t.order);
+    prof_start(st, &ev);
+    e = launch_link_small(lp, t, d.dtype, d.kind == PIC_MLA, st, &name);
+  }
   prof_stop(st, &ev, name);
   if (e != hipSuccess) return hip_fail(e, name);
   if (C.splits > 1) {

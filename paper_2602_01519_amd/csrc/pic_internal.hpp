@@ -203,4 +203,21 @@ struct SmallTabs {
 hipError_t launch_link_small(const LinkParams &p, const SmallTabs &t, int dtype, int mla,
                              hipStream_t st, const char **name);
 
+// Tables of a lean small call (link_lean_kernel): requests in dispatch
+// order, and for every tile of every request the link that holds it
+// (relative to the request's first link), so a workgroup finds its tiles
+// with one table read instead of a walk over the links.
+constexpr int kLeanTiles = 256;
+struct LeanTabs {
+  LinkEntry links[kSmallLinks];
+  ReqEntry reqs[kSmallReqs];          // reqs[i]: the i-th request in dispatch order
+  int32_t tile_base[kSmallReqs];      // first tile_link entry of reqs[i]
+  uint8_t tile_link[kLeanTiles];
+};
+// GQA shapes the lean kernel is built for: d_k = d_v = d in {32, 64, 128}
+// for fp32, {32, 64} for bf16, and a power-of-two query group.
+bool lean_supported(int dtype, int d_k, int d_v, int group);
+hipError_t launch_link_lean(const LinkParams &p, const LeanTabs &t, int dtype, hipStream_t st,
+                            const char **name);
+
 }  // namespace pic

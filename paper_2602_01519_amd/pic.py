@@ -137,6 +137,15 @@ def _host_i32(a):
     return None if a is None else np.ascontiguousarray(a, dtype=np.int32)
 
 
+def _addr(a: np.ndarray) -> int:
+    """Address of a contiguous host array's first byte (a ctypes view of a
+    writable buffer costs a third of numpy's .ctypes.data)."""
+    try:
+        return ctypes.addressof(ctypes.c_char.from_buffer(a))
+    except (TypeError, ValueError):      # read-only or empty
+        return a.ctypes.data
+
+
 class Store:
     """A chunk store (pool + hash table) on the current HIP device."""
 
@@ -221,10 +230,10 @@ def _req(chunk_offsets, chunk_ids, q_offsets, self_offsets, keep: list, layer: i
     st = _host_i32(chunk_starts)
     dl = _host_i32(q_doc_limits)
     keep += [co, ids, qo, so, st, dl]
-    return LinkReq(len(qo) - 1, int(layer), co.ctypes.data, ids.ctypes.data if ids.size else None,
-                   qo.ctypes.data, None if so is None else so.ctypes.data,
-                   None if st is None or not st.size else st.ctypes.data,
-                   None if dl is None or not dl.size else dl.ctypes.data)
+    return LinkReq(len(qo) - 1, int(layer), _addr(co), _addr(ids) if ids.size else None,
+                   _addr(qo), None if so is None else _addr(so),
+                   None if st is None or not st.size else _addr(st),
+                   None if dl is None or not dl.size else _addr(dl))
 
 
 def link_attn(store: Store, chunk_offsets, chunk_ids, q_offsets, self_offsets, n_q_heads: int, q,
@@ -248,6 +257,37 @@ def link_decode(store: Store, chunk_offsets, chunk_ids, q_offsets, self_offsets,
     _check(lib().pic_link_decode(store.handle, ctypes.byref(req), int(n_q_heads), _ptr(q), _ptr(k_self),
                                  _ptr(v_self), float(softmax_scale), int(num_splits), _ptr(out),
                                  _ptr(lse), stream))
+
+
+class PreparedCall:
+    """pic_link_attn (or pic_link_decode) with its arguments marshalled once:
+    the request struct, the host arrays it points at (kept alive here) and
+    the tensor addresses. Calling it runs the same C entry point on a stream;
+    the tensors must stay allocated and the host arrays unchanged."""
+
+    def __init__(self, decode: bool, store: Store, chunk_offsets, chunk_ids, q_offsets,
+                 self_offsets, n_q_heads: int, q, k_self, v_self, softmax_scale: float, out,
+                 lse=None, num_splits: int = 0, layer: int = 0, chunk_starts=None,
+                 q_doc_limits=None):
+        self._store = store
+        self._keep: list = []
+        self._req = _req(chunk_offsets, chunk_ids, q_offsets, self_offsets, self._keep, layer,
+                         chunk_starts, q_doc_limits)
+        vp = ctypes.c_void_p
+        head = (store.handle, ctypes.byref(self._req), ctypes.c_int32(int(n_q_heads)),
+                vp(_ptr(q)), vp(_ptr(k_self)), vp(_ptr(v_self)), ctypes.c_float(float(softmax_scale)))
+        tail = (vp(_ptr(out)), vp(_ptr(lse)))
+        if decode:
+            self._fn = lib().pic_link_decode
+            self._args = head + (ctypes.c_int32(int(num_splits)),) + tail
+        else:
+            self._fn = lib().pic_link_attn
+            self._args = head + tail
+
+    def __call__(self, stream: Optional[int] = None):
+        if not self._store.handle:
+            raise PicError(ERR_INVALID, "the store is closed")
+        _check(self._fn(*self._args, stream))
 
 
 def link_decode_noalloc(store: Store, chunk_offsets, chunk_ids, q_offsets, self_offsets,

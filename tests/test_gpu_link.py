@@ -162,6 +162,59 @@ def test_small_parity(name):
     run_and_check(SMALL[name])
 
 
+# Small calls (tables as a kernel argument) whose shape the lean kernel is
+# built for (GQA, d_k = d_v in {32, 64, 128} fp32 / {32, 64} bf16, power-of-
+# two query group, at most 256 tiles) run link_lean_kernel; the others keep
+# link_small_kernel. Each case names the kernel it must run.
+LEAN = {
+    "lean_f32_d32_g2": (W.small_config("lean_f32_d32_g2", dtype=W.F32, d_k=32, n_q_heads=4,
+                                       n_kv_heads=2, chunk_lens=(9, 64, 77, 130), batch=3,
+                                       links=(1, 3), q_len=(3, 12, 40), self_len=(3, 20, 70)),
+                        "link_lean_kernel<float>"),
+    "lean_f32_d128_mha": (W.small_config("lean_f32_d128_mha", dtype=W.F32, d_k=128, n_q_heads=4,
+                                         n_kv_heads=4, chunk_lens=(70, 64, 1, 130), batch=2,
+                                         links=(1, 3), q_len=(37, 5), self_len=(41, 5)),
+                          "link_lean_kernel<float>"),
+    "lean_bf16_d32_mqa": (W.small_config("lean_bf16_d32_mqa", d_k=32, n_q_heads=8, n_kv_heads=1,
+                                         chunk_lens=(70, 64, 1, 130), batch=2, links=(1, 3),
+                                         q_len=(19, 2), self_len=(19, 66)),
+                          "link_lean_kernel<bf16>"),
+    "lean_f32_cross_only": (W.small_config("lean_f32_cross_only", dtype=W.F32, d_k=64,
+                                           chunk_lens=(70, 64, 1, 130), batch=2, links=(1, 3),
+                                           q_len=(40, 3), self_len=None),
+                            "link_lean_kernel<float>"),
+    # 2 links of 600 / 700 tokens per request: 22+ tiles per request
+    "lean_f32_split": (W.small_config("lean_f32_split", dtype=W.F32, d_k=64,
+                                      chunk_lens=(600, 700), batch=2, links=(2, 2),
+                                      q_len=(37, 5), self_len=(41, 70)),
+                       "link_lean_kernel<float>"),
+    "lean_bf16_split": (W.small_config("lean_bf16_split", d_k=64, chunk_lens=(600, 700), batch=2,
+                                       links=(2, 2), q_len=(37, 5), self_len=(41, 70)),
+                        "link_lean_kernel<bf16>"),
+    # a group of 3 query heads per kv head: not a power of two
+    "small_f32_group3": (W.small_config("small_f32_group3", dtype=W.F32, d_k=64, n_q_heads=6,
+                                        n_kv_heads=2, chunk_lens=(70, 64, 1, 130), batch=2,
+                                        links=(1, 3), q_len=(37, 5), self_len=(41, 5)),
+                         "link_small_kernel"),
+    # 3 requests x 2 links of 6000 tokens: more tiles than the tile map holds
+    "small_f32_many_tiles": (W.small_config("small_f32_many_tiles", dtype=W.F32, d_k=64,
+                                            chunk_lens=(6000, 5990), batch=3, links=(2, 2),
+                                            q_len=(2, 1, 3), self_len=(2, 1, 3)),
+                             "link_small_kernel"),
+}
+
+
+@pytest.mark.parametrize("name", sorted(LEAN))
+def test_lean_small_calls(name):
+    cfg, kernel = LEAN[name]
+    pic.prof_begin()
+    try:
+        run_and_check(cfg)
+    finally:
+        _, launches, ran = pic.prof_end()
+    assert launches == 1 and (ran == kernel or ran.startswith(kernel + "<")), (launches, ran)
+
+
 # Degenerate requests in one batch: a duplicated link, a request with no
 # query rows, one with own KV only (no links), one linking every chunk.
 DEGENERATE_LINKS = [[2, 0, 2], [1, 3], [], [0, 1, 2, 3], [3, 3]]
