@@ -37,7 +37,7 @@ sys.path.insert(0, ROOT)
 
 PEAK_BF16_TFLOPS = 2500.0     # MI355X dense bf16 matrix peak
 PEAK_HBM_GBS = 8000.0         # MI355X HBM3E
-PEAK_FP32_VALU_TFLOPS = 157.3
+PEAK_FP32_TFLOPS = 157.3       # MI355X fp32: dense matrix and vector (packed) peaks alike
 PROF_EVERY = 5                # timed steps per kernel-timing event pair
 
 # Source file of each attention kernel: a traffic record measured with
@@ -48,6 +48,7 @@ KERNEL_SOURCES = {
     "link_mla_kernel": "kernels_mla.hip",
     "link_valu_kernel": "kernels_generic.hip",
     "link_small_kernel": "kernels_generic.hip",
+    "link_lean_kernel": "kernels_generic.hip",
     "proj_kernel": "kernels_mla_proj.hip",
 }
 PROFILES = os.path.join(ROOT, "profiles")
@@ -433,7 +434,10 @@ def main(argv=None):
     tflops = flops / (step_ms * 1e-3) / 1e12
     gbs = nbytes / (step_ms * 1e-3) / 1e9
     if cfg.dtype == W.F32:
-        bound, peak, unit, achieved = "alu", PEAK_FP32_VALU_TFLOPS, "TFLOP/s", flops / (kern_avg_ms * 1e-3) / 1e12
+        # fp32 products run on the matrix cores in the lean small-call kernel,
+        # on the vector ALUs in the generic ones
+        bound = "mfma" if kname.startswith("link_lean_kernel") else "alu"
+        peak, unit, achieved = PEAK_FP32_TFLOPS, "TFLOP/s", flops / (kern_avg_ms * 1e-3) / 1e12
     elif flops / nbytes < PEAK_BF16_TFLOPS * 1e12 / (PEAK_HBM_GBS * 1e9):
         # below the ridge point (about 312 FLOP/B): decode, and short questions
         # over long documents
@@ -445,7 +449,7 @@ def main(argv=None):
     # clock): the bf16 matrix-core rate with every SIMD busy, and a streaming
     # read of 2 GiB (far beyond the last-level cache).
     measured = None
-    if not args.no_measured_peaks and bound in ("mfma", "hbm"):
+    if not args.no_measured_peaks and bound in ("mfma", "hbm") and cfg.dtype != W.F32:
         if bound == "mfma":
             pic.peak_mfma_bf16(64)
             measured = max(pic.peak_mfma_bf16(256) for _ in range(3))
