@@ -51,6 +51,24 @@ __device__ __forceinline__ void lds_copy16(const void *base, uint32_t records, u
   __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (lds_ptr)dst, 16, voff, 0, 0, 0);
 }
 
+// Stores 16 bytes at base + off bytes with the sc1 (system coherence)
+// cache policy; base must be uniform across the wave and off < 2^31. These
+// kernels write more than they read (the absorption's 38 MB of outputs at
+// 2048 tokens x 16 heads are more than the L2s hold): with the default
+// policy the lines stayed dirty in L2 and their write-back at the end of
+// the kernel held the next launch back; with sc1 they leave as the kernel
+// runs (back to back, absorption 12.4 -> 10.1 us; the up-projection gained
+// only once its stores wrote whole 256-byte rows, 11.0 -> 10.2 us).
+__device__ __forceinline__ void store16_sc1(void *base, uint32_t off, uint4 v) {
+  const uint64_t b = (uint64_t)base;
+  const uint64_t ub = (uint64_t)(uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)b) |
+                      ((uint64_t)(uint32_t)__builtin_amdgcn_readfirstlane((int)(b >> 32)) << 32);
+  const __amdgpu_buffer_rsrc_t rs =
+      __builtin_amdgcn_make_buffer_rsrc((void *)ub, (short)0, 0x7fffffff, 0x00020000);
+  const u32x4 d = {v.x, v.y, v.z, v.w};
+  __builtin_amdgcn_raw_buffer_store_b128(d, rs, (int)off, 0, 16 /* sc1 */);
+}
+
 // Workgroup barrier without the memory fence of __syncthreads (whose release
 // half would wait for every copy and store in flight): this wave's LDS
 // accesses are done, and the empty asm statements keep the compiler from
@@ -261,10 +279,15 @@ __global__ __launch_bounds__(256, 1) void proj_kernel(ProjArgs p) {
         for (int s = 0; s < 8; ++s)
           b[s] = *(const uint4 *)(slot + (t * 16 + ((2 * s + g) ^ (t & 15))) * 16);
       }
+      // the block's output rows start at cb (offsets within a block stay far
+      // below 2^31 bytes)
+      uint16_t *cb = ch + (int64_t)min(tb * 32, last) * p.c_tok;
+      const int brow0 = min(tb * 32, last);
       {
         const uint4 rope = *(const uint4 *)(slot + 8192 + threadIdx.x * 16);
         const int tt = min(tb * 32 + (int)(threadIdx.x >> 3), last);
-        *(uint4 *)(ch + (int64_t)tt * p.c_tok + 512 + (threadIdx.x & 7) * 8) = rope;
+        store16_sc1(cb, (uint32_t)(((int64_t)(tt - brow0) * p.c_tok + 512 + (threadIdx.x & 7) * 8) * 2),
+                    rope);
       }
       f32x16 acc[4];
       products(b, acc);
@@ -283,7 +306,8 @@ __global__ __launch_bounds__(256, 1) void proj_kernel(ProjArgs p) {
       for (int j = 0; j < 8; ++j) {
         const int piece = lane + 64 * j, tok = piece >> 4, nb = (piece & 15) * 8;
         const uint4 v = *(const uint4 *)(mine + tok * kOutRow + nb);
-        *(uint4 *)(ch + (int64_t)min(tb * 32 + tok, last) * p.c_tok + n0 + nb) = v;
+        store16_sc1(cb, (uint32_t)(((int64_t)(min(tb * 32 + tok, last) - brow0) * p.c_tok + n0 + nb) * 2),
+                    v);
       }
       __builtin_amdgcn_wave_barrier();   // reads done before the next block's writes
     };
@@ -314,7 +338,8 @@ __global__ __launch_bounds__(256, 1) void proj_kernel(ProjArgs p) {
     load_a(tb_next, b);
     // partial tiles to LDS as [wave][token][n]; then every thread adds the
     // four partials of 8 consecutive n of one token (2 pieces per thread,
-    // consecutive lanes on consecutive tokens)
+    // 16 consecutive lanes on one token's 256-byte output row, so each
+    // store instruction writes whole rows)
     float *mine = red + wave * 32 * kRedRow;
 #pragma unroll
     for (int nt = 0; nt < 4; ++nt)
@@ -326,7 +351,7 @@ __global__ __launch_bounds__(256, 1) void proj_kernel(ProjArgs p) {
     __syncthreads();
 #pragma unroll
     for (int j = 0; j < 2; ++j) {
-      const int piece = threadIdx.x + 256 * j, tok = piece & 31, nb = (piece >> 5) * 8;
+      const int piece = threadIdx.x + 256 * j, tok = piece >> 4, nb = (piece & 15) * 8;
       float sum[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
@@ -338,8 +363,10 @@ __global__ __launch_bounds__(256, 1) void proj_kernel(ProjArgs p) {
       __bf16 v8[8];
 #pragma unroll
       for (int x = 0; x < 8; ++x) v8[x] = (__bf16)sum[x];
-      *(uint4 *)(ch + (int64_t)min(tb * 32 + tok, last) * p.c_tok + nb) =
-          __builtin_bit_cast(uint4, v8);
+      const int brow0 = min(tb * 32, last);
+      store16_sc1(ch + (int64_t)brow0 * p.c_tok,
+                  (uint32_t)(((int64_t)(min(tb * 32 + tok, last) - brow0) * p.c_tok + nb) * 2),
+                  __builtin_bit_cast(uint4, v8));
     }
     __syncthreads();      // before the next block overwrites the partials
   };
