@@ -230,10 +230,32 @@ __global__ void prep_own_kernel(PrepParams pp) {
   }
   if (R.ls == 0) return;
   if ((int)blockIdx.x < pp.rows_blocks) {
+    // K rows: dst [heads][lp][vpr] from src [token][heads][vpr] in 16-byte
+    // units (zeros past the own rows)
     const int vpr = pp.d_k * pp.esz / 16;
     const uint4 *src = (const uint4 *)pp.k_self;
     uint4 *dst = (uint4 *)L.k;
     const int64_t total = (int64_t)pp.heads * L.lp * vpr;
+    if (total < (int64_t)1 << 31) {
+      // 32-bit index math, and four units per thread loaded before any is
+      // stored, so their latencies overlap
+      const int per_h = L.lp * vpr, n = (int)total;
+      const int stride = pp.rows_blocks * blockDim.x;
+      for (int base = blockIdx.x * blockDim.x + threadIdx.x; base < n; base += 4 * stride) {
+        uint4 v[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          const int idx = min(base + u * stride, n - 1);
+          const int h = idx / per_h, rem = idx - h * per_h, t = rem / vpr, c = rem - t * vpr;
+          v[u] = t < R.ls ? src[((int64_t)(R.s0 + t) * pp.heads + h) * vpr + c]
+                          : make_uint4(0, 0, 0, 0);
+        }
+#pragma unroll
+        for (int u = 0; u < 4; ++u)
+          if (base + u * stride < n) dst[base + u * stride] = make_uint4(v[u].x, v[u].y, v[u].z, v[u].w);
+      }
+      return;
+    }
     for (int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; idx < total;
          idx += (int64_t)pp.rows_blocks * blockDim.x) {
       const int64_t h = idx / ((int64_t)L.lp * vpr);
