@@ -260,14 +260,17 @@ def test_batch_beyond_prologue_arguments(case):
         run_and_check(cfg, decode=True, num_splits=3)
 
 
-@pytest.mark.parametrize("case", ["gqa", "mla"])
+@pytest.mark.parametrize("case", ["gqa", "mla", "f32"])
 def test_empty_key_sets(case):
     """Cross-only attention with a request that links nothing: its rows see no
-    key at all (out = 0, lse = -inf)."""
+    key at all (out = 0, lse = -inf). The f32 case is a small call (lean
+    kernel), whose empty request has no tile in any split."""
     kw = dict(chunk_lens=(70, 64, 129), batch=3, q_len=(4, 6, 2), self_len=None, links=(0, 0))
     if case == "mla":
         cfg = W.small_config("empty_keys_mla", kind=W.MLA, n_q_heads=16, d_k=576, d_v=512,
                              q_std=1.0, scale=1 / math.sqrt(192), **kw)
+    elif case == "f32":
+        cfg = W.small_config("empty_keys_f32", dtype=W.F32, d_k=64, **kw)
     else:
         cfg = W.small_config("empty_keys_gqa", d_k=128, **kw)
     out, lse = run_and_check(cfg, links=[[0, 2], [], [1]])
