@@ -400,6 +400,22 @@ def test_skinny_split_prefill(q_len):
     run_and_check(cfg)
 
 
+# Small calls: one or two requests take up to 32 pieces of 1-4 tiles each (as
+# many as one round of workgroups holds); a ragged batch of eight stops at one
+# round.
+SHORT_CALLS = {
+    "b1_4x512_q16": dict(chunk_lens=(512,) * 8, batch=1, links=(4, 4), q_len=16, self_len=16),
+    "b1_16x1024_q4": dict(chunk_lens=(1024,) * 16, batch=1, links=(16, 16), q_len=4, self_len=4),
+    "b2_16x1024_q32": dict(chunk_lens=(1024,) * 32, batch=2, links=(16, 16), q_len=32, self_len=32),
+    "b8_ragged_q16": dict(chunk_lens=(1024,) * 32, batch=8, links=(8, 16), q_len=16, self_len=16),
+}
+
+
+@pytest.mark.parametrize("name", list(SHORT_CALLS))
+def test_short_call_splits(name):
+    run_and_check(W.small_config(name, d_k=128, **SHORT_CALLS[name]))
+
+
 # ---------------------------------------------------------------------------
 # invariants on the GPU
 
