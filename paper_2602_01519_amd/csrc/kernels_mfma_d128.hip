@@ -54,7 +54,7 @@ constexpr int kWaves = 8;                       // waves (32 rows each) per work
 constexpr int kCopySets = 16 / kWaves;          // 64-chunk copies per lane per K (or V) tile
 constexpr int kRowsPerWave = 32;
 constexpr int kRows = kWaves * kRowsPerWave;
-constexpr float kLazy = 8.0f;
+constexpr float kJumpSum = 18446744073709551616.0f;   // 2^64: redo a tile past it
 constexpr int kQkAhead = 5;    // K-fragment read lead, in QK steps
 constexpr int kPvAhead = 8;    // V-fragment read lead, in PV MFMAs
 
@@ -278,15 +278,42 @@ __device__ __forceinline__ void compute_tile(const Ctx &c, const uint4 *kt, cons
   }
   mask_tile<kLim>(c, s0, s1, ref, lim, dlm);
 
-  float tmax = -INFINITY;
+  // Probabilities against the running max as it stands, and this lane's
+  // (bf16-rounded) sum of them. The tile's own max is only computed when
+  // some lane's sum exceeds 2^64 (a probability could then overflow in a
+  // later sum) or a row with a visible key has no running max yet; the tile
+  // is then redone against the new max.
+  bf16x8 pf[4];
+  const bf16x2 ones = {(__bf16)1.0f, (__bf16)1.0f};
+  auto probs = [&]() {
+    const float neg_m = a.m_used == -INFINITY ? 0.f : -a.m_used;
 #pragma unroll
-  for (int x = 0; x < 16; x += 2) {
-    tmax = fmaxf(fmaxf(tmax, s0[x]), s0[x + 1]);
-    tmax = fmaxf(fmaxf(tmax, s1[x]), s1[x + 1]);
-  }
-  tmax = half_swap_max(tmax);
-  const float mnew = fmaxf(a.m_used, tmax * sc);
-  if (__any(mnew > a.m_used + kLazy)) {
+    for (int x = 0; x < 8; ++x) {
+      pf[0][x] = (__bf16)__builtin_amdgcn_exp2f(__builtin_fmaf(s0[x], sc, neg_m));
+      pf[1][x] = (__bf16)__builtin_amdgcn_exp2f(__builtin_fmaf(s0[8 + x], sc, neg_m));
+      pf[2][x] = (__bf16)__builtin_amdgcn_exp2f(__builtin_fmaf(s1[x], sc, neg_m));
+      pf[3][x] = (__bf16)__builtin_amdgcn_exp2f(__builtin_fmaf(s1[8 + x], sc, neg_m));
+    }
+    float ts = 0.f;
+#pragma unroll
+    for (int ks = 0; ks < 4; ++ks)
+#pragma unroll
+      for (int x = 0; x < 8; x += 2) {
+        const bf16x2 pp = {pf[ks][x], pf[ks][x + 1]};
+        ts = __builtin_amdgcn_fdot2_f32_bf16(pp, ones, ts, false);
+      }
+    return ts;
+  };
+  float ts = probs();
+  if (__any(!(ts <= kJumpSum) || (a.m_used == -INFINITY && ts > 0.f))) {
+    float tmax = -INFINITY;
+#pragma unroll
+    for (int x = 0; x < 16; x += 2) {
+      tmax = fmaxf(fmaxf(tmax, s0[x]), s0[x + 1]);
+      tmax = fmaxf(fmaxf(tmax, s1[x]), s1[x + 1]);
+    }
+    tmax = half_swap_max(tmax);
+    const float mnew = fmaxf(a.m_used, tmax * sc);
     const float alpha = mnew == a.m_used ? 1.f : __builtin_amdgcn_exp2f(a.m_used - mnew);
     a.m_used = mnew;
     a.lsum *= alpha;
@@ -294,24 +321,9 @@ __device__ __forceinline__ void compute_tile(const Ctx &c, const uint4 *kt, cons
     for (int d = 0; d < 4; ++d)
 #pragma unroll
       for (int x = 0; x < 16; ++x) a.o[d][x] *= alpha;
+    ts = probs();
   }
-  const float neg_m = a.m_used == -INFINITY ? 0.f : -a.m_used;
-  bf16x8 pf[4];
-#pragma unroll
-  for (int x = 0; x < 8; ++x) {
-    pf[0][x] = (__bf16)__builtin_amdgcn_exp2f(__builtin_fmaf(s0[x], sc, neg_m));
-    pf[1][x] = (__bf16)__builtin_amdgcn_exp2f(__builtin_fmaf(s0[8 + x], sc, neg_m));
-    pf[2][x] = (__bf16)__builtin_amdgcn_exp2f(__builtin_fmaf(s1[x], sc, neg_m));
-    pf[3][x] = (__bf16)__builtin_amdgcn_exp2f(__builtin_fmaf(s1[8 + x], sc, neg_m));
-  }
-  const bf16x2 ones = {(__bf16)1.0f, (__bf16)1.0f};
-#pragma unroll
-  for (int ks = 0; ks < 4; ++ks)
-#pragma unroll
-    for (int x = 0; x < 8; x += 2) {
-      const bf16x2 pp = {pf[ks][x], pf[ks][x + 1]};
-      a.lsum = __builtin_amdgcn_fdot2_f32_bf16(pp, ones, a.lsum, false);
-    }
+  a.lsum += ts;
 
 #pragma unroll
   for (int ks = 0; ks < 4; ++ks)
