@@ -33,10 +33,13 @@
 // step are 8 consecutive keys: P^T feeds the PV product straight from
 // registers and the V^T fragment for those keys is one 16-byte LDS read.
 //
-// Softmax: log2 domain (scale * log2 e applied by FMA), row max through one
-// cross-half lane swap, and a lazy rescale: the running max used for the
-// exponentials only moves when a row's max grows by more than 8 (p stays
-// <= 2^8), which skips the accumulator rescale on almost every tile. Row
+// Softmax: log2 domain (scale * log2 e applied by FMA). Probabilities are
+// formed against the running max as it stands; only when a lane's share of
+// the tile's row sum exceeds 2^64 (or a row with a visible key has no
+// running max yet, i.e. on its first such tile) does the wave form the
+// tile's row max (one cross-half lane swap), rescale O and the sums, and
+// redo the tile. fp32 and bf16 keep their relative precision at any such
+// magnitude, so almost every tile skips both the max and the rescale. Row
 // sums are kept per lane half (bf16 dot products of the rounded
 // probabilities, i.e. the weights the PV product uses) and added at the end.
 #include "pic_internal.hpp"
@@ -240,8 +243,8 @@ __device__ __forceinline__ void mask_tile(const Ctx &c, f32x16 &s0, f32x16 &s1, 
   }
 }
 
-// One tile: S = K Q^T from kt, mask, online softmax (log2 domain, lazy
-// rescale), O += V^T P^T from vt. In both matrix sections the LDS fragment
+// One tile: S = K Q^T from kt, mask, online softmax (log2 domain, against
+// the running max as it stands), O += V^T P^T from vt. In both matrix sections the LDS fragment
 // reads are issued a few MFMAs ahead of their use (scheduling groups), so an
 // MFMA does not wait on the read issued right before it.
 template <bool kLim, int kAux>
