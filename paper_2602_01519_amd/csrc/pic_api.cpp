@@ -802,20 +802,24 @@ pic_status setup_call(pic_store *s, const pic_link_req *req, int32_t n_q_heads, 
     // 1 for the vector-ALU kernel, whose tiles are slow) and at most 16
     // pieces. A piece of the d=128 matrix-core kernel only has to read more
     // keys and values than the partial results it writes and the merge
-    // reads back (2 x rows x (d_v + 2) fp32), at most 8 tiles; with that
-    // bound it takes up to 32 pieces, which fills the GPU for a single short
-    // request (4 links of 512 tokens, 16 questions: 15 -> 10 us).
+    // reads back (2 x rows x (d_v + 2) fp32), at most 8 tiles; and a d=128
+    // call whose row blocks fill at most half the GPU takes as many pieces
+    // as one round of workgroups holds, up to 32 (a single short request,
+    // 4 links of 512 tokens and 16 questions: 15 -> 10 us), but no more: the
+    // pieces of a second round cost more than they save (8 ragged requests
+    // x 2 kv heads: 16 pieces 28 us, 19 pieces 41 us). Its partials then
+    // stay below 256 x 256 rows x (d_v + 2) fp32 (34 MB).
     const int64_t per_cu =
         kern == Kern::Mla ? 1 : kern == Kern::Mfma128 ? mfma_d128_blocks_per_cu() : 4;
+    const int64_t slots = (int64_t)s->shape.cus * per_cu;
     int min_piece = kern == Kern::Valu ? 1 : 8;
-    int max_splits = 16;
+    int64_t max_splits = 16;
     if (kern == Kern::Mfma128) {
       const int64_t part = 2 * (int64_t)std::min(P.max_rows, rows_per_block) * (d.d_v + 2) * 4;
       const int64_t tile = (int64_t)kTile * (d.d_k + d.d_v) * s->esz;
       min_piece = (int)std::max<int64_t>(1, std::min<int64_t>(8, part / tile));
-      max_splits = 32;
+      if (2 * blocks <= slots) max_splits = std::min<int64_t>(32, slots / blocks);
     }
-    const int64_t slots = (int64_t)s->shape.cus * per_cu;
     int64_t work = 0;   // tiles summed over all non-empty workgroups
     for (const ReqEntry &R : P.reqs) {
       const int64_t rows = (int64_t)R.lq * lp.group;
@@ -823,12 +827,6 @@ pic_status setup_call(pic_store *s, const pic_link_req *req, int32_t n_q_heads, 
     }
     const int64_t per_slot = std::max<int64_t>(min_piece, (work + slots - 1) / slots);
     splits = (int32_t)std::min<int64_t>(max_splits, (P.max_tiles + per_slot - 1) / per_slot);
-    // A d=128 call whose row blocks fill at most half the GPU takes no more
-    // pieces than fit in one round of workgroups: the pieces of a second
-    // round cost more than they save (8 ragged requests x 2 kv heads: 16
-    // pieces 28 us, 19 pieces 41 us).
-    if (kern == Kern::Mfma128 && 2 * blocks <= slots)
-      splits = (int32_t)std::min<int64_t>(splits, slots / blocks);
     splits = std::max(1, std::min(splits, P.max_tiles / min_piece));
   }
   // A small generic call of a shape the lean kernel is built for (tables as
