@@ -416,6 +416,61 @@ def test_short_call_splits(name):
     run_and_check(W.small_config(name, d_k=128, **SHORT_CALLS[name]))
 
 
+# A seeded sweep over shapes the library supports: dtype, GQA or MLA, head
+# widths, query groups (powers of two or not), ragged chunk lengths on and
+# off the 64-key tile boundaries, 0-5 links per request, cross-only calls and
+# decode calls. Each draw lands on whichever kernel the planner picks (lean,
+# small-call, generic, matrix-core d=128 with or without split key ranges,
+# decode, MLA) and is compared with the oracle as every other case.
+def _sweep_config(seed):
+    import random
+    rnd = random.Random(1000 + seed)
+    dtype = W.BF16 if rnd.random() < 0.6 else W.F32
+    if rnd.random() < 0.2:
+        kind, n_kv = W.MLA, 1
+        if dtype == W.BF16:
+            d_k, d_v = rnd.choice([(576, 512), (576, 512), (192, 128)])
+        else:
+            d_k, d_v = 64, 32
+        n_q = rnd.choice([4, 8, 16])
+    else:
+        kind = W.GQA
+        d_k = rnd.choice([32, 64, 128, 128])
+        d_v = d_k if rnd.random() < 0.8 else d_k // 2
+        n_kv = rnd.choice([1, 2, 4])
+        n_q = n_kv * rnd.choice([1, 2, 3, 4, 8])
+    n_chunks = rnd.randint(3, 8)
+    lens = []
+    for _ in range(n_chunks):
+        if rnd.random() < 0.3:
+            lens.append(max(1, 64 * rnd.randint(1, 16) + rnd.choice([-1, 0, 1])))
+        else:
+            lens.append(rnd.randint(1, 1200))
+    batch = rnd.randint(1, 5)
+    lo = rnd.randint(0, 2)
+    hi = min(n_chunks, lo + rnd.randint(0, 3))
+    decode = rnd.random() < 0.25
+    q_len = tuple(rnd.randint(1, 4) if decode else rnd.randint(1, 70) for _ in range(batch))
+    if rnd.random() < 0.2 and hi > 0:
+        self_len = None
+        lo = max(lo, 1)
+    else:
+        self_len = tuple(q + rnd.randint(0, 40) for q in q_len)   # own KV ends with the queries
+    kw = {}
+    if kind == W.MLA:
+        kw = dict(q_std=1.0, scale=1 / math.sqrt(192))
+    return W.small_config(f"sweep{seed}", dtype=dtype, kind=kind, n_q_heads=n_q, n_kv_heads=n_kv,
+                          d_k=d_k, d_v=d_v, chunk_lens=tuple(lens), batch=batch, links=(lo, hi),
+                          q_len=q_len, self_len=self_len, seed=seed, decode=decode, **kw)
+
+
+@pytest.mark.parametrize("seed", range(96))
+def test_random_shapes(seed):
+    cfg = _sweep_config(seed)
+    print(f"sweep {seed}: {cfg}", flush=True)
+    run_and_check(cfg)
+
+
 # ---------------------------------------------------------------------------
 # invariants on the GPU
 
