@@ -44,7 +44,11 @@ def check_bound(gpu, ref, absum, K, label):
 
 @pytest.mark.parametrize("T,H", [(37, 3), (1, 16), (2048, 16), (1541, 16), (300, 64), (1000, 64)])
 def test_absorb_q(T, H):
-    rng = np.random.default_rng(1000 + T + H)
+    absorb_case(T, H, 1000 + T + H)
+
+
+def absorb_case(T, H, seed):
+    rng = np.random.default_rng(seed)
     q = bf16(rng, (T, H, D_NOPE + D_ROPE))
     w = bf16(rng, (H, R_LAT, D_NOPE), 1 / np.sqrt(D_NOPE))
     print(f"case absorb T={T} H={H}", flush=True)
@@ -61,7 +65,11 @@ def test_absorb_q(T, H):
 
 @pytest.mark.parametrize("T,H", [(37, 3), (1, 16), (130, 2), (2048, 16), (1541, 16), (300, 64), (1000, 64)])
 def test_up_v(T, H):
-    rng = np.random.default_rng(2000 + T + H)
+    up_case(T, H, 2000 + T + H)
+
+
+def up_case(T, H, seed):
+    rng = np.random.default_rng(seed)
     o = bf16(rng, (T, H, R_LAT))
     w = bf16(rng, (H, D_V, R_LAT), 1 / np.sqrt(R_LAT))
     print(f"case up T={T} H={H}", flush=True)
@@ -73,6 +81,23 @@ def test_up_v(T, H):
     ref = oracle.mla_up_v(o, w)
     absum = np.einsum("hdr,thr->thd", np.abs(f64(w)), np.abs(f64(o)))
     check_bound(got, ref, absum, R_LAT, f"up {T}x{H}")
+
+
+# Seeded token and head counts: ragged last token blocks, head counts that do
+# and do not divide the XCD count, more heads than CUs per head.
+def _sweep_shape(seed):
+    import random
+    rnd = random.Random(3000 + seed)
+    H = rnd.choice([1, 2, 3, 5, 7, 8, 12, 16, 24, 40])
+    T = rnd.randint(1, min(6000, 16000 // H))
+    return T, H
+
+
+@pytest.mark.parametrize("seed", range(12))
+def test_projection_sweep(seed):
+    T, H = _sweep_shape(seed)
+    absorb_case(T, H, 4000 + seed)
+    up_case(T, H, 5000 + seed)
 
 
 def test_projection_errors_launch_nothing():
