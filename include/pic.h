@@ -259,7 +259,11 @@ pic_status pic_link_decode(pic_store *store, const pic_link_req *req, int32_t n_
  * the call allocates nothing (no hipMalloc, hipFree, pinned staging or
  * event). The host tables are copied with hipMemcpyAsync from pageable
  * memory, which the runtime completes before returning (the host therefore
- * waits for the stream's earlier work). Every kernel writes what it later
+ * waits for the stream's earlier work). Small calls (at most 32 links and 8
+ * requests, no per-query limits, a shape without a matrix-core kernel) run
+ * the kernels pic_link_decode runs for them, which take the tables as a
+ * kernel argument and read the own KV in place: they use the scratch for
+ * split partials only and copy nothing. Every kernel writes what it later
  * reads, so nothing in the scratch has to start at zero.
  * All calls on one GPU share its scratch: calls must not overlap on a GPU
  * (enqueue them on one stream, or order them); calls that overlap race.

@@ -908,19 +908,16 @@ bool small_call(const Setup &C) {
          C.P.reqs.size() <= (size_t)kSmallReqs && C.P.doc_lim.empty();
 }
 
-pic_status small_link_call(pic_store *s, const Setup &C, const void *q, const void *k_self,
-                           const void *v_self, float scale, void *out, float *lse,
-                           hipStream_t st) {
-  const pic_store_desc &d = s->desc;
-  Stage *stage = nullptr;
-  pic_status rc = stage_acquire(s, 0, &stage);
-  if (rc != PIC_OK) return rc;
+// A small call's kernels: the tables go as a kernel argument and the own KV
+// is read in place, so the only device memory besides the caller's tensors
+// is `work` for the split partials (C.part_bytes, unused when not split).
+pic_status launch_small(const pic_store_desc &d, const Setup &C, void *work, const void *q,
+                        const void *k_self, const void *v_self, float scale, void *out,
+                        float *lse, hipStream_t st) {
   LinkParams lp = C.lp;
   if (C.splits > 1) {
-    rc = ensure_work(stage, C.part_bytes);
-    if (rc != PIC_OK) return rc;
     const size_t rows = (size_t)C.P.total_q * lp.n_q_heads;
-    lp.part_o = (float *)stage->work;
+    lp.part_o = (float *)work;
     lp.part_m = lp.part_o + rows * C.splits * d.d_v;
     lp.part_l = lp.part_m + rows * C.splits;
   }
@@ -970,6 +967,21 @@ pic_status small_link_call(pic_store *s, const Setup &C, const void *q, const vo
     e = launch_combine(lp, d.dtype, st);
     if (e != hipSuccess) return hip_fail(e, "combine_kernel");
   }
+  return PIC_OK;
+}
+
+pic_status small_link_call(pic_store *s, const Setup &C, const void *q, const void *k_self,
+                           const void *v_self, float scale, void *out, float *lse,
+                           hipStream_t st) {
+  Stage *stage = nullptr;
+  pic_status rc = stage_acquire(s, 0, &stage);
+  if (rc != PIC_OK) return rc;
+  if (C.splits > 1) {
+    rc = ensure_work(stage, C.part_bytes);
+    if (rc != PIC_OK) return rc;
+  }
+  rc = launch_small(s->desc, C, stage->work, q, k_self, v_self, scale, out, lse, st);
+  if (rc != PIC_OK) return rc;
   HIP_TRY(hipEventRecord(stage->done, st), "hipEventRecord(stage)");
   stage->pending = true;
   return PIC_OK;
@@ -1547,6 +1559,21 @@ pic_status pic_link_decode_noalloc(pic_store *s, const pic_link_req *req, int32_
   rc = check_tensors(s, C.P, q, k_self, v_self, out);
   if (rc != PIC_OK) return rc;
   if (C.P.total_q == 0) return PIC_OK;
+  // A small call runs the kernels pic_link_decode runs for it (tables as a
+  // kernel argument, own KV read in place): the scratch holds only its
+  // split partials.
+  if (small_call(C)) {
+    if (C.part_bytes > kStaticScratchBytes)
+      return fail(PIC_ERR_INVALID,
+                  "the call needs %zu bytes of scratch (split partials); the static scratch "
+                  "holds %zu", C.part_bytes, kStaticScratchBytes);
+    DeviceGuard dg(s->device);
+    if (!dg.ok) return fail(PIC_ERR_HIP, "cannot select the store's device");
+    void *base = nullptr;
+    HIP_TRY(static_scratch(&base), "hipGetSymbolAddress(scratch)");
+    return launch_small(s->desc, C, base, q, k_self, v_self, softmax_scale, out, lse,
+                        (hipStream_t)stream);
+  }
   // scratch layout: [link table][request table][order][per-query limits][workspace]
   Plan &P = C.P;
   const size_t nl = P.links.size(), nr = P.reqs.size();

@@ -15,7 +15,7 @@ import torch
 import oracle
 from paper_2602_01519_amd import pic, runner
 from paper_2602_01519_amd import workloads as W
-from test_gpu_link import compare
+from test_gpu_link import _sweep_config, compare
 
 pytestmark = pytest.mark.gpu
 
@@ -54,6 +54,19 @@ def _run(cfg, splits):
 def test_noalloc_matches_decode_twice_shrinking(splits):
     _run(_case(6, 31), splits)
     _run(_case(3, 32), splits)
+
+
+# The decode-shaped draws of the link tests' seeded sweep (fp32 / bf16, GQA /
+# MLA, several head widths and groups, ragged chunks): each through the entry
+# point twice in a row, against pic_link_decode and the oracle.
+_DECODE_SEEDS = [s for s in range(96) if _sweep_config(s).decode][:12]
+
+
+@pytest.mark.parametrize("seed", _DECODE_SEEDS)
+def test_noalloc_sweep(seed):
+    cfg = _sweep_config(seed)
+    _run(cfg, 0)
+    _run(cfg, 0)
 
 
 def test_noalloc_rejects_a_call_beyond_the_scratch():
