@@ -401,3 +401,53 @@ def test_derive_lifecycle_and_errors():
         assert store.usage()[0] == 9 * 64
     finally:
         store.close()
+
+
+# Per-query limits on the linked rows over the link tests' seeded shapes
+# (every kernel's limit variant: matrix-core d=128 and MLA, generic, decode
+# calls), limits drawn uniformly, increasing with the query token (the
+# CacheBlend pattern) or mostly full, against the oracle.
+def _random_limits(wl, rng):
+    cfg, p = wl.cfg, wl.plan
+    lims = np.zeros(wl.q.shape[0], np.int32)
+    style = rng.integers(0, 3)
+    for r in range(cfg.batch):
+        ld = sum(cfg.chunk_length(int(c))
+                 for c in p.chunk_index[p.chunk_offsets[r]:p.chunk_offsets[r + 1]])
+        q0, q1 = int(p.q_offsets[r]), int(p.q_offsets[r + 1])
+        if style == 0:
+            lims[q0:q1] = rng.integers(0, ld + 1, q1 - q0)
+        elif style == 1:
+            lims[q0:q1] = np.sort(rng.integers(0, ld + 1, q1 - q0))
+        else:
+            lims[q0:q1] = np.where(rng.random(q1 - q0) < 0.8, ld, rng.integers(0, ld + 1, q1 - q0))
+    return lims
+
+
+@pytest.mark.parametrize("seed", range(24))
+def test_random_limits(seed):
+    from test_gpu_link import _sweep_config
+    cfg = _sweep_config(seed)
+    wl = W.make_workload(cfg)
+    lims = _random_limits(wl, np.random.default_rng(7000 + seed))
+    print(f"case limits sweep {seed}: {cfg}", flush=True)
+    p = wl.plan
+    dw = runner.upload(wl)
+    try:
+        args = (dw.store, p.chunk_offsets, wl.link_ids(), p.q_offsets, p.self_offsets,
+                cfg.n_q_heads, dw.q, dw.k_self, dw.v_self, float(np.float32(cfg.scale)), dw.out,
+                dw.lse)
+        if cfg.decode:
+            pic.link_decode(*args, stream=stream(), q_doc_limits=lims)
+        else:
+            pic.link_attn(*args, stream=stream(), q_doc_limits=lims)
+        torch.cuda.synchronize()
+        out, lse = dw.results()
+        links = oracle.workload_links(wl, dict(dw.chunks))
+        ref, ref_lse = oracle.link_attn(
+            dtype=cfg.dtype, mla=cfg.kind == W.MLA, n_q_heads=cfg.n_q_heads, d_v=cfg.d_v,
+            links=links, q=wl.q, q_offsets=p.q_offsets, k_self=wl.k_self, v_self=wl.v_self,
+            self_offsets=p.self_offsets, tau=float(np.float32(cfg.scale)), q_doc_limits=lims)
+        compare(cfg, out, lse, ref, ref_lse, label=f"limits sweep {seed}")
+    finally:
+        dw.close()

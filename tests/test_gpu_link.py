@@ -471,6 +471,17 @@ def test_random_shapes(seed):
     run_and_check(cfg)
 
 
+# Decode-shaped draws with a caller-chosen split count, up to more splits
+# than the request has tiles (empty pieces).
+@pytest.mark.parametrize("seed", [s for s in range(96) if _sweep_config(s).decode][:16])
+def test_random_decode_splits(seed):
+    import random
+    cfg = _sweep_config(seed)
+    splits = random.Random(9000 + seed).choice([1, 2, 5, 16, 64, 256])
+    print(f"sweep {seed}: {cfg} splits {splits}", flush=True)
+    run_and_check(cfg, decode=True, num_splits=splits)
+
+
 # ---------------------------------------------------------------------------
 # invariants on the GPU
 
