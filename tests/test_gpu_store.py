@@ -164,3 +164,51 @@ def test_plan_keeps_its_chunks():
         assert store.usage()[2] == 1
     finally:
         store.close()
+
+
+# Seeded sequences of puts, removals, gathers and links on a small pool
+# (30 pages of 64 tokens, 1 or 2 layers, d 64 or 128), against a host model
+# of the pages in use: a put fits exactly when the free pages (those of
+# removed chunks included, once their readers are done) cover it, chunks
+# may be split over several runs of pages, and every gather is bit-exact and
+# every link matches the oracle.
+@pytest.mark.parametrize("seed", range(4))
+def test_random_put_remove_link(seed):
+    import random
+    rnd = random.Random(500 + seed)
+    n_layers = 1 + seed % 2
+    d = (64, 128)[(seed // 2) % 2]
+    lens = tuple(rnd.randint(1, 500) for _ in range(12))
+    cfg = W.small_config(f"store_rand{seed}", d_k=d, chunk_lens=lens, batch=1, links=(1, 1),
+                         q_len=(29,), self_len=(33,), seed=600 + seed)
+    cap = 30
+    pages = [-(-n // 64) for n in lens]
+    print(f"case store sequence {seed}: layers {n_layers} d {d} lens {lens}", flush=True)
+    store = pic.Store(W.GQA, W.BF16, cfg.n_kv_heads, d, d, cap * 64, n_layers=n_layers)
+    present = {}
+    try:
+        for op in range(40):
+            c = rnd.randrange(len(lens))
+            if c in present and rnd.random() < 0.6:
+                store.remove(W.chunk_id_of(c), stream())
+                del present[c]
+            elif c not in present:
+                torch.cuda.synchronize()            # removed chunks' readers are done
+                free = cap - sum(pages[x] for x in present)
+                if free >= pages[c]:
+                    present[c] = put(store, cfg, c, n_layers)
+                    used = sum(pages[x] for x in present) * 64
+                    assert store.usage() == (used, cap * 64, len(present)), f"op {op}"
+                else:
+                    with pytest.raises(pic.PicError) as e:
+                        put(store, cfg, c, n_layers)
+                    assert e.value.status == pic.ERR_OOM, f"op {op}"
+            assert store.usage()[2] == len(present)
+            if op % 5 == 4 and present:
+                idx = [rnd.choice(sorted(present)) for _ in range(rnd.randint(1, 5))]
+                layer = rnd.randrange(n_layers)
+                host = {x: present[x][layer] for x in present}
+                gather_check(store, cfg, idx, host, layer=layer)
+                link_and_check(store, cfg, idx, host, layer=layer, label=f"seq {seed} op {op}")
+    finally:
+        store.close()
