@@ -798,3 +798,44 @@ def test_cross_and_self_merge_to_the_joint_call(case):
     compare(cfg, merged, merged_lse, ref, ref_lse, label=f"merge {cfg.name}")
     compare(cfg, merged, merged_lse, joint.astype(np.float64), joint_lse,
             label=f"merge vs joint {cfg.name}")
+
+
+# Sub-range links (each link starts at a random multiple of 64 tokens below
+# its chunk's length) over the seeded shapes, against the oracle on the
+# sliced chunks.
+@pytest.mark.parametrize("seed", range(24))
+def test_random_starts(seed):
+    import random
+    rnd = random.Random(8000 + seed)
+    cfg = _sweep_config(seed)
+    wl = W.make_workload(cfg)
+    p = wl.plan
+    starts = np.array([64 * rnd.randint(0, (cfg.chunk_length(int(c)) - 1) // 64)
+                       for c in p.chunk_index], np.int32)
+    print(f"case starts sweep {seed}: {cfg} starts {starts.tolist()}", flush=True)
+    dw = runner.upload(wl)
+    try:
+        args = (dw.store, p.chunk_offsets, wl.link_ids(), p.q_offsets, p.self_offsets,
+                cfg.n_q_heads, dw.q, dw.k_self, dw.v_self, float(np.float32(cfg.scale)), dw.out,
+                dw.lse)
+        stream = torch.cuda.current_stream().cuda_stream
+        if cfg.decode:
+            pic.link_decode(*args, stream=stream, chunk_starts=starts)
+        else:
+            pic.link_attn(*args, stream=stream, chunk_starts=starts)
+        torch.cuda.synchronize()
+        out, lse = dw.results()
+        links = oracle.workload_links(wl, dict(dw.chunks))
+        i = 0
+        for r, l in enumerate(links):
+            for j, (k, v) in enumerate(l):
+                s0 = int(starts[i])
+                l[j] = (k[s0:], None if v is None else v[s0:])
+                i += 1
+        ref, ref_lse = oracle.link_attn(
+            dtype=cfg.dtype, mla=cfg.kind == W.MLA, n_q_heads=cfg.n_q_heads, d_v=cfg.d_v,
+            links=links, q=wl.q, q_offsets=p.q_offsets, k_self=wl.k_self, v_self=wl.v_self,
+            self_offsets=p.self_offsets, tau=float(np.float32(cfg.scale)))
+        compare(cfg, out, lse, ref, ref_lse, label=f"starts sweep {seed}")
+    finally:
+        dw.close()
