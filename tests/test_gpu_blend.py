@@ -451,3 +451,117 @@ def test_random_limits(seed):
         compare(cfg, out, lse, ref, ref_lse, label=f"limits sweep {seed}")
     finally:
         dw.close()
+
+
+# Seeded chains of derived chunks (derive from a base or from a derived
+# chunk, bases removed while derived chunks live, rows written into derived
+# chunks) against a host model of every chunk's content and of the chunks
+# holding each 64-token page: a write is accepted exactly when each of its
+# rows lies on a page only that derived chunk holds, every gather is
+# bit-exact, and links over the live chunks match the oracle.
+@pytest.mark.parametrize("seed", range(6))
+def test_random_derive_chains(seed):
+    import random
+    rnd = random.Random(700 + seed)
+    rng = np.random.default_rng(700 + seed)
+    kind = W.MLA if seed % 2 else W.GQA
+    d_k, d_v = (576, 512) if kind == W.MLA else (128, 128)
+    lens = tuple(rnd.randint(1, 600) for _ in range(3))
+    cfg = W.small_config(f"derive_rand{seed}", kind=kind, d_k=d_k, d_v=d_v, n_q_heads=8,
+                         chunk_lens=lens, batch=1, links=(1, 1), q_len=(9,), self_len=(12,),
+                         seed=710 + seed)
+    print(f"case derive chains {seed}: {'MLA' if kind == W.MLA else 'GQA'} lens {lens}", flush=True)
+    cap = sum(runner.padded(n) for n in lens) + 64 * 8 * 36   # every derive may copy 8 pages
+    store = pic.Store(kind, cfg.dtype, cfg.n_kv_heads, d_k, d_v, cap)
+    chunks = {}         # id -> [k, v, page ids, derived]
+    refs = {}           # page id -> chunks holding it
+    next_page = [0]
+
+    def fresh_page():
+        next_page[0] += 1
+        refs[next_page[0]] = 1
+        return next_page[0]
+
+    def new_rows(n):
+        k = rand_q(cfg, rng, n, heads=cfg.n_kv_heads, std=1.0)
+        v = None if kind == W.MLA else rand_q(cfg, rng, n, heads=cfg.n_kv_heads, width=d_v, std=1.0)
+        return k, v
+
+    def write(cid, rows, expect_ok, op):
+        k_new, v_new = new_rows(len(rows))
+        args = (cid, 0, np.array(rows, np.int32), dev(k_new), None if v_new is None else dev(v_new),
+                stream())
+        if expect_ok:
+            store.write_rows(*args)
+            chunks[cid][0][rows] = k_new
+            if v_new is not None:
+                chunks[cid][1][rows] = v_new
+        else:
+            with pytest.raises(pic.PicError) as e:
+                store.write_rows(*args)
+            assert e.value.status == pic.ERR_INVALID, f"op {op}"
+
+    try:
+        for c in range(3):
+            k, v = W.make_chunk(cfg, c)
+            cid = int(W.chunk_id_of(c))
+            store.put(cid, lens[c], dev(k), None if v is None else dev(v), stream())
+            chunks[cid] = [k, v, [fresh_page() for _ in range(-(-lens[c] // 64))], False]
+        next_id = int(W.chunk_id_of(900))
+        for op in range(36):
+            ids = sorted(chunks)
+            r = rnd.random()
+            if r < 0.35:
+                parent = rnd.choice(ids)
+                pk, pv, ppages, _ = chunks[parent]
+                n = pk.shape[0]
+                rows = sorted(set(rnd.randrange(n) for _ in range(rnd.randint(0, 6)))
+                              | ({0} if rnd.random() < 0.3 else set())
+                              | ({n - 1} if rnd.random() < 0.3 else set()))
+                store.derive(next_id, parent, np.array(rows, np.int32), stream())
+                own = {x // 64 for x in rows}
+                pages = []
+                for i, pg in enumerate(ppages):
+                    if i in own:
+                        pages.append(fresh_page())
+                    else:
+                        refs[pg] += 1
+                        pages.append(pg)
+                chunks[next_id] = [pk.copy(), None if pv is None else pv.copy(), pages, True]
+                next_id += 1
+            elif r < 0.5 and len(chunks) > 1:
+                victim = rnd.choice(ids)
+                store.remove(victim, stream())
+                for pg in chunks[victim][2]:
+                    refs[pg] -= 1
+                del chunks[victim]
+            elif r < 0.75:
+                cid = rnd.choice(ids)
+                n = chunks[cid][0].shape[0]
+                alone = [x for x in range(n)
+                         if chunks[cid][3] and refs[chunks[cid][2][x // 64]] == 1]
+                pool = alone if alone and rnd.random() < 0.6 else range(n)
+                rows = sorted(rnd.sample(pool, rnd.randint(1, min(8, len(pool)))))
+                ok = chunks[cid][3] and all(refs[chunks[cid][2][x // 64]] == 1 for x in rows)
+                write(cid, rows, ok, op)
+            else:
+                cid = rnd.choice(ids)
+                k, v = gather(store, cfg, [cid])
+                assert np.array_equal(k, chunks[cid][0]), f"op {op}: chunk {cid:#x} K"
+                if v is not None:
+                    assert np.array_equal(v, chunks[cid][1]), f"op {op}: chunk {cid:#x} V"
+            if op % 6 == 5:
+                ids = sorted(chunks)
+                pick = [rnd.choice(ids) for _ in range(rnd.randint(1, 4))]
+                q = rand_q(cfg, rng, 9)
+                ks, vs = new_rows(12)
+                so = np.array([0, 12], np.int32)
+                qo = np.array([0, 9], np.int32)
+                co = np.array([0, len(pick)], np.int32)
+                out, lse = run_link(store, cfg, co, pick, qo, so, q, ks, vs)
+                ref, ref_lse = ref_link(cfg, [[(chunks[i][0], chunks[i][1]) for i in pick]], q, qo,
+                                        ks, vs, so)
+                compare(cfg, out, lse, ref, ref_lse, label=f"derive chains {seed} op {op}")
+        assert store.usage()[2] == len(chunks)
+    finally:
+        store.close()
