@@ -176,3 +176,33 @@ def test_decode_plan_cross_only_every_layer(splits):
     finally:
         plan.close()
         store.close()
+
+
+# Link plans over the link tests' seeded shapes (prefill and decode plans, every
+# kernel choice, cross-only calls): one plan per shape on a two-layer store,
+# run on both layers, each run against the oracle on that layer's caches.
+@pytest.mark.parametrize("seed", range(24))
+def test_random_plans(seed):
+    from test_gpu_link import _sweep_config
+    cfg = _sweep_config(seed)
+    wl = W.make_workload(cfg)
+    print(f"case plan sweep {seed}: {cfg}", flush=True)
+    store, per_layer = layered_store(cfg, wl, n_layers=2)
+    p = wl.plan
+    plan = pic.LinkPlan(store, p.chunk_offsets, wl.link_ids(), p.q_offsets, p.self_offsets,
+                        cfg.n_q_heads, mode=pic.DECODE if cfg.decode else pic.PREFILL)
+    try:
+        stream = torch.cuda.current_stream().cuda_stream
+        q = runner.to_device(wl.q, "cuda")
+        ks = None if wl.k_self is None else runner.to_device(wl.k_self, "cuda")
+        vs = None if wl.v_self is None else runner.to_device(wl.v_self, "cuda")
+        for layer in (1, 0):
+            out, lse = outputs(cfg, wl.q.shape[0])
+            plan.run(layer, q, ks, vs, float(np.float32(cfg.scale)), out, lse, stream=stream)
+            torch.cuda.synchronize()
+            ref, ref_lse = oracle.run_workload(wl, per_layer[layer])
+            compare(cfg, runner.to_host(out, cfg.dtype), lse.cpu().numpy().astype(np.float64), ref,
+                    ref_lse, label=f"plan sweep {seed} layer {layer}")
+    finally:
+        plan.close()
+        store.close()
