@@ -287,10 +287,10 @@ pic_status pic_link_decode_noalloc(pic_store *store, const pic_link_req *req, in
  * pic_link_plan_create: req as for pic_link_attn (req->layer must be 0);
  *   mode PIC_PREFILL (num_splits must be 0) computes as pic_link_attn,
  *   PIC_DECODE as pic_link_decode with the given num_splits (0 = auto),
- *   with the same kernel and split choice except for small calls (at most
- *   32 links and 8 requests on the generic kernel): the direct calls pass
- *   their tables as a kernel argument, a plan runs the general kernels from
- *   its device tables, so results agree to rounding, not bit for bit.
+ *   with the same kernels and split choice, so a run returns the bits the
+ *   direct call returns (small calls, at most 32 links and 8 requests on
+ *   the generic kernel, pass the tables as a kernel argument from the
+ *   plan's host copy of each layer's table, as the direct calls do).
  *   Blocking: copies the tables to the device before returning. The plan
  *   keeps no pointer into req; the store must outlive it
  *   (pic_store_destroy refuses while plans are alive).

@@ -911,9 +911,11 @@ bool small_call(const Setup &C) {
 // A small call's kernels: the tables go as a kernel argument and the own KV
 // is read in place, so the only device memory besides the caller's tensors
 // is `work` for the split partials (C.part_bytes, unused when not split).
-pic_status launch_small(const pic_store_desc &d, const Setup &C, void *work, const void *q,
-                        const void *k_self, const void *v_self, float scale, void *out,
-                        float *lse, hipStream_t st) {
+// links: host, C.P.links.size() entries (C.P.links, or a plan's for one
+// layer).
+pic_status launch_small(const pic_store_desc &d, const Setup &C, const LinkEntry *links,
+                        void *work, const void *q, const void *k_self, const void *v_self,
+                        float scale, void *out, float *lse, hipStream_t st) {
   LinkParams lp = C.lp;
   if (C.splits > 1) {
     const size_t rows = (size_t)C.P.total_q * lp.n_q_heads;
@@ -937,14 +939,14 @@ pic_status launch_small(const pic_store_desc &d, const Setup &C, void *work, con
   if (C.lean) {
     LeanTabs t;
     memset(&t, 0, sizeof(t));
-    std::copy(C.P.links.begin(), C.P.links.end(), t.links);
+    std::copy(links, links + C.P.links.size(), t.links);
     int32_t base = 0;
     for (size_t i = 0; i < C.P.order.size(); ++i) {
       const ReqEntry &R = C.P.reqs[C.P.order[i]];
       t.reqs[i] = R;
       t.tile_base[i] = base;
       for (int32_t k = 0; k < R.nlinks; ++k) {
-        const LinkEntry &L = C.P.links[R.link0 + k];
+        const LinkEntry &L = links[R.link0 + k];
         const int32_t n = (L.len + kTile - 1) / kTile;
         for (int32_t j = 0; j < n; ++j) t.tile_link[base + L.tile0 + j] = (uint8_t)k;
       }
@@ -955,7 +957,7 @@ pic_status launch_small(const pic_store_desc &d, const Setup &C, void *work, con
   } else {
     SmallTabs t;
     memset(&t, 0, sizeof(t));
-    std::copy(C.P.links.begin(), C.P.links.end(), t.links);
+    std::copy(links, links + C.P.links.size(), t.links);
     std::copy(C.P.reqs.begin(), C.P.reqs.end(), t.reqs);
     std::copy(C.P.order.begin(), C.P.order.end(), t.order);
     prof_start(st, &ev);
@@ -980,7 +982,8 @@ pic_status small_link_call(pic_store *s, const Setup &C, const void *q, const vo
     rc = ensure_work(stage, C.part_bytes);
     if (rc != PIC_OK) return rc;
   }
-  rc = launch_small(s->desc, C, stage->work, q, k_self, v_self, scale, out, lse, st);
+  rc = launch_small(s->desc, C, C.P.links.data(), stage->work, q, k_self, v_self, scale, out,
+                    lse, st);
   if (rc != PIC_OK) return rc;
   HIP_TRY(hipEventRecord(stage->done, st), "hipEventRecord(stage)");
   stage->pending = true;
@@ -1035,6 +1038,11 @@ struct pic_link_plan {
   size_t off_r = 0, off_o = 0;   // request / order tables within a layer's tables
   size_t off_d = 0;              // per-query limits (if any) within a layer's tables
   void *work = nullptr;          // inside dev
+  // small calls (see small_call): every layer's link table on the host,
+  // [layer][link], run by the small-call kernels as pic_link_attn /
+  // pic_link_decode run them (tables as a kernel argument)
+  bool small = false;
+  std::vector<LinkEntry> small_links;
 };
 
 extern "C" {
@@ -1571,8 +1579,8 @@ pic_status pic_link_decode_noalloc(pic_store *s, const pic_link_req *req, int32_
     if (!dg.ok) return fail(PIC_ERR_HIP, "cannot select the store's device");
     void *base = nullptr;
     HIP_TRY(static_scratch(&base), "hipGetSymbolAddress(scratch)");
-    return launch_small(s->desc, C, base, q, k_self, v_self, softmax_scale, out, lse,
-                        (hipStream_t)stream);
+    return launch_small(s->desc, C, C.P.links.data(), base, q, k_self, v_self, softmax_scale,
+                        out, lse, (hipStream_t)stream);
   }
   // scratch layout: [link table][request table][order][per-query limits][workspace]
   Plan &P = C.P;
@@ -1656,6 +1664,21 @@ pic_status pic_link_plan_create(pic_store *s, const pic_link_req *req, int32_t n
       return hip_fail(e, "hipMalloc(plan)");
     }
     pl->work = (char *)pl->dev + tables;
+    pl->small = small_call(pl->C);
+    if (pl->small) {
+      pl->small_links.resize((size_t)s->n_layers * nl);
+      std::vector<bool> own_link(nl, false);
+      for (auto &o : P.own) own_link[o.first] = true;
+      for (int32_t l = 0; l < s->n_layers; ++l)
+        for (size_t i = 0; i < nl; ++i) {
+          LinkEntry E = P.links[i];
+          if (!own_link[i]) {
+            E.k = (const char *)E.k + (int64_t)l * s->layer_bytes;
+            E.v = (const char *)E.v + (int64_t)l * s->layer_bytes;
+          }
+          pl->small_links[(size_t)l * nl + i] = E;
+        }
+    }
     // Every layer's tables differ only in the chunk links' addresses: layer
     // l of a slot sits l pool layers further on; own-KV links point at the
     // plan's workspace in every layer.
@@ -1707,6 +1730,11 @@ pic_status pic_link_plan_run(pic_link_plan *pl, int32_t layer, const void *q, co
   if (pl->C.P.total_q == 0) return PIC_OK;
   DeviceGuard dg(s->device);
   if (!dg.ok) return fail(PIC_ERR_HIP, "cannot select the store's device");
+  if (pl->small)
+    return launch_small(s->desc, pl->C,
+                        pl->small_links.data() + (size_t)layer * pl->C.P.links.size(),
+                        (char *)pl->work + pl->C.part_off, q, k_self, v_self, softmax_scale, out,
+                        lse, (hipStream_t)stream);
   LinkParams lp = pl->C.lp;
   const char *t = (const char *)pl->dev + (size_t)layer * pl->table_bytes;
   lp.links = (const LinkEntry *)t;
