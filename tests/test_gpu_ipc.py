@@ -21,6 +21,10 @@ CASES = {
     "gqa": W.small_config("ipc_gqa", d_k=128, n_q_heads=8, n_kv_heads=2,
                           chunk_lens=(70, 64, 1, 130, 300), batch=3, links=(2, 4),
                           q_len=(37, 5, 16), self_len=(41, 5, 16), seed=41),
+    # a small call (tables as a kernel argument, the lean kernel) on the imported store
+    "gqa_small": W.small_config("ipc_small", d_k=64, n_q_heads=8, n_kv_heads=2,
+                                chunk_lens=(70, 64, 1, 130), batch=2, links=(1, 3),
+                                q_len=(9, 3), self_len=(12, 3), seed=45),
     "mla": W.small_config("ipc_mla", kind=W.MLA, n_q_heads=16, d_k=576, d_v=512,
                           chunk_lens=(70, 64, 130), batch=2, links=(1, 3), q_len=(9, 4),
                           self_len=(9, 6), q_std=1.0, scale=1 / math.sqrt(192), seed=43),
