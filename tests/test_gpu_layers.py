@@ -180,8 +180,8 @@ def test_decode_plan_cross_only_every_layer(splits):
 
 # Link plans over the link tests' seeded shapes (prefill and decode plans, every
 # kernel choice, cross-only calls): one plan per shape on a two-layer store,
-# run on both layers, each run against the oracle on that layer's caches, and
-# the last (layer 0) bit for bit against the direct call.
+# run on both layers, each run against the oracle on that layer's caches and
+# bit for bit against the direct call on that layer.
 @pytest.mark.parametrize("seed", range(24))
 def test_random_plans(seed):
     from test_gpu_link import _sweep_config
@@ -204,16 +204,17 @@ def test_random_plans(seed):
             ref, ref_lse = oracle.run_workload(wl, per_layer[layer])
             compare(cfg, runner.to_host(out, cfg.dtype), lse.cpu().numpy().astype(np.float64), ref,
                     ref_lse, label=f"plan sweep {seed} layer {layer}")
-        # the direct call on layer 0 returns the same bits (same kernels and splits)
-        out2, lse2 = outputs(cfg, wl.q.shape[0])
-        args = (store, p.chunk_offsets, wl.link_ids(), p.q_offsets, p.self_offsets, cfg.n_q_heads,
-                q, ks, vs, float(np.float32(cfg.scale)), out2, lse2)
-        if cfg.decode:
-            pic.link_decode(*args, stream=stream)
-        else:
-            pic.link_attn(*args, stream=stream)
-        torch.cuda.synchronize()
-        assert torch.equal(out, out2) and torch.equal(lse, lse2), "plan and direct call differ"
+            # the direct call on the same layer returns the same bits (same kernels and splits)
+            out2, lse2 = outputs(cfg, wl.q.shape[0])
+            args = (store, p.chunk_offsets, wl.link_ids(), p.q_offsets, p.self_offsets,
+                    cfg.n_q_heads, q, ks, vs, float(np.float32(cfg.scale)), out2, lse2)
+            if cfg.decode:
+                pic.link_decode(*args, stream=stream, layer=layer)
+            else:
+                pic.link_attn(*args, stream=stream, layer=layer)
+            torch.cuda.synchronize()
+            assert torch.equal(out, out2) and torch.equal(lse, lse2), \
+                f"layer {layer}: plan and direct call differ"
     finally:
         plan.close()
         store.close()
