@@ -1650,8 +1650,25 @@ pic_status pic_link_plan_create(pic_store *s, const pic_link_req *req, int32_t n
   pl->off_o = pl->off_r + round_up(sizeof(ReqEntry) * nr, 256);
   pl->off_d = pl->off_o + round_up(sizeof(int32_t) * nr, 256);
   pl->table_bytes = round_up(pl->off_d + sizeof(int32_t) * P.doc_lim.size(), 256);
-  const size_t tables = pl->table_bytes * s->n_layers;
-  const size_t bytes = tables + pl->C.work_bytes();
+  // A small call keeps its tables on the host (one per layer) and needs
+  // device memory for its split partials only.
+  pl->small = small_call(pl->C);
+  if (pl->small) {
+    pl->small_links.resize((size_t)s->n_layers * nl);
+    std::vector<bool> own_link(nl, false);
+    for (auto &o : P.own) own_link[o.first] = true;
+    for (int32_t l = 0; l < s->n_layers; ++l)
+      for (size_t i = 0; i < nl; ++i) {
+        LinkEntry E = P.links[i];
+        if (!own_link[i]) {
+          E.k = (const char *)E.k + (int64_t)l * s->layer_bytes;
+          E.v = (const char *)E.v + (int64_t)l * s->layer_bytes;
+        }
+        pl->small_links[(size_t)l * nl + i] = E;
+      }
+  }
+  const size_t tables = pl->small ? 0 : pl->table_bytes * s->n_layers;
+  const size_t bytes = pl->small ? pl->C.part_bytes : tables + pl->C.work_bytes();
   if (bytes > 0) {
     DeviceGuard dg(s->device);
     if (!dg.ok) {
@@ -1664,20 +1681,13 @@ pic_status pic_link_plan_create(pic_store *s, const pic_link_req *req, int32_t n
       return hip_fail(e, "hipMalloc(plan)");
     }
     pl->work = (char *)pl->dev + tables;
-    pl->small = small_call(pl->C);
-    if (pl->small) {
-      pl->small_links.resize((size_t)s->n_layers * nl);
-      std::vector<bool> own_link(nl, false);
-      for (auto &o : P.own) own_link[o.first] = true;
-      for (int32_t l = 0; l < s->n_layers; ++l)
-        for (size_t i = 0; i < nl; ++i) {
-          LinkEntry E = P.links[i];
-          if (!own_link[i]) {
-            E.k = (const char *)E.k + (int64_t)l * s->layer_bytes;
-            E.v = (const char *)E.v + (int64_t)l * s->layer_bytes;
-          }
-          pl->small_links[(size_t)l * nl + i] = E;
-        }
+  }
+  if (bytes > 0 && !pl->small) {
+    DeviceGuard dg(s->device);
+    if (!dg.ok) {
+      (void)hipFree(pl->dev);
+      delete pl;
+      return fail(PIC_ERR_HIP, "cannot select the store's device");
     }
     // Every layer's tables differ only in the chunk links' addresses: layer
     // l of a slot sits l pool layers further on; own-KV links point at the
@@ -1702,7 +1712,7 @@ pic_status pic_link_plan_create(pic_store *s, const pic_link_req *req, int32_t n
       if (!P.doc_lim.empty())
         memcpy(h + pl->off_d, P.doc_lim.data(), sizeof(int32_t) * P.doc_lim.size());
     }
-    e = hipMemcpy(pl->dev, host.data(), tables, hipMemcpyHostToDevice);
+    hipError_t e = hipMemcpy(pl->dev, host.data(), tables, hipMemcpyHostToDevice);
     if (e != hipSuccess) {
       (void)hipFree(pl->dev);
       delete pl;
@@ -1733,8 +1743,8 @@ pic_status pic_link_plan_run(pic_link_plan *pl, int32_t layer, const void *q, co
   if (pl->small)
     return launch_small(s->desc, pl->C,
                         pl->small_links.data() + (size_t)layer * pl->C.P.links.size(),
-                        (char *)pl->work + pl->C.part_off, q, k_self, v_self, softmax_scale, out,
-                        lse, (hipStream_t)stream);
+                        pl->work, q, k_self, v_self, softmax_scale, out, lse,
+                        (hipStream_t)stream);
   LinkParams lp = pl->C.lp;
   const char *t = (const char *)pl->dev + (size_t)layer * pl->table_bytes;
   lp.links = (const LinkEntry *)t;
